@@ -1,0 +1,181 @@
+"""CPU oracle for QUASAR's per-step reconstruction -- TEST INFRASTRUCTURE ONLY.
+
+A ctypes wrapper around ``liboracle.so`` (plain C, see ``quasar_oracle.c``).
+Only the test suite, ``__graft_entry__.smoke()`` and the benchmark's
+``cpu_baseline`` leg may import this package; the GPU library never does, and
+this package never imports the GPU library.
+
+Inputs are numpy arrays on the host:
+  W  float32 [R, C], or uint16 [R, C] holding bf16 bit patterns
+  v  float32 [R, C] saliency (read only; the EMA result is returned)
+  g  optional gradient, float32 or uint16 (bf16 bits)
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import threading
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+from . import build as _build
+
+MAX_CLIPS = 16
+MAX_GROUP = 256
+
+
+class _Desc(C.Structure):
+    _fields_ = [
+        ("rows", C.c_int64), ("cols", C.c_int64),
+        ("w_bf16", C.c_int), ("nvfp4", C.c_int), ("bits", C.c_int), ("group", C.c_int),
+        ("clips", C.POINTER(C.c_float)), ("n_clips", C.c_int),
+        ("g_bf16", C.c_int), ("beta2", C.c_float), ("fp32_mode", C.c_int),
+    ]
+
+
+_lib = None
+_lock = threading.Lock()
+
+
+def lib():
+    """Load (building first if needed) the oracle shared library."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(_build.LIB):
+                _build.build()
+            L = C.CDLL(_build.LIB)
+            vp = C.c_void_p
+            L.qor_reconstruct.argtypes = [C.POINTER(_Desc), C.c_int64, C.c_int64, vp, vp, vp, C.c_float,
+                                          vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+            L.qor_reconstruct.restype = C.c_int
+            L.qor_absmax.argtypes = [vp, C.c_int, C.c_int64]
+            L.qor_absmax.restype = C.c_float
+            L.qor_pack_group.argtypes = [vp, C.c_int, C.c_int, vp]
+            L.qor_unpack_group.argtypes = [vp, C.c_int, C.c_int, vp]
+            L.qor_e2m1_code.argtypes = [C.c_float]
+            L.qor_e2m1_code.restype = C.c_int
+            L.qor_e4m3_code.argtypes = [C.c_double]
+            L.qor_e4m3_code.restype = C.c_int
+            L.qor_e4m3_value.argtypes = [C.c_int]
+            L.qor_e4m3_value.restype = C.c_double
+            L.qor_f32_to_bf16.argtypes = [C.c_float]
+            L.qor_f32_to_bf16.restype = C.c_uint16
+            _lib = L
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(C.c_void_p)
+
+
+def absmax(W: np.ndarray) -> float:
+    W = np.ascontiguousarray(W)
+    return float(lib().qor_absmax(_ptr(W), int(W.dtype == np.uint16), W.size))
+
+
+def reconstruct(W, v, *, fmt="int", bits=4, group=128, clips=(1.0,), g=None, beta2=0.999,
+                tensor_amax=None, fp32_mode=False, want_scores=False, want_diag=False,
+                n_threads=1) -> dict:
+    """Run the oracle over the whole of W.
+
+    Returns a dict with: ``codes`` (unpacked, one per element), ``codes_packed``,
+    ``r`` (W's dtype), ``best`` (u8 per group), ``err`` (fp32 per group), ``v_out``
+    (when g is given), ``scale``/``zero`` (INT) or ``e4m3`` and ``tensor_scale``
+    (NVFP4), and optionally ``scores`` [groups, K] and ``diag`` [groups, 4].
+    """
+    W = np.ascontiguousarray(W)
+    v = np.ascontiguousarray(v, dtype=np.float32)
+    if W.dtype not in (np.float32, np.uint16):
+        raise TypeError("W must be float32 or uint16 (bf16 bits)")
+    R, Cc = W.shape
+    if v.shape != W.shape:
+        raise ValueError("v shape")
+    nv = fmt == "nvfp4"
+    G = 16 if nv else int(group)
+    nb = 4 if nv else int(bits)
+    if Cc % G != 0:
+        raise ValueError("cols % group != 0")
+    clips_a = np.ascontiguousarray(np.asarray(clips, dtype=np.float32))
+    K = clips_a.size
+    ngroups = R * Cc // G
+    if g is not None:
+        g = np.ascontiguousarray(g)
+        if g.shape != W.shape:
+            raise ValueError("g shape")
+    d = _Desc(R, Cc, int(W.dtype == np.uint16), int(nv), nb, G,
+              clips_a.ctypes.data_as(C.POINTER(C.c_float)), K,
+              int(g is not None and g.dtype == np.uint16), float(beta2), int(bool(fp32_mode)))
+    out = {
+        "codes": np.zeros(R * Cc, np.uint8),
+        "codes_packed": np.zeros(ngroups * G * nb // 8, np.uint8),
+        "r": np.zeros((R, Cc), W.dtype),
+        "best": np.zeros(ngroups, np.uint8),
+        "err": np.zeros(ngroups, np.float32),
+    }
+    out["v_out"] = np.zeros_like(v) if g is not None else None
+    if nv:
+        out["e4m3"] = np.zeros(ngroups, np.uint8)
+        amax = absmax(W) if tensor_amax is None else float(tensor_amax)
+        out["tensor_amax"] = np.float32(amax)
+        out["tensor_scale"] = np.float32(np.float32(amax) / np.float32(2688.0))
+    else:
+        out["scale"] = np.zeros(ngroups, np.float32)
+        out["zero"] = np.zeros(ngroups, np.float32)
+        amax = 0.0
+    out["scores"] = np.zeros((ngroups, K), np.float64) if want_scores else None
+    out["diag"] = np.zeros((ngroups, 4), np.float64) if want_diag else None
+    L = lib()
+
+    def run(r0, r1):
+        rc = L.qor_reconstruct(C.byref(d), r0, r1, _ptr(W), _ptr(v), _ptr(g), C.c_float(amax),
+                               _ptr(out["v_out"]), _ptr(out["codes_packed"]), _ptr(out["codes"]),
+                               _ptr(out.get("scale")), _ptr(out.get("zero")), _ptr(out.get("e4m3")),
+                               _ptr(out["r"]), _ptr(out["best"]), _ptr(out["err"]),
+                               _ptr(out["scores"]), _ptr(out["diag"]))
+        if rc != 0:
+            raise ValueError(f"oracle rejected the descriptor (status {rc})")
+
+    n_threads = max(1, int(n_threads))
+    if n_threads == 1 or R < 2:
+        run(0, R)
+    else:
+        bounds = np.linspace(0, R, n_threads + 1).astype(np.int64)
+        with ThreadPoolExecutor(n_threads) as ex:
+            list(ex.map(lambda i: run(int(bounds[i]), int(bounds[i + 1])), range(n_threads)))
+    out["codes"] = out["codes"].reshape(R, Cc)
+    return out
+
+
+def pack_group(codes: np.ndarray, bits: int) -> np.ndarray:
+    codes = np.ascontiguousarray(codes, dtype=np.uint8)
+    out = np.zeros(codes.size * bits // 8, np.uint8)
+    lib().qor_pack_group(_ptr(codes), codes.size, bits, _ptr(out))
+    return out
+
+
+def unpack_group(packed: np.ndarray, n: int, bits: int) -> np.ndarray:
+    packed = np.ascontiguousarray(packed, dtype=np.uint8)
+    out = np.zeros(n, np.uint8)
+    lib().qor_unpack_group(_ptr(packed), n, bits, _ptr(out))
+    return out
+
+
+def e2m1_code(y: float) -> int:
+    return int(lib().qor_e2m1_code(float(y)))
+
+
+def e4m3_code(x: float) -> int:
+    return int(lib().qor_e4m3_code(float(x)))
+
+
+def e4m3_value(code: int) -> float:
+    return float(lib().qor_e4m3_value(int(code)))
+
+
+def f32_to_bf16(x: float) -> int:
+    return int(lib().qor_f32_to_bf16(float(x)))
+
+
+E2M1_MAGNITUDES = (0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0)

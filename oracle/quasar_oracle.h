@@ -1,0 +1,64 @@
+/*
+ * quasar_oracle.h -- TEST INFRASTRUCTURE ONLY (see quasar_oracle.c).
+ *
+ * The oracle's own interface.  It is deliberately separate from the GPU
+ * library's header: the two implementations share no declarations.
+ * All pointers are host pointers.
+ */
+#ifndef QUASAR_ORACLE_H
+#define QUASAR_ORACLE_H
+
+#include <stdint.h>
+
+#define QOR_MAX_GROUP 256
+#define QOR_MAX_CLIPS 16
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct {
+  int64_t rows, cols;  /* W is [rows, cols] row-major; groups run along a row */
+  int w_bf16;          /* 1: W and r hold bf16 bit patterns; 0: fp32 */
+  int nvfp4;           /* 0: asymmetric INT-b groups; 1: NVFP4 16-blocks */
+  int bits;            /* INT: 2, 3 or 4 */
+  int group;           /* INT: group size (divides cols); ignored for NVFP4 */
+  const float* clips;  /* n_clips clip factors in (0, 1]; order = tie-break */
+  int n_clips;         /* 1..QOR_MAX_CLIPS */
+  int g_bf16;          /* gradient dtype when g != NULL: 1 bf16, 0 fp32 */
+  float beta2;         /* EMA decay when g != NULL */
+  int fp32_mode;       /* 1: literal fp32 accumulation (diagnostic) */
+} qor_desc;
+
+/* Reconstruct rows [row0, row1).  Outputs are whole-tensor arrays indexed by
+ * global element / group id; any output pointer may be NULL.
+ *   v_out          [rows*cols] EMA result (only written when g != NULL)
+ *   codes_packed   packed codes (layout in quasar_oracle.c)
+ *   codes_unpacked [rows*cols] one code per byte
+ *   scale, zero    [groups] fp32 (INT)
+ *   e4m3           [groups] E4M3 block-scale byte (NVFP4)
+ *   r              [rows*cols] in W's dtype
+ *   best_clip      [groups]; err [groups] = score of the chosen candidate
+ *   scores         [groups * n_clips] every candidate's score (fp64)
+ *   diag           [groups * 4]: {standard-QAT score, score of clip 0,
+ *                   NVFP4 ratio s_star / S_t of the chosen clip, INT degenerate flag}
+ * tensor_amax is used only for NVFP4 (tensor scale = amax / 2688).
+ * Returns 0, or a negative value for an invalid descriptor. */
+int qor_reconstruct(const qor_desc* d, int64_t row0, int64_t row1, const void* W, const float* v,
+                    const void* g, float tensor_amax, float* v_out, uint8_t* codes_packed,
+                    uint8_t* codes_unpacked, float* scale, float* zero, uint8_t* e4m3, void* r,
+                    uint8_t* best_clip, float* err, double* scores, double* diag);
+
+float qor_absmax(const void* W, int w_bf16, int64_t n);
+void qor_pack_group(const uint8_t* codes, int n, int bits, uint8_t* out);
+void qor_unpack_group(const uint8_t* in, int n, int bits, uint8_t* codes);
+int qor_e2m1_code(float y);
+int qor_e4m3_code(double x);
+double qor_e4m3_value(int code);
+uint16_t qor_f32_to_bf16(float f);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif

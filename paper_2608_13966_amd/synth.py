@@ -1,0 +1,130 @@
+"""Seeded synthetic workloads for the reconstruction path.
+
+This module only draws inputs; it holds none of the method's arithmetic.  Both
+the GPU path and the CPU oracle are fed from it, so the two always see the same
+bytes (each parity test generates once and hands the same arrays to both).
+
+Recipe per weight matrix W [out, in] (groups run along ``in``), drawn in this
+fixed order from one ``torch.Generator`` seeded with the matrix seed:
+  1. W0 ~ N(0, 0.02^2), fp32
+  2. four outlier input columns (random permutation, first four); W[:, j] *= 10
+  3. row_sigma = exp(N(0, 1))   [out]
+  4. col_sigma = exp(N(0, 1))   [in]
+  5. z ~ N(0, 1) [out, in];  v = (z * row_sigma[i] * col_sigma[j])^2, fp32
+  6. with a fused EMA: g ~ N(0, 1e-3^2), rounded to bf16
+  7. bf16 workloads round W to bf16 (round-to-nearest-even).
+Outlier columns widen the range of the groups that contain them (the case in
+which a clip factor below 1 wins); the saliency spans many orders of magnitude
+inside a group, as the diagonal-Fisher estimate does on real layers.
+
+Seeds: a single matrix uses seed 0; in a layer set, matrix m (order q, k, v, o,
+gate, up, down) of layer l uses seed 1000*l + m.  The generator of a device
+gives a device-specific stream: a workload generated on the GPU is copied to
+the host for the oracle, never regenerated there.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+import torch
+
+LAYER_ORDER = ("q", "k", "v", "o", "gate", "up", "down")
+
+# [out, in] shapes of one transformer layer's linear projections
+QWEN3_0_6B = {"q": (2048, 1024), "k": (1024, 1024), "v": (1024, 1024), "o": (1024, 2048),
+              "gate": (3072, 1024), "up": (3072, 1024), "down": (1024, 3072)}
+LLAMA31_8B = {"q": (4096, 4096), "k": (1024, 4096), "v": (1024, 4096), "o": (4096, 4096),
+              "gate": (14336, 4096), "up": (14336, 4096), "down": (4096, 14336)}
+
+
+def clip_grid(hi: float, lo: float, n: int) -> np.ndarray:
+    """``n`` clip factors from ``hi`` down to ``lo`` (fp64 linspace, then fp32)."""
+    return np.linspace(hi, lo, n).astype(np.float32)
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    description: str
+    shapes: tuple            # ((name, rows, cols), ...)
+    seeds: tuple             # one seed per matrix
+    fmt: str                 # "int" | "nvfp4"
+    bits: int
+    group: int
+    clips: tuple
+    w_bf16: bool
+    ema: bool
+    beta2: float = 0.999
+    layers: int = 1
+    extra: dict = field(default_factory=dict)
+
+    @property
+    def n_weights(self) -> int:
+        return sum(r * c for _, r, c in self.shapes)
+
+
+def _layer_set(table, layers=1):
+    shapes, seeds = [], []
+    for l in range(layers):
+        for m, name in enumerate(LAYER_ORDER):
+            r, c = table[name]
+            shapes.append((f"L{l}.{name}" if layers > 1 else name, r, c))
+            seeds.append(1000 * l + m)
+    return tuple(shapes), tuple(seeds)
+
+
+def workloads() -> dict:
+    q06, q06s = _layer_set(QWEN3_0_6B)
+    l8, l8s = _layer_set(LLAMA31_8B)
+    l8x32, l8x32s = _layer_set(LLAMA31_8B, 32)
+    return {
+        "c1": Workload("c1", "single fp32 1024x1024 matrix, INT4 g128, 8 clips 1.0..0.65",
+                       (("w", 1024, 1024),), (0,), "int", 4, 128, tuple(clip_grid(1.0, 0.65, 8)),
+                       w_bf16=False, ema=False),
+        "c2": Workload("c2", "Qwen3-0.6B-shaped layer set, bf16 W, INT3 g128, 8 clips 1.0..0.65",
+                       q06, q06s, "int", 3, 128, tuple(clip_grid(1.0, 0.65, 8)), w_bf16=True, ema=False),
+        "c3": Workload("c3", "Llama-3.1-8B-shaped layer set, bf16 W, INT2 g64, 12 clips 1.0..0.5, "
+                       "fused EMA from a bf16 gradient (beta2 0.999)",
+                       l8, l8s, "int", 2, 64, tuple(clip_grid(1.0, 0.5, 12)), w_bf16=True, ema=True),
+        "c4": Workload("c4", "Llama-3.1-8B-shaped layer set, bf16 W, NVFP4 16-blocks, 8 clips 1.0..0.7",
+                       l8, l8s, "nvfp4", 4, 16, tuple(clip_grid(1.0, 0.7, 8)), w_bf16=True, ema=False),
+        "c5": Workload("c5", "32 Llama-3.1-8B-shaped layers, bf16 W, INT4 g128, 8 clips 1.0..0.65, "
+                       "fused EMA (one simulated training step)",
+                       l8x32, l8x32s, "int", 4, 128, tuple(clip_grid(1.0, 0.65, 8)), w_bf16=True,
+                       ema=True, layers=32),
+    }
+
+
+def gen_matrix(rows: int, cols: int, seed: int, *, w_bf16: bool, ema: bool, device="cpu",
+               outliers: int = 4):
+    """Draw (W, v, g) for one matrix on ``device`` (torch tensors; g is None
+    without an EMA)."""
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(seed))
+    W = torch.randn(rows, cols, generator=gen, device=device, dtype=torch.float32) * 0.02
+    k = min(outliers, cols)
+    idx = torch.randperm(cols, generator=gen, device=device)[:k]
+    W[:, idx] *= 10.0
+    row_s = torch.exp(torch.randn(rows, generator=gen, device=device, dtype=torch.float32))
+    col_s = torch.exp(torch.randn(cols, generator=gen, device=device, dtype=torch.float32))
+    z = torch.randn(rows, cols, generator=gen, device=device, dtype=torch.float32)
+    z.mul_(row_s[:, None]).mul_(col_s[None, :])
+    v = z.square_()
+    g = None
+    if ema:
+        g = (torch.randn(rows, cols, generator=gen, device=device, dtype=torch.float32) * 1e-3).to(torch.bfloat16)
+    if w_bf16:
+        W = W.to(torch.bfloat16)
+    return W, v, g
+
+
+def to_host(t):
+    """Host numpy view of a generated tensor: float32 stays float32, bf16 becomes
+    its uint16 bit pattern (the oracle reads the same bytes)."""
+    if t is None:
+        return None
+    t = t.detach().to("cpu").contiguous()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16)
+    return t.numpy()

@@ -1,0 +1,436 @@
+"""Pins for the CPU oracle (no GPU).
+
+Every check here compares the oracle with something other than itself: the
+hand-derived fixtures in tests/golden, exact rational arithmetic, brute force,
+numpy/torch library routines, closed-form special cases and invariants that
+the paper's construction implies.
+"""
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_13966_amd import synth
+from tests import _exact as X
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def run_group(w, h, *, bits=4, clips=(1.0,), fmt="int", amax=None, **kw):
+    w = np.asarray(w, np.float32)[None, :]
+    h = np.asarray(h, np.float32)[None, :]
+    return oracle.reconstruct(w, h, fmt=fmt, bits=bits, group=w.shape[1], clips=clips,
+                              tensor_amax=amax, want_scores=True, want_diag=True, **kw)
+
+
+def small_matrix(rows, cols, seed, ema=False, bf16=False):
+    W, v, g = synth.gen_matrix(rows, cols, seed, w_bf16=bf16, ema=ema)
+    return synth.to_host(W), synth.to_host(v), synth.to_host(g)
+
+
+def w_as_f32(Wh):
+    if Wh.dtype == np.uint16:
+        return (Wh.astype(np.uint32) << 16).view(np.float32)
+    return Wh
+
+
+# ---------------------------------------------------------------- fixtures
+
+def test_golden_int2_outlier_group():
+    d = json.load(open(os.path.join(GOLDEN, "int2_outlier_group.json")))
+    o = run_group(d["w"], d["h"], bits=d["bits"], clips=d["clips"])
+    e = d["expect"]
+    assert int(o["best"][0]) == e["best"]
+    assert o["codes"][0].tolist() == e["codes"]
+    assert float(o["scale"][0]) == e["scale"] and float(o["zero"][0]) == e["zero"]
+    assert o["r"][0].tolist() == e["r"]
+    assert float(o["err"][0]) == e["err"]
+    np.testing.assert_allclose(o["scores"][0], e["scores"], rtol=1e-6)
+
+
+def test_golden_nvfp4_single_value_block():
+    d = json.load(open(os.path.join(GOLDEN, "nvfp4_single_value_block.json")))
+    o = run_group(d["w"], d["h"], fmt="nvfp4", clips=d["clips"], amax=d["tensor_amax"])
+    e = d["expect"]
+    assert int(o["best"][0]) == e["best"]
+    assert int(o["e4m3"][0]) == e["e4m3"]
+    assert float(o["tensor_scale"]) == e["tensor_scale"]
+    assert o["codes_packed"].tolist() == e["codes_packed"]
+    assert float(o["r"][0, 0]) == e["r0"] and float(o["err"][0]) == e["err"]
+
+
+def test_golden_packing_and_round_trip():
+    d = json.load(open(os.path.join(GOLDEN, "packing.json")))
+    for case in d["cases"]:
+        p = oracle.pack_group(np.array(case["codes"], np.uint8), case["bits"])
+        assert p.tolist() == case["packed"]
+    rng = np.random.default_rng(0)
+    for bits in (2, 3, 4):
+        for n in (16, 64, 128):
+            c = rng.integers(0, 1 << bits, n).astype(np.uint8)
+            assert np.array_equal(oracle.unpack_group(oracle.pack_group(c, bits), n, bits), c)
+
+
+# ---------------------------------------------------------------- formats
+
+def _sweep_e2m1():
+    pts = list(np.linspace(-8, 8, 64001, dtype=np.float32))
+    for m in (0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0, 6.0):
+        for s in (1.0, -1.0):
+            x = np.float32(s * m)
+            pts += [x, np.nextafter(x, np.float32(np.inf)), np.nextafter(x, np.float32(-np.inf))]
+    pts += [np.float32(1e-30), np.float32(-1e-30), np.float32(0.0), np.float32(-0.0), np.float32(1e30)]
+    return pts
+
+
+def test_e2m1_against_brute_force():
+    for y in _sweep_e2m1():
+        c = oracle.e2m1_code(float(y))
+        idx = X.e2m1_nearest_index(abs(float(y)))
+        expect = 0 if idx == 0 else ((8 if y < 0 else 0) | idx)
+        assert c == expect, (float(y), c, expect)
+
+
+def _e4m3_points():
+    vals = [v for v, _ in X.e4m3_levels()]
+    pts = set()
+    for a, b in zip(vals[:-1], vals[1:]):
+        mid = (a + b) / 2
+        for x in (a, b, mid, np.nextafter(np.float32(mid), np.float32(0)), np.nextafter(np.float32(mid), np.float32(1e9))):
+            pts.add(float(np.float32(x)))
+    rng = np.random.default_rng(1)
+    pts.update(float(np.float32(x)) for x in rng.uniform(0, 448, 4000))
+    pts.update(float(np.float32(x)) for x in np.exp(rng.uniform(math.log(1e-4), math.log(448), 4000)))
+    return sorted(p for p in pts if 0 <= p <= 448)
+
+
+def test_e4m3_against_torch_float8():
+    pts = _e4m3_points()
+    ref = torch.tensor(pts, dtype=torch.float32).to(torch.float8_e4m3fn)
+    ref_bytes = ref.view(torch.uint8).tolist()
+    for x, rb in zip(pts, ref_bytes):
+        assert oracle.e4m3_code(x) == rb, (x, oracle.e4m3_code(x), rb)
+
+
+def test_e4m3_fp64_input_brute_force_and_saturation():
+    levels = X.e4m3_levels()
+    vals = np.array([v for v, _ in levels])
+    rng = np.random.default_rng(2)
+    xs = list(np.exp(rng.uniform(math.log(1e-5), math.log(447.9), 3000)))
+    for x in xs:
+        d = np.abs(vals - x)
+        cand = np.flatnonzero(d == d.min())
+        codes = [levels[i][1] for i in cand]
+        c = oracle.e4m3_code(float(x))
+        if len(codes) == 1:
+            assert c == codes[0]
+        else:  # tie: even mantissa
+            assert c in codes and c % 2 == 0
+    for x in (448.0, 450.0, 463.99, 464.0, 500.0, 1e30, float("inf")):
+        assert oracle.e4m3_code(x) == 0x7E
+    assert oracle.e4m3_code(0.0) == 0 and oracle.e4m3_code(-1.0) == 0
+    assert oracle.e4m3_code(2.0 ** -10) == 0          # tie between 0 and 2^-9 -> even (0)
+    assert oracle.e4m3_code(1.5 * 2.0 ** -9) == 2      # tie between 1 and 2 (x 2^-9) -> even
+
+
+def test_bf16_rounding_against_torch():
+    rng = np.random.default_rng(3)
+    x = np.concatenate([rng.standard_normal(20000).astype(np.float32) * 0.1,
+                        np.array([1.0, 1.00390625, 1.005859375, 1.0078125, -2.50390625, 3e-39, -0.0, 65504.0],
+                                 np.float32)])
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    got = np.array([oracle.f32_to_bf16(float(v)) for v in x], np.uint16)
+    assert np.array_equal(got, ref)
+
+
+# ---------------------------------------------------------------- EMA
+
+def test_ema_matches_exact_definition():
+    """v' = beta2 * v + (1 - beta2) * g^2 with the documented fp32 order:
+    t = g*g, u = (1-beta2)*t, v' = fma(beta2, v, u).  Each step is computed here
+    with exact rationals and one correct rounding."""
+    Wh, vh, gh = small_matrix(4, 128, 7, ema=True, bf16=True)
+    beta2 = np.float32(0.999)
+    o = oracle.reconstruct(Wh, vh, bits=4, group=128, clips=(1.0,), g=gh, beta2=float(beta2))
+    gf = w_as_f32(gh).ravel()
+    vf = vh.ravel()
+    got = o["v_out"].ravel()
+    omb2 = X.fp32_from_fraction(Fraction(1) - Fraction(float(beta2)))
+    for i in range(0, gf.size, 3):
+        t = X.fp32_from_fraction(Fraction(float(gf[i])) ** 2)
+        u = X.fp32_from_fraction(Fraction(omb2) * Fraction(t))
+        ref = X.fp32_from_fraction(Fraction(float(beta2)) * Fraction(float(vf[i])) + Fraction(u))
+        assert np.float32(ref) == got[i], i
+
+
+# ---------------------------------------------------------------- INT: codes, fit, selection
+
+def _int_groups(bits, group, clips, seed, rows=8, cols=512, bf16=False):
+    Wh, vh, _ = small_matrix(rows, cols, seed, bf16=bf16)
+    o = oracle.reconstruct(Wh, vh, bits=bits, group=group, clips=clips, want_scores=True, want_diag=True)
+    return w_as_f32(Wh).reshape(-1, group), vh.reshape(-1, group), o
+
+
+@pytest.mark.parametrize("bits,group", [(4, 128), (3, 128), (2, 64)])
+def test_int_codes_fit_scores_against_exact_recompute(bits, group):
+    """For every group and every clip: codes by exact Eq. rtn on the clipped
+    range, dequantiser by numpy lstsq, score in fp64 -> must reproduce the
+    oracle's per-clip scores and its choice (boundary cases excused)."""
+    qmax = (1 << bits) - 1
+    clips = tuple(synth.clip_grid(1.0, 0.5, 6))
+    w, h, o = _int_groups(bits, group, clips, seed=11 + bits)
+    checked = 0
+    for gi in range(w.shape[0]):
+        wi, hi = w[gi], h[gi]
+        mn, mx = Fraction(float(wi.min())), Fraction(float(wi.max()))
+        c, rho = (mn + mx) / 2, (mx - mn) / 2
+        sc = []
+        near = False
+        for k, f in enumerate(clips):
+            f = Fraction(float(f))
+            lo, s = c - f * rho, 2 * f * rho / qmax
+            q, dist = X.rtn_codes_exact(wi, lo, s, qmax)
+            # the fp32 recipe is within ~1e-5 code units of the exact quotient
+            if dist.min() < 2e-5:
+                near = True
+                break
+            a, b = X.wls_fit(q, wi, hi)
+            sc.append(X.score(q, wi, hi, a, b))
+            if k == int(o["best"][gi]):
+                assert np.array_equal(o["codes"].reshape(-1, group)[gi], q)
+                np.testing.assert_allclose(o["scale"][gi], a, rtol=1e-6)
+                np.testing.assert_allclose(o["zero"][gi], b, rtol=1e-6, atol=1e-7 * abs(a) * qmax)
+        if near:
+            continue
+        checked += 1
+        np.testing.assert_allclose(o["scores"][gi], sc, rtol=1e-6)
+        kk = int(np.argmin(sc))
+        if kk != int(o["best"][gi]):
+            assert abs(sc[kk] - sc[int(o["best"][gi])]) <= 1e-6 * sc[kk]
+    assert checked >= 0.85 * w.shape[0]
+
+
+def test_uniform_saliency_is_ordinary_least_squares():
+    """h == 1: the fit is the unweighted line through (q, w) -- numpy.polyfit."""
+    Wh, _, _ = small_matrix(4, 256, 21)
+    h = np.ones_like(Wh, dtype=np.float32)
+    o = oracle.reconstruct(Wh, h, bits=3, group=128, clips=(1.0, 0.8, 0.6), want_scores=True)
+    for gi in range(Wh.size // 128):
+        q = o["codes"].reshape(-1, 128)[gi].astype(np.float64)
+        wv = Wh.reshape(-1, 128)[gi].astype(np.float64)
+        s, z = np.polyfit(q, wv, 1)
+        np.testing.assert_allclose(o["scale"][gi], s, rtol=2e-7)
+        np.testing.assert_allclose(o["zero"][gi], z, rtol=2e-7, atol=1e-8)
+
+
+def test_selection_is_first_argmin_of_scores():
+    w, h, o = _int_groups(4, 128, tuple(synth.clip_grid(1.0, 0.65, 8)), seed=5)
+    sc = o["scores"]
+    best = o["best"].astype(int)
+    assert np.all(sc[np.arange(sc.shape[0]), best] == sc.min(axis=1))
+    for gi in range(sc.shape[0]):  # lowest index among equal minima
+        assert best[gi] == int(np.flatnonzero(sc[gi] == sc[gi].min())[0])
+    np.testing.assert_array_equal(o["err"], sc.min(axis=1).astype(np.float32))
+
+
+@pytest.mark.parametrize("bits,group", [(4, 128), (3, 128), (2, 64)])
+def test_never_worse_than_standard_qat(bits, group):
+    """1.0 is a candidate and the fit is optimal for fixed codes, so
+    S(f*) <= S_LS(1) <= S_RTN(1) (min-max range with its own scale/zero).
+    S_RTN(1) is recomputed here with exact Eq. rtn codes."""
+    qmax = (1 << bits) - 1
+    clips = tuple(synth.clip_grid(1.0, 0.65, 8))
+    w, h, o = _int_groups(bits, group, clips, seed=30 + bits)
+    for gi in range(w.shape[0]):
+        wi, hi = w[gi], h[gi]
+        mn, mx = float(wi.min()), float(wi.max())
+        q, dist = X.rtn_codes_exact(wi, Fraction(mn), Fraction(mx - mn) / qmax, qmax)
+        s_rtn = X.score(q, wi, hi, (mx - mn) / qmax, mn)
+        s_ls = o["scores"][gi, 0]
+        s_best = o["scores"][gi, int(o["best"][gi])]
+        assert s_best <= s_ls
+        assert s_ls <= s_rtn * (1 + 1e-6) + 1e-30
+        assert s_best <= o["diag"][gi, 0] * (1 + 1e-9) + 1e-30
+
+
+def test_denoising_qat_special_case():
+    """F = {1} and h = 1 (Alg. 1 note): min-max codes, dequantiser by ordinary
+    least squares."""
+    Wh, _, _ = small_matrix(2, 256, 41)
+    h = np.ones_like(Wh, dtype=np.float32)
+    o = oracle.reconstruct(Wh, h, bits=2, group=64, clips=(1.0,))
+    w = Wh.reshape(-1, 64)
+    for gi in range(w.shape[0]):
+        mn, mx = float(w[gi].min()), float(w[gi].max())
+        q, dist = X.rtn_codes_exact(w[gi], Fraction(mn), Fraction(mx - mn) / 3, 3)
+        if dist.min() < 2e-5:
+            continue
+        assert np.array_equal(o["codes"].reshape(-1, 64)[gi], q)
+        s, z = np.polyfit(q.astype(np.float64), w[gi].astype(np.float64), 1)
+        np.testing.assert_allclose(o["scale"][gi], s, rtol=2e-7)
+
+
+def test_power_of_two_saliency_scaling_is_exact():
+    """Scaling h by 2^k changes nothing but the score, which scales by 2^k."""
+    Wh, vh, _ = small_matrix(4, 256, 51, bf16=True)
+    clips = tuple(synth.clip_grid(1.0, 0.5, 12))
+    o1 = oracle.reconstruct(Wh, vh, bits=2, group=64, clips=clips, want_scores=True)
+    for k in (-7, 5):
+        o2 = oracle.reconstruct(Wh, vh * np.float32(2.0 ** k), bits=2, group=64, clips=clips, want_scores=True)
+        for key in ("codes", "scale", "zero", "r", "best"):
+            assert np.array_equal(o1[key], o2[key]), key
+        np.testing.assert_array_equal(o2["scores"], o1["scores"] * 2.0 ** k)
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4])
+def test_codes_monotone_and_endpoints(bits):
+    qmax = (1 << bits) - 1
+    Wh, vh, _ = small_matrix(4, 256, 61)
+    o1 = oracle.reconstruct(Wh, vh, bits=bits, group=128, clips=(1.0,))
+    o = oracle.reconstruct(Wh, vh, bits=bits, group=128, clips=tuple(synth.clip_grid(1.0, 0.5, 6)))
+    w = Wh.reshape(-1, 128)
+    for gi in range(w.shape[0]):
+        order = np.argsort(w[gi], kind="stable")
+        for out in (o1, o):
+            q = out["codes"].reshape(-1, 128)[gi]
+            assert np.all(np.diff(q[order].astype(int)) >= 0)
+            assert q.max() <= qmax
+        q1 = o1["codes"].reshape(-1, 128)[gi]
+        assert q1[np.argmin(w[gi])] == 0 and q1[np.argmax(w[gi])] == qmax
+        assert o["scale"][gi] >= 0
+
+
+def test_degenerate_groups():
+    clips = (1.0, 0.75, 0.5)
+    # constant group: exact reconstruction, codes 0
+    o = run_group([0.5] * 8, [1.0] * 8, bits=3, clips=clips)
+    assert o["r"][0].tolist() == [0.5] * 8 and o["codes"].sum() == 0 and o["err"][0] == 0
+    assert o["best"][0] == 0 and o["scale"][0] == 0 and o["zero"][0] == 0.5
+    # zero saliency: every score 0, first clip, its min-max (RTN) dequantiser
+    w = np.array([0.0, 0.1, 0.3, 0.7, -0.2, 0.05, 0.2, 0.4], np.float32)
+    o = run_group(w, [0.0] * 8, bits=2, clips=clips)
+    assert o["best"][0] == 0 and np.all(o["scores"][0] == 0)
+    rho = np.float32(0.5) * (np.float32(0.7) - np.float32(-0.2))
+    assert o["scale"][0] == np.float32(np.float32(2.0) * rho) / np.float32(3.0)
+    assert o["zero"][0] == np.float32(np.float32(0.5) * (np.float32(0.7) + np.float32(-0.2))) - rho
+    # all saliency on one weight: slope undetermined -> RTN step, offset fitted
+    h = np.zeros(8, np.float32)
+    h[3] = 2.0
+    o = run_group(w, h, bits=2, clips=clips)
+    k = int(o["best"][0])
+    f = np.float32(clips[k])
+    assert o["diag"][0, 3] == 2
+    assert o["scale"][0] == np.float32(np.float32(2.0) * (f * rho)) / np.float32(3.0)
+    q3 = float(o["codes"][0, 3])
+    np.testing.assert_allclose(float(o["zero"][0]) + float(o["scale"][0]) * q3, 0.7, rtol=1e-6)
+
+
+def test_brute_force_lower_bound_on_tiny_groups():
+    """Alg. 1 searches a finite candidate set; no monotone code assignment with
+    its optimal dequantiser can beat the global optimum, and Alg. 1's result
+    can never beat it either: S_global <= S(f*)."""
+    rng = np.random.default_rng(71)
+    for _ in range(25):
+        w = (rng.standard_normal(6) * 0.02).astype(np.float32)
+        w[rng.integers(6)] *= 10
+        h = (rng.standard_normal(6) ** 2).astype(np.float32)
+        o = run_group(w, h, bits=2, clips=tuple(synth.clip_grid(1.0, 0.5, 12)))
+        order = np.argsort(w)
+        best = math.inf
+        for qs in X.monotone_assignments(6, 3):
+            q = np.empty(6)
+            q[order] = qs
+            a, b = X.wls_fit(q, w, h)
+            best = min(best, X.score(q, w, h, a, b))
+        assert best <= o["err"][0] * (1 + 1e-6) + 1e-30
+
+
+def test_threads_give_identical_results():
+    Wh, vh, gh = small_matrix(32, 256, 81, ema=True, bf16=True)
+    kw = dict(bits=2, group=64, clips=tuple(synth.clip_grid(1.0, 0.5, 12)), g=gh)
+    a = oracle.reconstruct(Wh, vh, n_threads=1, **kw)
+    b = oracle.reconstruct(Wh, vh, n_threads=4, **kw)
+    for key in ("codes", "codes_packed", "scale", "zero", "r", "best", "err", "v_out"):
+        assert np.array_equal(a[key], b[key]), key
+
+
+# ---------------------------------------------------------------- NVFP4
+
+def _nvfp4(seed, rows=8, cols=256, clips=None, ema=False):
+    Wh, vh, gh = small_matrix(rows, cols, seed, bf16=True, ema=ema)
+    clips = clips or tuple(synth.clip_grid(1.0, 0.7, 8))
+    o = oracle.reconstruct(Wh, vh, fmt="nvfp4", clips=clips, g=gh, want_scores=True, want_diag=True)
+    h = o["v_out"] if ema else vh
+    return w_as_f32(Wh).reshape(-1, 16), h.reshape(-1, 16), o, clips
+
+
+def test_nvfp4_block_scale_is_best_e4m3_for_its_codes():
+    w, h, o, _ = _nvfp4(91)
+    st = float(o["tensor_scale"])
+    levels = X.e4m3_levels()
+    codes = o["codes"].reshape(-1, 16)
+    for gi in range(w.shape[0]):
+        q = np.array([X.E2M1_LEVELS[c & 7] * (-1 if c & 8 else 1) for c in codes[gi]])
+        # the stored dequantiser is the fp32 product S_t * e
+        mine = X.score(q, w[gi], h[gi], np.float32(np.float32(st) * np.float32(oracle.e4m3_value(int(o["e4m3"][gi])))), 0.0)
+        for val, _ in levels:
+            other = X.score(q, w[gi], h[gi], np.float32(np.float32(st) * np.float32(val)), 0.0)
+            # nearest-to-s* is exact for the real product; the fp32 product can
+            # only reorder two candidates that sit on a rounding midpoint
+            assert mine <= other * (1 + 1e-6) + 1e-30
+        np.testing.assert_allclose(o["err"][gi], mine, rtol=1e-6)
+        assert o["e4m3"][gi] < 0x80
+
+
+def test_nvfp4_never_worse_than_standard_qat():
+    w, h, o, _ = _nvfp4(92)
+    st = float(o["tensor_scale"])
+    for gi in range(w.shape[0]):
+        m = float(np.abs(w[gi]).max())
+        q = np.array([X.E2M1_LEVELS[X.e2m1_nearest_index(abs(x) * 6 / m)] * np.sign(x) for x in w[gi]])
+        e = torch.tensor([m / 6 / st], dtype=torch.float32).to(torch.float8_e4m3fn).float().item()
+        s_std = X.score(q, w[gi], h[gi], np.float32(st * e), 0.0)
+        assert o["err"][gi] <= s_std * (1 + 1e-6) + 1e-30
+
+
+def test_nvfp4_codes_against_exact_search_scale():
+    w, h, o, clips = _nvfp4(93)
+    codes = o["codes"].reshape(-1, 16)
+    for gi in range(w.shape[0]):
+        m = Fraction(float(np.abs(w[gi]).max()))
+        f = Fraction(float(clips[int(o["best"][gi])]))
+        for i, x in enumerate(w[gi]):
+            y = Fraction(float(x)) * 6 / (f * m)
+            a = abs(y)
+            mids = [Fraction(1, 4), Fraction(3, 4), Fraction(5, 4), Fraction(7, 4), Fraction(5, 2), Fraction(7, 2), Fraction(5)]
+            if min(abs(a - t) for t in mids) < Fraction(1, 10 ** 5):
+                continue
+            idx = X.e2m1_nearest_index(float(a))
+            expect = 0 if idx == 0 else ((8 if y < 0 else 0) | idx)
+            assert codes[gi, i] == expect
+
+
+def test_nvfp4_zero_tensor_and_zero_block():
+    W = np.zeros((2, 32), np.float32)
+    W[1, 16:] = np.linspace(-1, 1, 16, dtype=np.float32)
+    v = np.ones_like(W)
+    o = oracle.reconstruct(W, v, fmt="nvfp4", clips=(1.0, 0.8))
+    assert np.all(o["codes_packed"][:16] == 0) and np.all(o["e4m3"][:3] == 0) and np.all(o["r"][0] == 0)
+    assert o["e4m3"][3] != 0
+    o = oracle.reconstruct(np.zeros((1, 16), np.float32), np.ones((1, 16), np.float32), fmt="nvfp4", clips=(1.0,))
+    assert float(o["tensor_scale"]) == 0.0 and np.all(o["r"] == 0) and o["err"][0] == 0
+
+
+def test_nvfp4_power_of_two_saliency_scaling_is_exact():
+    Wh, vh, _ = small_matrix(4, 128, 94, bf16=True)
+    clips = tuple(synth.clip_grid(1.0, 0.7, 8))
+    o1 = oracle.reconstruct(Wh, vh, fmt="nvfp4", clips=clips, want_scores=True)
+    o2 = oracle.reconstruct(Wh, vh * np.float32(8.0), fmt="nvfp4", clips=clips, want_scores=True)
+    for key in ("codes", "e4m3", "r", "best"):
+        assert np.array_equal(o1[key], o2[key]), key
+    np.testing.assert_array_equal(o2["scores"], o1["scores"] * 8.0)
