@@ -1,0 +1,143 @@
+/*
+ * quasar.h -- C ABI of libquasar.so: QUASAR's per-step loss-aware weight
+ * reconstruction (arXiv 2608.13966) as HIP kernels for MI355X (gfx950).
+ *
+ * One call reconstructs one weight matrix W [rows = out, cols = in], row-major,
+ * with quantisation groups running along a row (Sec. 3.1: "each row ... is
+ * partitioned into groups"; App. B: groups run along the input dimension).
+ * For every group it takes the saliency h (Sec. 4.1.1: the EMA of squared
+ * gradients, AdamW's second moment v; optionally updated in the same pass from
+ * the current gradient g as v = beta2*v + (1-beta2)*g^2, App. A.2), then runs
+ * Algorithm 1 (Sec. 4.1.2): for each clip factor f in F, RTN codes on the range
+ * [c - f*rho, c + f*rho] (Eq. rtn), the saliency-weighted least-squares
+ * dequantiser (s, z) (Eq. ridgefit) and its score sum h (s q + z - w)^2
+ * (Eq. fisher-obj); the argmin is kept and emitted as codes, scale, zero and
+ * the reconstruction r = s q + z.  NVFP4 (Sec. 4.2) uses 16-element blocks of
+ * E2M1 codes, an E4M3 block scale fitted to the same objective (scale only,
+ * no zero-point) and an fp32 tensor scale from the tensor absmax.
+ *
+ * Conventions
+ *  - Every data pointer is HIP device memory owned by the caller, except
+ *    desc->clip_ratios, which is a host array read during the call.
+ *  - The library allocates no memory and keeps no state between calls; it is
+ *    reentrant.  Work is enqueued on `stream` (a hipStream_t; NULL = the null
+ *    stream) and the call returns without waiting; results are valid once the
+ *    caller has synchronised that stream.
+ *  - Argument errors are detected on the host before anything is launched; a
+ *    call that returns an error has written nothing.  QUASAR_ERR_DEVICE reports
+ *    a launch failure; faults during execution surface at the caller's sync.
+ *  - Every device pointer must be 16-byte aligned.
+ *  - v >= 0 is a precondition (saliency is non-negative, Alg. 1 input); it is
+ *    not checked.  NaN or Inf inputs give unspecified (but in-bounds) results.
+ *
+ * Output layouts (the paper fixes none; these are this library's):
+ *  - codes: groups in row-major order, each group's codes contiguous:
+ *      INT4 / NVFP4: two per byte, even element in the low nibble;
+ *      INT2: four per byte, element 4k+j at bits 2j;
+ *      INT3: per group a little-endian bit stream, code i at bits [3i, 3i+3)
+ *            (48 bytes per 128-group, 24 per 64-group).
+ *    NVFP4 code = (sign << 3) | magnitude index, magnitudes 0, 0.5, 1, 1.5, 2,
+ *    3, 4, 6; zero is always +0.
+ *  - INT: scales = fp32 s, zeros = fp32 z, one each per group ([rows, cols/group]).
+ *  - NVFP4: scales = one E4M3FN byte per 16-block ([rows, cols/16]); zeros unused;
+ *    tensor_scale = one fp32 S_t; the block's dequantiser is S_t * e4m3.
+ *  - r: [rows, cols] in W's dtype (fp32 r = fmaf(s, q, z); bf16 = its
+ *    round-to-nearest-even).
+ *  - best_clip: u8 index into clip_ratios per group; err: fp32 score of the
+ *    chosen candidate per group.
+ */
+#ifndef QUASAR_H
+#define QUASAR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  QUASAR_OK = 0,
+  QUASAR_ERR_ARG = -1,       /* NULL required pointer, n_clips, clip ratio or beta2 out of range */
+  QUASAR_ERR_SHAPE = -2,     /* rows/cols < 1, cols % group != 0, too many groups */
+  QUASAR_ERR_ALIGN = -3,     /* a device pointer is not 16-byte aligned */
+  QUASAR_ERR_FORMAT = -4,    /* unsupported format / bits / group / dtype */
+  QUASAR_ERR_WORKSPACE = -5, /* workspace missing or smaller than quasar_workspace_bytes() */
+  QUASAR_ERR_DEVICE = -6     /* HIP reported an error when launching */
+} quasar_status;
+
+typedef enum { QUASAR_F32 = 0, QUASAR_BF16 = 1 } quasar_dtype;
+typedef enum { QUASAR_INT = 0, QUASAR_NVFP4 = 1 } quasar_format;
+
+#define QUASAR_MAX_CLIPS 16
+
+typedef struct {
+  int64_t rows;               /* out features, >= 1 */
+  int64_t cols;               /* in features, >= 1, multiple of group */
+  int32_t w_dtype;            /* quasar_dtype of W and of r */
+  int32_t format;             /* quasar_format */
+  int32_t bits;               /* INT: 2, 3 or 4 (qmax = 2^bits - 1); ignored for NVFP4 */
+  int32_t group;              /* INT: 64 or 128; NVFP4: 16 */
+  const float* clip_ratios;   /* HOST array of n_clips factors, each in (0, 1]; order breaks ties
+                                 (the lowest index wins among equal scores) */
+  int32_t n_clips;            /* 1 .. QUASAR_MAX_CLIPS */
+  int32_t g_dtype;            /* quasar_dtype of g when g != NULL */
+  float beta2;                /* EMA decay when g != NULL, in [0.5, 1) */
+} quasar_desc;
+
+/*
+ * Reconstruct one matrix (Alg. 1 for every group; Sec. 4.2 for NVFP4).
+ *
+ *  W            [rows, cols] in desc->w_dtype (read)
+ *  v            [rows, cols] fp32 saliency.  Read only when g == NULL.  When g
+ *               != NULL it is read and overwritten in place with
+ *               v' = fmaf(beta2, v, (1 - beta2) * (g * g)) (fp32, this order), and
+ *               v' is the saliency used.
+ *  g            [rows, cols] gradient in desc->g_dtype, or NULL (no EMA)
+ *  codes        packed codes, quasar_codes_bytes(desc) bytes (required)
+ *  scales       INT: fp32 [rows, cols/group]; NVFP4: u8 E4M3 [rows, cols/16] (required)
+ *  zeros        INT: fp32 [rows, cols/group] (required); NVFP4: unused, pass NULL
+ *  r            [rows, cols] in w_dtype, or NULL to skip writing r (export only)
+ *  best_clip    u8 [groups] or NULL;  err  fp32 [groups] or NULL
+ *  tensor_scale NVFP4: fp32 [1] output S_t = amax / 2688 (required); INT: NULL
+ *  tensor_amax  NVFP4: optional fp32 [1] input, the tensor absmax (e.g. tracked
+ *               by the optimiser); NULL = computed here with an extra pass over W.
+ *               INT: NULL.
+ *  workspace    device scratch of at least quasar_workspace_bytes(desc) bytes, or
+ *               NULL when that size is 0.  Not read before it is written.
+ *  stream       hipStream_t to enqueue on.
+ * Returns a quasar_status.
+ */
+int quasar_reconstruct(const quasar_desc* desc, const void* W, float* v, const void* g,
+                       uint8_t* codes, void* scales, float* zeros, void* r, uint8_t* best_clip,
+                       float* err, float* tensor_scale, const float* tensor_amax, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
+/* Host-only validation: the status quasar_reconstruct would return for these
+ * arguments, without launching anything or touching device memory. */
+int quasar_check(const quasar_desc* desc, const void* W, const float* v, const void* g,
+                 const uint8_t* codes, const void* scales, const float* zeros, const void* r,
+                 const uint8_t* best_clip, const float* err, const float* tensor_scale,
+                 const float* tensor_amax, const void* workspace, size_t workspace_bytes);
+
+/* Number of groups (INT) or 16-blocks (NVFP4) of the matrix; 0 for an invalid desc. */
+int64_t quasar_num_groups(const quasar_desc* desc);
+
+/* Bytes of the packed code buffer; 0 for an invalid desc. */
+size_t quasar_codes_bytes(const quasar_desc* desc);
+
+/* Bytes of device workspace the call needs (NVFP4 without tensor_amax: 256;
+ * otherwise 0). */
+size_t quasar_workspace_bytes(const quasar_desc* desc, int has_tensor_amax);
+
+/* Static description of a status code. */
+const char* quasar_status_string(int status);
+
+/* Library version, "major.minor.patch". */
+const char* quasar_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QUASAR_H */

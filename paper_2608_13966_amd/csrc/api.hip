@@ -1,0 +1,167 @@
+// api.hip -- the C ABI of libquasar.so (declared in include/quasar.h):
+// host-side argument validation, clip-table preparation and kernel dispatch.
+#include <math.h>
+#include <string.h>
+
+#include "quasar.h"
+#include "quasar_internal.h"
+
+namespace {
+
+bool aligned16(const void* p) { return p == nullptr || (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int group_of(const quasar_desc* d) { return d->format == QUASAR_NVFP4 ? 16 : d->group; }
+int bits_of(const quasar_desc* d) { return d->format == QUASAR_NVFP4 ? 4 : d->bits; }
+
+// Validation of the descriptor alone.
+int check_desc(const quasar_desc* d) {
+  if (d == nullptr) return QUASAR_ERR_ARG;
+  if (d->w_dtype != QUASAR_F32 && d->w_dtype != QUASAR_BF16) return QUASAR_ERR_FORMAT;
+  if (d->format == QUASAR_INT) {
+    if (d->bits < 2 || d->bits > 4) return QUASAR_ERR_FORMAT;
+    if (d->group != 64 && d->group != 128) return QUASAR_ERR_FORMAT;
+  } else if (d->format == QUASAR_NVFP4) {
+    if (d->group != 16) return QUASAR_ERR_FORMAT;
+  } else {
+    return QUASAR_ERR_FORMAT;
+  }
+  if (d->rows < 1 || d->cols < 1) return QUASAR_ERR_SHAPE;
+  if (d->cols % group_of(d) != 0) return QUASAR_ERR_SHAPE;
+  // group ids and grid sizes stay far inside int64 / launch limits
+  if (d->rows > ((int64_t)1 << 40) / d->cols) return QUASAR_ERR_SHAPE;
+  if (d->n_clips < 1 || d->n_clips > QUASAR_MAX_CLIPS) return QUASAR_ERR_ARG;
+  if (d->clip_ratios == nullptr) return QUASAR_ERR_ARG;
+  for (int k = 0; k < d->n_clips; k++) {
+    const float f = d->clip_ratios[k];
+    // (0, 1] as in Alg. 1; factors below 2^-24 would overflow qmax / (2 f)
+    if (!(f > 0.0f && f <= 1.0f) || f < 5.9604645e-08f) return QUASAR_ERR_ARG;
+  }
+  return QUASAR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* quasar_version(void) { return "0.1.0"; }
+
+const char* quasar_status_string(int s) {
+  switch (s) {
+    case QUASAR_OK: return "ok";
+    case QUASAR_ERR_ARG: return "invalid argument (NULL pointer, n_clips, clip ratio or beta2 out of range)";
+    case QUASAR_ERR_SHAPE: return "invalid shape (rows/cols < 1, cols not a multiple of the group, too large)";
+    case QUASAR_ERR_ALIGN: return "device pointer not 16-byte aligned";
+    case QUASAR_ERR_FORMAT: return "unsupported format, bits, group size or dtype";
+    case QUASAR_ERR_WORKSPACE: return "workspace missing or too small";
+    case QUASAR_ERR_DEVICE: return "HIP launch error";
+    default: return "unknown status";
+  }
+}
+
+int64_t quasar_num_groups(const quasar_desc* d) {
+  if (check_desc(d) != QUASAR_OK) return 0;
+  return d->rows * (d->cols / group_of(d));
+}
+
+size_t quasar_codes_bytes(const quasar_desc* d) {
+  if (check_desc(d) != QUASAR_OK) return 0;
+  return (size_t)(d->rows * d->cols) * (size_t)bits_of(d) / 8u;
+}
+
+size_t quasar_workspace_bytes(const quasar_desc* d, int has_tensor_amax) {
+  if (check_desc(d) != QUASAR_OK) return 0;
+  return (d->format == QUASAR_NVFP4 && !has_tensor_amax) ? 256u : 0u;
+}
+
+int quasar_check(const quasar_desc* d, const void* W, const float* v, const void* g, const uint8_t* codes,
+                 const void* scales, const float* zeros, const void* r, const uint8_t* best_clip,
+                 const float* err, const float* tensor_scale, const float* tensor_amax, const void* workspace,
+                 size_t workspace_bytes) {
+  int s = check_desc(d);
+  if (s != QUASAR_OK) return s;
+  if (g != nullptr) {
+    if (d->g_dtype != QUASAR_F32 && d->g_dtype != QUASAR_BF16) return QUASAR_ERR_FORMAT;
+    if (!(d->beta2 >= 0.5f && d->beta2 < 1.0f)) return QUASAR_ERR_ARG;
+  }
+  if (W == nullptr || v == nullptr || codes == nullptr || scales == nullptr) return QUASAR_ERR_ARG;
+  if (d->format == QUASAR_INT && zeros == nullptr) return QUASAR_ERR_ARG;
+  if (d->format == QUASAR_NVFP4 && tensor_scale == nullptr) return QUASAR_ERR_ARG;
+  const void* ptrs[] = {W, v, g, codes, scales, zeros, r, best_clip, err, tensor_scale, tensor_amax, workspace};
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return QUASAR_ERR_ALIGN;
+  const size_t need = quasar_workspace_bytes(d, tensor_amax != nullptr);
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return QUASAR_ERR_WORKSPACE;
+  return QUASAR_OK;
+}
+
+int quasar_reconstruct(const quasar_desc* d, const void* W, float* v, const void* g, uint8_t* codes,
+                       void* scales, float* zeros, void* r, uint8_t* best_clip, float* err, float* tensor_scale,
+                       const float* tensor_amax, void* workspace, size_t workspace_bytes, void* stream) {
+  const int s = quasar_check(d, W, v, g, codes, scales, zeros, r, best_clip, err, tensor_scale, tensor_amax,
+                             workspace, workspace_bytes);
+  if (s != QUASAR_OK) return s;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const int ema_mode = g == nullptr ? 0 : (d->g_dtype == QUASAR_BF16 ? 1 : 2);
+  const bool w_bf16 = d->w_dtype == QUASAR_BF16;
+  const int K = d->n_clips;
+  const float beta2 = g ? d->beta2 : 0.0f;
+  const float omb2 = 1.0f - beta2;
+  hipError_t e;
+  if (d->format == QUASAR_INT) {
+    quasar::IntParams p;
+    memset(&p, 0, sizeof(p));
+    p.W = W;
+    p.v = v;
+    p.g = g;
+    p.codes = codes;
+    p.scales = static_cast<float*>(scales);
+    p.zeros = zeros;
+    p.r = r;
+    p.best_clip = best_clip;
+    p.err = err;
+    p.n_groups = d->rows * (d->cols / d->group);
+    p.beta2 = beta2;
+    p.omb2 = omb2;
+    p.n_clips = K;
+    const float qmax = (float)((1 << d->bits) - 1);
+    for (int k = 0; k < quasar::kMaxClips; k++) {
+      const float f = d->clip_ratios[k < K ? k : K - 1];  // entries past K repeat the last clip
+      p.clip[k] = f;
+      p.alpha[k] = qmax / (2.0f * f);
+    }
+    e = quasar::launch_int(p, d->bits, d->group, w_bf16, ema_mode, st);
+  } else {
+    quasar::Nvfp4Params p;
+    memset(&p, 0, sizeof(p));
+    p.W = W;
+    p.v = v;
+    p.g = g;
+    p.codes = codes;
+    p.scales = static_cast<uint8_t*>(scales);
+    p.r = r;
+    p.best_clip = best_clip;
+    p.err = err;
+    p.tensor_scale = tensor_scale;
+    p.n_blocks = d->rows * (d->cols / 16);
+    p.beta2 = beta2;
+    p.omb2 = omb2;
+    p.n_clips = K;
+    for (int k = 0; k < quasar::kMaxClips; k++) {
+      const float f = d->clip_ratios[k < K ? k : K - 1];
+      p.clip[k] = f;
+      p.c6[k] = 6.0f / f;
+    }
+    if (tensor_amax != nullptr) {
+      p.amax = tensor_amax;
+    } else {
+      unsigned* ws = static_cast<unsigned*>(workspace);
+      e = quasar::launch_absmax(W, w_bf16, d->rows * d->cols, ws, st);
+      if (e != hipSuccess) return QUASAR_ERR_DEVICE;
+      p.amax = reinterpret_cast<const float*>(ws);
+    }
+    e = quasar::launch_nvfp4(p, w_bf16, ema_mode, st);
+  }
+  return e == hipSuccess ? QUASAR_OK : QUASAR_ERR_DEVICE;
+}
+
+}  // extern "C"

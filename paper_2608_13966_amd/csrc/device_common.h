@@ -1,0 +1,183 @@
+// device_common.h -- device helpers for the CDNA4 (gfx950) kernels:
+// 128-bit loads/stores, bf16 <-> fp32, DPP lane exchanges inside a row of 16.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace quasar {
+
+// ---- bit casts -------------------------------------------------------------
+__device__ __forceinline__ float as_f32(uint32_t u) { return __uint_as_float(u); }
+__device__ __forceinline__ uint32_t as_u32(float f) { return __float_as_uint(f); }
+
+// A value known to be the same in every lane, moved to a scalar register
+// (bit copy: the builtin's operand is an int).
+__device__ __forceinline__ float uniform_f32(float x) {
+  return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(x)));
+}
+
+// ---- bf16 ------------------------------------------------------------------
+// Round-to-nearest-even fp32 -> bf16 bits; a NaN stays a (quiet) NaN.
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = as_u32(f);
+  uint32_t rounded = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+  uint32_t nan = (u >> 16) | 0x40u;
+  return ((u & 0x7fffffffu) > 0x7f800000u) ? nan : rounded;
+}
+
+// ---- 128-bit global memory access ------------------------------------------
+__device__ __forceinline__ uint4 ld128(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+__device__ __forceinline__ void st128(void* p, uint4 v) { *reinterpret_cast<uint4*>(p) = v; }
+
+// Load N = 16 consecutive elements of a fp32 or bf16 tensor as fp32.
+template <bool BF16>
+__device__ __forceinline__ void load16(const void* base, int64_t e0, float (&x)[16]) {
+  if constexpr (BF16) {
+    const uint16_t* p = reinterpret_cast<const uint16_t*>(base) + e0;
+#pragma unroll
+    for (int c = 0; c < 2; c++) {
+      uint4 t = ld128(p + 8 * c);
+      uint32_t w4[4] = {t.x, t.y, t.z, t.w};
+#pragma unroll
+      for (int k = 0; k < 4; k++) {
+        x[8 * c + 2 * k] = as_f32(w4[k] << 16);
+        x[8 * c + 2 * k + 1] = as_f32(w4[k] & 0xffff0000u);
+      }
+    }
+  } else {
+    const float* p = reinterpret_cast<const float*>(base) + e0;
+#pragma unroll
+    for (int c = 0; c < 4; c++) {
+      uint4 t = ld128(p + 4 * c);
+      x[4 * c] = as_f32(t.x);
+      x[4 * c + 1] = as_f32(t.y);
+      x[4 * c + 2] = as_f32(t.z);
+      x[4 * c + 3] = as_f32(t.w);
+    }
+  }
+}
+
+template <bool BF16>
+__device__ __forceinline__ void store16(void* base, int64_t e0, const float (&x)[16]) {
+  if constexpr (BF16) {
+    uint16_t* p = reinterpret_cast<uint16_t*>(base) + e0;
+#pragma unroll
+    for (int c = 0; c < 2; c++) {
+      uint32_t w4[4];
+#pragma unroll
+      for (int k = 0; k < 4; k++)
+        w4[k] = f32_to_bf16_bits(x[8 * c + 2 * k]) | (f32_to_bf16_bits(x[8 * c + 2 * k + 1]) << 16);
+      st128(p + 8 * c, make_uint4(w4[0], w4[1], w4[2], w4[3]));
+    }
+  } else {
+    float* p = reinterpret_cast<float*>(base) + e0;
+#pragma unroll
+    for (int c = 0; c < 4; c++)
+      st128(p + 4 * c, make_uint4(as_u32(x[4 * c]), as_u32(x[4 * c + 1]), as_u32(x[4 * c + 2]),
+                                  as_u32(x[4 * c + 3])));
+  }
+}
+
+// 16 consecutive W elements held in their storage format (bf16: 8 packed
+// dwords) and widened to fp32 on use.
+template <bool BF16>
+struct WRegs;
+template <>
+struct WRegs<true> {
+  uint32_t d[8];
+  __device__ __forceinline__ void load(const void* base, int64_t e0) {
+    const uint16_t* p = reinterpret_cast<const uint16_t*>(base) + e0;
+    uint4 a = ld128(p), b = ld128(p + 8);
+    d[0] = a.x; d[1] = a.y; d[2] = a.z; d[3] = a.w;
+    d[4] = b.x; d[5] = b.y; d[6] = b.z; d[7] = b.w;
+  }
+  __device__ __forceinline__ float get(int i) const {
+    return (i & 1) ? as_f32(d[i >> 1] & 0xffff0000u) : as_f32(d[i >> 1] << 16);
+  }
+};
+template <>
+struct WRegs<false> {
+  float f[16];
+  __device__ __forceinline__ void load(const void* base, int64_t e0) { load16<false>(base, e0, f); }
+  __device__ __forceinline__ float get(int i) const { return f[i]; }
+};
+
+// ---- DPP exchanges (GFX9 encodings; all stay inside a row of 16 lanes) ------
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141; // lane i <-> 7 - i inside each 8
+constexpr int kDppMirror = 0x140;     // lane i <-> 15 - i inside each 16
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float x) { return as_f32(dpp_u32<CTRL>(as_u32(x))); }
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double x) {
+  uint64_t u = __double_as_longlong(x);
+  uint32_t lo = dpp_u32<CTRL>((uint32_t)u), hi = dpp_u32<CTRL>((uint32_t)(u >> 32));
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// All-reduce over aligned runs of L consecutive lanes (L in 1, 2, 4, 8, 16).
+// The patterns pair lanes symmetrically, and IEEE addition / min / max are
+// commutative, so every lane of a run ends with a bit-identical result.
+template <int L>
+__device__ __forceinline__ float run_min(float x) {
+  if constexpr (L >= 2) x = fminf(x, dpp_f32<kDppXor1>(x));
+  if constexpr (L >= 4) x = fminf(x, dpp_f32<kDppXor2>(x));
+  if constexpr (L >= 8) x = fminf(x, dpp_f32<kDppHalfMirror>(x));
+  if constexpr (L >= 16) x = fminf(x, dpp_f32<kDppMirror>(x));
+  return x;
+}
+template <int L>
+__device__ __forceinline__ float run_max(float x) {
+  if constexpr (L >= 2) x = fmaxf(x, dpp_f32<kDppXor1>(x));
+  if constexpr (L >= 4) x = fmaxf(x, dpp_f32<kDppXor2>(x));
+  if constexpr (L >= 8) x = fmaxf(x, dpp_f32<kDppHalfMirror>(x));
+  if constexpr (L >= 16) x = fmaxf(x, dpp_f32<kDppMirror>(x));
+  return x;
+}
+template <int L>
+__device__ __forceinline__ double run_sum(double x) {
+  if constexpr (L >= 2) x = x + dpp_f64<kDppXor1>(x);
+  if constexpr (L >= 4) x = x + dpp_f64<kDppXor2>(x);
+  if constexpr (L >= 8) x = x + dpp_f64<kDppHalfMirror>(x);
+  if constexpr (L >= 16) x = x + dpp_f64<kDppMirror>(x);
+  return x;
+}
+template <int L>
+__device__ __forceinline__ double run_min_f64(double x) {
+  if constexpr (L >= 2) x = fmin(x, dpp_f64<kDppXor1>(x));
+  if constexpr (L >= 4) x = fmin(x, dpp_f64<kDppXor2>(x));
+  if constexpr (L >= 8) x = fmin(x, dpp_f64<kDppHalfMirror>(x));
+  if constexpr (L >= 16) x = fmin(x, dpp_f64<kDppMirror>(x));
+  return x;
+}
+
+// A non-negative score with the candidate index in its 4 low mantissa bits:
+// ordering keys as doubles orders by score (to 2^-48 relative) and then by
+// index, so a min over keys is the argmin with ties to the lowest index.
+__device__ __forceinline__ double make_key(double score, int k) {
+  score = fmax(score, 0.0);
+  uint64_t u = (uint64_t)__double_as_longlong(score);
+  u = (u & ~(uint64_t)15) | (uint64_t)(k & 15);
+  return __longlong_as_double((long long)u);
+}
+__device__ __forceinline__ int key_index(double key) {
+  return (int)((uint64_t)__double_as_longlong(key) & 15);
+}
+
+// Orders this wave's LDS accesses across lanes: writes issued before the
+// fence are visible to reads issued after it (a wavefront executes its LDS
+// instructions in order; the fence stops the compiler from reordering them).
+__device__ __forceinline__ void wave_lds_fence() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+}  // namespace quasar

@@ -1,0 +1,330 @@
+// int_kernel.hip -- QUASAR reconstruction for asymmetric INT-b groups on gfx950.
+//
+// Algorithm 1 (Sec. 4.1.2) for every group of G weights along a row:
+//   c, rho from the group's min/max; for each clip factor f: codes on
+//   [c - f rho, c + f rho] (Eq. rtn), weighted least-squares (s, z) (Eq. ridgefit),
+//   score sum h (s q + z - w)^2 (Eq. fisher-obj); emit the argmin.
+//
+// Work decomposition: a group is owned by L = G/16 consecutive lanes of one
+// wavefront, each holding 16 consecutive weights in registers (G = 128: 8 lanes,
+// G = 64: 4 lanes); a wavefront processes 64/L groups.  W, v (and g) are read
+// from HBM exactly once with 128-bit loads; codes, r, v' are written once.
+//
+// Per weight and clip: fp32 code (fma, rint, clamp -- the same fp32 recipe as
+// the oracle, so codes are bit-identical) and three fp64 moments
+// (sum v q, sum v q^2, sum v q w).  fp64 keeps the 2x2 normal equations and the
+// expanded score exact enough to reproduce the argmin under heavy-tailed
+// saliency (the weighted code variance can be 1e-4 of its mean square).
+// Moments are combined across the L lanes through LDS (a transpose: each lane
+// sums the partials of the clips it owns), the owner solves its clips, and an
+// argmin over keys (score with the clip index in the low bits) picks the winner
+// with DPP.  No atomics; every result has a single owner, so runs are
+// deterministic.
+#include <type_traits>
+
+#include "device_common.h"
+#include "quasar_internal.h"
+
+namespace quasar {
+namespace {
+
+constexpr int N = 16;  // weights per lane
+
+template <bool W_BF16, int EMA, int BITS, int G, int KC, bool MULTI>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu((KC > 8 || MULTI) ? 3 : 4)))
+void int_reconstruct_kernel(IntParams p) {
+  constexpr int L = G / N;          // lanes per group
+  constexpr int GPW = 64 / L;       // groups per wavefront
+  constexpr int QMAX = (1 << BITS) - 1;
+  constexpr int OWN = (KC + L - 1) / L;  // clips owned per lane per chunk
+  constexpr float kQmax = (float)QMAX;
+  constexpr float kBeta = 0.5f * (float)QMAX;
+
+  __shared__ double s_red[kThreads / 64][64 * KC];
+  __shared__ float s_alpha[kMaxClips], s_clip[kMaxClips];
+  __shared__ float s_win[kThreads / 64][GPW][4];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int j = lane % L, slot = lane / L;
+  const int K = p.n_clips;
+
+  if (tid < kMaxClips) {  // the host pads both tables to kMaxClips entries
+    s_alpha[tid] = p.alpha[tid];
+    s_clip[tid] = p.clip[tid];
+  }
+  __syncthreads();
+
+  int64_t gid = ((int64_t)blockIdx.x * (kThreads / 64) + wave) * GPW + slot;
+  const bool active = gid < p.n_groups;
+  if (!active) gid = p.n_groups - 1;  // recompute the last group; nothing is stored
+  const int64_t e0 = gid * G + (int64_t)j * N;
+
+  // ---- load (each byte of W, v, g once) ------------------------------------
+  // W stays in its storage format in registers (bf16: 8 dwords) and is widened
+  // on use, which keeps the kernel inside 128 VGPRs (4 waves per SIMD).
+  WRegs<W_BF16> wr;
+  wr.load(p.W, e0);
+  float v[N];
+  load16<false>(p.v, e0, v);
+  if constexpr (EMA != 0) {
+    float g[N];
+    load16<EMA == 1>(p.g, e0, g);
+#pragma unroll
+    for (int i = 0; i < N; i++) {
+      // v' = beta2 v + (1 - beta2) g^2 in the oracle's fp32 order
+      float t = g[i] * g[i];
+      float u = p.omb2 * t;
+      v[i] = __builtin_fmaf(p.beta2, v[i], u);
+    }
+    if (active) store16<false>(p.v, e0, v);
+  }
+
+  // ---- group range (Alg. 1, first line) ------------------------------------
+  float mn = wr.get(0), mx = wr.get(0);
+#pragma unroll
+  for (int i = 1; i < N; i++) {
+    mn = fminf(mn, wr.get(i));
+    mx = fmaxf(mx, wr.get(i));
+  }
+  mn = run_min<L>(mn);
+  mx = run_max<L>(mx);
+  const bool constant = (mx == mn);
+  const float c = 0.5f * (mx + mn);
+  const float rho = 0.5f * (mx - mn);
+  const float rrho = 1.0f / rho;
+  const float nc = -(c * rrho);
+  // normalised position u = fmaf(w, 1/rho, -c/rho), recomputed where used
+
+  // ---- clip-independent moments (fp64), accumulated in the first pass --------
+  double Sv = 0.0, Svw = 0.0, Svww = 0.0;
+  double best_key = __longlong_as_double(0x7ff0000000000000ll);  // +inf
+  float best_a = 0.f, best_b = 0.f, best_err = 0.f;
+  double thr = 0.0;
+  double* red = s_red[wave];
+
+  // One pass over the lane's 16 weights for clips k0 .. k0+KC-1 (entries past
+  // the last clip repeat it and are never selected).
+  auto pass = [&](const int k0, auto first_tag) {
+    constexpr bool FIRST = decltype(first_tag)::value;
+    float al[KC];
+#pragma unroll
+    for (int kk = 0; kk < KC; kk++)
+      al[kk] = uniform_f32(s_alpha[(k0 + kk) < kMaxClips ? (k0 + kk) : kMaxClips - 1]);
+
+    double acc[KC][3];
+#pragma unroll
+    for (int kk = 0; kk < KC; kk++) acc[kk][0] = acc[kk][1] = acc[kk][2] = 0.0;
+
+#pragma unroll
+    for (int i = 0; i < N; i++) {
+      float vi = v[i], wi = wr.get(i);
+      if constexpr (!FIRST) {
+        // keep the per-weight fp64 values inside this pass (not hoisted and
+        // held across passes)
+        asm volatile("" : "+v"(vi), "+v"(wi));
+      }
+      const float ui = __builtin_fmaf(wi, rrho, nc);
+      const double V = (double)vi, Wd = (double)wi;
+      const double VW = V * Wd;
+      if constexpr (FIRST) {
+        Sv += V;
+        Svw += VW;
+        Svww = __builtin_fma(VW, Wd, Svww);
+      }
+#pragma unroll
+      for (int kk = 0; kk < KC; kk++) {
+        float x = __builtin_fmaf(ui, al[kk], kBeta);
+        float q = __builtin_rintf(x);
+        q = __builtin_amdgcn_fmed3f(q, 0.0f, kQmax);
+        const double Q = (double)q;
+        const double VQ = V * Q;
+        acc[kk][0] += VQ;
+        acc[kk][1] = __builtin_fma(VQ, Q, acc[kk][1]);
+        acc[kk][2] = __builtin_fma(VW, Q, acc[kk][2]);
+      }
+      // one weight at a time: interleaving weights buys no latency hiding that
+      // the other wavefronts on the SIMD do not already give, and costs VGPRs
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (FIRST) {
+      Sv = run_sum<L>(Sv);
+      Svw = run_sum<L>(Svw);
+      Svww = run_sum<L>(Svww);
+      thr = 1e-12 * Sv * Sv * (double)QMAX * (double)QMAX;
+    }
+
+    // ---- combine the L partials: lane j sums the clips kk = j + L t ---------
+    double own[OWN][3];
+#pragma unroll
+    for (int m = 0; m < 3; m++) {
+#pragma unroll
+      for (int kk = 0; kk < KC; kk++) red[(slot * KC + kk) * L + j] = acc[kk][m];
+      wave_lds_fence();
+#pragma unroll
+      for (int t = 0; t < OWN; t++) {
+        const int kk = j + L * t;
+        const int kr = kk < KC ? kk : KC - 1;
+        double s = 0.0;
+#pragma unroll
+        for (int jj = 0; jj < L; jj++) s += red[(slot * KC + kr) * L + jj];
+        own[t][m] = s;
+      }
+      wave_lds_fence();
+    }
+
+    // ---- solve the owned clips (Eq. ridgefit) and score them ----------------
+#pragma unroll
+    for (int t = 0; t < OWN; t++) {
+      const int kk = j + L * t;
+      const int k = k0 + kk;
+      if (kk < KC && k < K) {
+        const double A0 = own[t][0], A1 = own[t][1], A2 = own[t][2];
+        const double D = Sv * A1 - A0 * A0;
+        double a, b;
+        if (Sv == 0.0 || D <= thr) {
+          // no saliency, or all of it on one code: the slope is undetermined
+          // and the RTN step of this range is kept
+          const float f = s_clip[k];
+          const float fr = f * rho;
+          const float s_rtn = (2.0f * fr) / kQmax;
+          a = (double)s_rtn;
+          b = (Sv == 0.0) ? (double)(c - fr) : (Svw - a * A0) / Sv;
+        } else {
+          a = (Sv * A2 - A0 * Svw) / D;
+          b = (Svw - a * A0) / Sv;
+        }
+        const float af = (float)a, bf = (float)b;
+        const double ad = (double)af, bd = (double)bf;
+        // Eq. fisher-obj of the emitted fp32 dequantiser, expanded in fp64
+        const double score =
+            Svww + ad * (ad * A1 + 2.0 * bd * A0 - 2.0 * A2) + bd * (bd * Sv - 2.0 * Svw);
+        const double key = make_key(score, k);
+        if (key < best_key) {
+          best_key = key;
+          best_a = af;
+          best_b = bf;
+          best_err = (float)fmax(score, 0.0);
+        }
+      }
+    }
+  };
+  pass(0, std::true_type{});
+  if constexpr (MULTI) {
+    for (int k0 = KC; k0 < K; k0 += KC) pass(k0, std::false_type{});
+  }
+
+  // ---- argmin over the group's lanes, winner broadcast -----------------------
+  const double gkey = run_min_f64<L>(best_key);
+  const int kstar = key_index(gkey);
+  float* win = s_win[wave][slot];
+  if (best_key == gkey) {  // exactly one lane of the group owns clip kstar
+    win[0] = best_a;
+    win[1] = best_b;
+    win[2] = best_err;
+  }
+  wave_lds_fence();
+  float a = win[0], b = win[1], errv = win[2];
+  const float alpha = s_alpha[kstar];
+  int kout = kstar;
+  if (constant) {  // every code 0, z = w: exact reconstruction
+    a = 0.0f;
+    b = mn;
+    errv = 0.0f;
+    kout = 0;
+  }
+
+  // ---- emit: codes of f*, r = fmaf(s, q, z) ---------------------------------
+  uint32_t qi[N];
+  float r[N];
+#pragma unroll
+  for (int i = 0; i < N; i++) {
+    const float ui = __builtin_fmaf(wr.get(i), rrho, nc);
+    float x = __builtin_fmaf(ui, alpha, kBeta);
+    float q = __builtin_amdgcn_fmed3f(__builtin_rintf(x), 0.0f, kQmax);
+    if (constant) q = 0.0f;
+    qi[i] = (uint32_t)q;
+    r[i] = constant ? mn : __builtin_fmaf(a, q, b);
+  }
+  if (!active) return;
+  if (p.r) store16<W_BF16>(p.r, e0, r);
+  if constexpr (BITS == 4) {
+    uint32_t lo = 0, hi = 0;
+#pragma unroll
+    for (int i = 0; i < 8; i++) {
+      lo |= qi[i] << (4 * i);
+      hi |= qi[8 + i] << (4 * i);
+    }
+    *reinterpret_cast<uint2*>(p.codes + gid * (G / 2) + j * 8) = make_uint2(lo, hi);
+  } else if constexpr (BITS == 2) {
+    uint32_t x = 0;
+#pragma unroll
+    for (int i = 0; i < N; i++) x |= qi[i] << (2 * i);
+    *reinterpret_cast<uint32_t*>(p.codes + gid * (G / 4) + j * 4) = x;
+  } else {  // BITS == 3: 48 bits per lane at byte offset 6 j of the group's stream
+    uint64_t x = 0;
+#pragma unroll
+    for (int i = 0; i < N; i++) x |= (uint64_t)qi[i] << (3 * i);
+    uint16_t* dst = reinterpret_cast<uint16_t*>(p.codes + gid * (3 * G / 8) + j * 6);
+    dst[0] = (uint16_t)x;
+    dst[1] = (uint16_t)(x >> 16);
+    dst[2] = (uint16_t)(x >> 32);
+  }
+  if (j == 0) {
+    p.scales[gid] = a;
+    p.zeros[gid] = b;
+    if (p.best_clip) p.best_clip[gid] = (uint8_t)kout;
+    if (p.err) p.err[gid] = errv;
+  }
+}
+
+template <bool W_BF16, int EMA, int BITS, int G>
+hipError_t launch_kc(const IntParams& p, hipStream_t s) {
+  constexpr int L = G / N;
+  constexpr int groups_per_block = kThreads / L;
+  const int64_t blocks = (p.n_groups + groups_per_block - 1) / groups_per_block;
+  // clips per pass: one pass of 4, 8 or 12 clips when K <= 12 (entries past K
+  // repeat the last clip and are never selected); passes of 8 beyond that
+  const int K = p.n_clips;
+  const dim3 grid((unsigned)blocks), block(kThreads);
+  if (K <= 4)
+    hipLaunchKernelGGL((int_reconstruct_kernel<W_BF16, EMA, BITS, G, 4, false>), grid, block, 0, s, p);
+  else if (K <= 8)
+    hipLaunchKernelGGL((int_reconstruct_kernel<W_BF16, EMA, BITS, G, 8, false>), grid, block, 0, s, p);
+  else if (K <= 12)
+    hipLaunchKernelGGL((int_reconstruct_kernel<W_BF16, EMA, BITS, G, 12, false>), grid, block, 0, s, p);
+  else
+    hipLaunchKernelGGL((int_reconstruct_kernel<W_BF16, EMA, BITS, G, 8, true>), grid, block, 0, s, p);
+  return hipGetLastError();
+}
+
+template <bool W_BF16, int EMA, int BITS>
+hipError_t launch_g(const IntParams& p, int group, hipStream_t s) {
+  return group == 64 ? launch_kc<W_BF16, EMA, BITS, 64>(p, s) : launch_kc<W_BF16, EMA, BITS, 128>(p, s);
+}
+
+template <bool W_BF16, int EMA>
+hipError_t launch_b(const IntParams& p, int bits, int group, hipStream_t s) {
+  switch (bits) {
+    case 2: return launch_g<W_BF16, EMA, 2>(p, group, s);
+    case 3: return launch_g<W_BF16, EMA, 3>(p, group, s);
+    default: return launch_g<W_BF16, EMA, 4>(p, group, s);
+  }
+}
+
+template <bool W_BF16>
+hipError_t launch_e(const IntParams& p, int bits, int group, int ema_mode, hipStream_t s) {
+  switch (ema_mode) {
+    case 1: return launch_b<W_BF16, 1>(p, bits, group, s);
+    case 2: return launch_b<W_BF16, 2>(p, bits, group, s);
+    default: return launch_b<W_BF16, 0>(p, bits, group, s);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_int(const IntParams& p, int bits, int group, bool w_bf16, int ema_mode, hipStream_t s) {
+  return w_bf16 ? launch_e<true>(p, bits, group, ema_mode, s) : launch_e<false>(p, bits, group, ema_mode, s);
+}
+
+}  // namespace quasar

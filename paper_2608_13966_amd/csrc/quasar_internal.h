@@ -1,0 +1,57 @@
+// quasar_internal.h -- internal declarations shared by the HIP translation units
+// of libquasar.so (not part of the public C ABI, which is include/quasar.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace quasar {
+
+constexpr int kMaxClips = 16;
+constexpr int kThreads = 256;   // 4 wavefronts of 64 lanes per workgroup
+
+// Per-call parameters of the INT-b kernel (passed by value as the kernel argument).
+struct IntParams {
+  const void* W;        // [rows, cols] fp32 or bf16
+  float* v;             // [rows, cols] fp32 saliency (overwritten with the EMA when g != NULL)
+  const void* g;        // gradient or NULL
+  uint8_t* codes;       // packed codes
+  float* scales;        // [groups] fp32 s
+  float* zeros;         // [groups] fp32 z
+  void* r;              // [rows, cols] in W's dtype, or NULL
+  uint8_t* best_clip;   // [groups] or NULL
+  float* err;           // [groups] or NULL
+  int64_t n_groups;
+  float beta2, omb2;    // EMA decay and 1 - beta2 (fp32)
+  int n_clips;
+  float alpha[kMaxClips];  // qmax / (2 f_k), fp32 division on the host
+  float clip[kMaxClips];   // f_k
+};
+
+// Per-call parameters of the NVFP4 kernels.
+struct Nvfp4Params {
+  const void* W;
+  float* v;
+  const void* g;
+  uint8_t* codes;       // two E2M1 codes per byte
+  uint8_t* scales;      // [blocks] E4M3 byte
+  void* r;
+  uint8_t* best_clip;
+  float* err;
+  float* tensor_scale;  // [1] output S_t
+  const float* amax;    // [1] tensor absmax (caller's, or the workspace filled by the amax pass)
+  int64_t n_blocks;
+  float beta2, omb2;
+  int n_clips;
+  float c6[kMaxClips];  // 6 / f_k, fp32 division on the host
+  float clip[kMaxClips];
+};
+
+// Launchers (return the hipGetLastError() of the launches).
+hipError_t launch_int(const IntParams& p, int bits, int group, bool w_bf16, int ema_mode, hipStream_t s);
+hipError_t launch_nvfp4(const Nvfp4Params& p, bool w_bf16, int ema_mode, hipStream_t s);
+// amax over n elements of W into *ws (as fp32 bits); clears *ws first.
+hipError_t launch_absmax(const void* W, bool w_bf16, int64_t n, unsigned* ws, hipStream_t s);
+
+// ema_mode: 0 = no gradient, 1 = bf16 gradient, 2 = fp32 gradient
+}  // namespace quasar

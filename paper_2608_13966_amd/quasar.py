@@ -1,0 +1,195 @@
+"""ctypes binding of libquasar.so (the C ABI in include/quasar.h).
+
+Argument marshalling only: every step of the reconstruction runs in the HIP
+kernels behind ``quasar_reconstruct``.  Tensors are torch tensors on the GPU
+(torch supplies device memory and the current stream); there is no CPU path,
+and a missing library raises instead of falling back.
+
+The functions ``quasar_reconstruct``, ``quasar_check``, ``quasar_num_groups``,
+``quasar_codes_bytes``, ``quasar_workspace_bytes``, ``quasar_status_string`` and
+``quasar_version`` mirror the C entry points one to one; ``reconstruct`` is a
+convenience wrapper that allocates the outputs and calls ``quasar_reconstruct``.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import threading
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libquasar.so")
+
+OK, ERR_ARG, ERR_SHAPE, ERR_ALIGN, ERR_FORMAT, ERR_WORKSPACE, ERR_DEVICE = 0, -1, -2, -3, -4, -5, -6
+F32, BF16 = 0, 1
+INT, NVFP4 = 0, 1
+MAX_CLIPS = 16
+
+EXPORTS = ("quasar_reconstruct", "quasar_check", "quasar_num_groups", "quasar_codes_bytes",
+           "quasar_workspace_bytes", "quasar_status_string", "quasar_version")
+
+
+class QuasarError(RuntimeError):
+    def __init__(self, status: int, where: str = "quasar_reconstruct"):
+        self.status = status
+        super().__init__(f"{where}: status {status} ({quasar_status_string(status)})")
+
+
+class Desc(C.Structure):
+    _fields_ = [("rows", C.c_int64), ("cols", C.c_int64), ("w_dtype", C.c_int32), ("format", C.c_int32),
+                ("bits", C.c_int32), ("group", C.c_int32), ("clip_ratios", C.POINTER(C.c_float)),
+                ("n_clips", C.c_int32), ("g_dtype", C.c_int32), ("beta2", C.c_float)]
+
+
+_lib = None
+_lock = threading.Lock()
+
+
+def lib():
+    """Open libquasar.so (built in-tree by ``paper_2608_13966_amd.build``)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2608_13966_amd.build` "
+                                   "(there is no fallback path)")
+            L = C.CDLL(LIB_PATH)
+            vp, dp = C.c_void_p, C.POINTER(Desc)
+            L.quasar_reconstruct.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, C.c_size_t, vp]
+            L.quasar_reconstruct.restype = C.c_int
+            L.quasar_check.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, C.c_size_t]
+            L.quasar_check.restype = C.c_int
+            L.quasar_num_groups.argtypes = [dp]
+            L.quasar_num_groups.restype = C.c_int64
+            L.quasar_codes_bytes.argtypes = [dp]
+            L.quasar_codes_bytes.restype = C.c_size_t
+            L.quasar_workspace_bytes.argtypes = [dp, C.c_int]
+            L.quasar_workspace_bytes.restype = C.c_size_t
+            L.quasar_status_string.argtypes = [C.c_int]
+            L.quasar_status_string.restype = C.c_char_p
+            L.quasar_version.argtypes = []
+            L.quasar_version.restype = C.c_char_p
+            _lib = L
+    return _lib
+
+
+class Descriptor:
+    """A quasar_desc plus the host clip array it points to (kept alive here)."""
+
+    def __init__(self, rows, cols, *, fmt="int", bits=4, group=128, clips=(1.0,), w_dtype=BF16,
+                 g_dtype=BF16, beta2=0.999):
+        self.clips = np.ascontiguousarray(np.asarray(clips, dtype=np.float32))
+        nv = fmt == "nvfp4"
+        self.desc = Desc(int(rows), int(cols), int(w_dtype), NVFP4 if nv else INT, 4 if nv else int(bits),
+                         16 if nv else int(group), self.clips.ctypes.data_as(C.POINTER(C.c_float)),
+                         int(self.clips.size), int(g_dtype), float(beta2))
+
+    @property
+    def ref(self):
+        return C.byref(self.desc)
+
+
+def _p(x):
+    """Device pointer of a tensor (or raw int / None)."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def quasar_reconstruct(d: Descriptor, W, v, g, codes, scales, zeros, r, best_clip, err, tensor_scale,
+                       tensor_amax, workspace, workspace_bytes: int, stream) -> int:
+    return lib().quasar_reconstruct(d.ref, _p(W), _p(v), _p(g), _p(codes), _p(scales), _p(zeros), _p(r),
+                                    _p(best_clip), _p(err), _p(tensor_scale), _p(tensor_amax), _p(workspace),
+                                    int(workspace_bytes), stream)
+
+
+def quasar_check(d: Descriptor, W, v, g, codes, scales, zeros, r, best_clip, err, tensor_scale, tensor_amax,
+                 workspace, workspace_bytes: int) -> int:
+    return lib().quasar_check(d.ref, _p(W), _p(v), _p(g), _p(codes), _p(scales), _p(zeros), _p(r),
+                              _p(best_clip), _p(err), _p(tensor_scale), _p(tensor_amax), _p(workspace),
+                              int(workspace_bytes))
+
+
+def quasar_num_groups(d: Descriptor) -> int:
+    return int(lib().quasar_num_groups(d.ref))
+
+
+def quasar_codes_bytes(d: Descriptor) -> int:
+    return int(lib().quasar_codes_bytes(d.ref))
+
+
+def quasar_workspace_bytes(d: Descriptor, has_tensor_amax: bool) -> int:
+    return int(lib().quasar_workspace_bytes(d.ref, int(bool(has_tensor_amax))))
+
+
+def quasar_status_string(status: int) -> str:
+    return lib().quasar_status_string(int(status)).decode()
+
+
+def quasar_version() -> str:
+    return lib().quasar_version().decode()
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def alloc_outputs(d: Descriptor, W, *, want_r=True, want_diag=True, has_amax=False):
+    """Allocate the output buffers of one call (torch, on W's device)."""
+    import torch
+    dev = W.device
+    ng = quasar_num_groups(d)
+    nv = d.desc.format == NVFP4
+    out = {"codes": torch.empty(quasar_codes_bytes(d), dtype=torch.uint8, device=dev)}
+    if nv:
+        out["scales"] = torch.empty(ng, dtype=torch.uint8, device=dev)
+        out["zeros"] = None
+        out["tensor_scale"] = torch.empty(4, dtype=torch.float32, device=dev)
+    else:
+        out["scales"] = torch.empty(ng, dtype=torch.float32, device=dev)
+        out["zeros"] = torch.empty(ng, dtype=torch.float32, device=dev)
+        out["tensor_scale"] = None
+    out["r"] = torch.empty_like(W) if want_r else None
+    out["best_clip"] = torch.empty(ng, dtype=torch.uint8, device=dev) if want_diag else None
+    out["err"] = torch.empty(ng, dtype=torch.float32, device=dev) if want_diag else None
+    wsb = quasar_workspace_bytes(d, has_amax)
+    out["workspace"] = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev) if wsb else None
+    out["workspace_bytes"] = wsb
+    return out
+
+
+def reconstruct(W, v, g=None, *, fmt="int", bits=4, group=128, clips=(1.0,), beta2=0.999, tensor_amax=None,
+                want_r=True, want_diag=True, out=None, stream=None):
+    """Reconstruct W (torch tensor [rows, cols], fp32 or bf16, on the GPU).
+
+    ``v`` (fp32, same shape) is overwritten with the EMA when ``g`` is given.
+    Returns the dict of output tensors (see ``alloc_outputs``).  The call is
+    asynchronous on ``stream`` (default: torch's current stream).
+    """
+    import torch
+    if W.dim() != 2 or v.shape != W.shape or v.dtype != torch.float32:
+        raise ValueError("W must be 2-D and v an fp32 tensor of the same shape")
+    for t in (W, v, g):
+        if t is not None and not t.is_contiguous():
+            raise ValueError("tensors must be contiguous")
+    d = Descriptor(W.shape[0], W.shape[1], fmt=fmt, bits=bits, group=group, clips=clips, w_dtype=_dtype_code(W),
+                   g_dtype=_dtype_code(g) if g is not None else BF16, beta2=beta2)
+    if out is None:
+        out = alloc_outputs(d, W, want_r=want_r, want_diag=want_diag, has_amax=tensor_amax is not None)
+    if stream is None:
+        stream = torch.cuda.current_stream(W.device).cuda_stream
+    s = quasar_reconstruct(d, W, v, g, out["codes"], out["scales"], out["zeros"], out["r"], out["best_clip"],
+                           out["err"], out["tensor_scale"], tensor_amax, out["workspace"], out["workspace_bytes"],
+                           stream)
+    if s != OK:
+        raise QuasarError(s)
+    out["desc"] = d
+    return out

@@ -1,0 +1,261 @@
+"""GPU parity: libquasar.so (through its C ABI) against the CPU oracle on the
+same seeded inputs.  See tests/_parity.py for the protocol."""
+import itertools
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_13966_amd import quasar as Q
+from paper_2608_13966_amd import synth
+from tests import _parity
+
+pytestmark = pytest.mark.gpu
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+STATS = os.path.join(ROOT, "gpurun_out", "parity_stats.jsonl")
+THREADS = min(16, os.cpu_count() or 1)
+
+
+def record(name, st):
+    os.makedirs(os.path.dirname(STATS), exist_ok=True)
+    with open(STATS, "a") as f:
+        f.write(json.dumps({"case": name, **{k: int(v) for k, v in st.items()}}) + "\n")
+    print(name, dict(st), flush=True)
+
+
+def host(t):
+    return None if t is None else synth.to_host(t)
+
+
+def run_case(name, rows, cols, seed, *, fmt="int", bits=4, group=128, clips=(1.0, 0.9, 0.8), w_bf16=True,
+             ema=False, g_fp32=False, row_step=1, supply_amax=False, want_r=True, W=None, v=None, g=None):
+    dev = "cuda"
+    if W is None:
+        W, v, g = synth.gen_matrix(rows, cols, seed, w_bf16=w_bf16, ema=ema, device=dev)
+        if g is not None and g_fp32:
+            g = g.float()
+    Wh, vh, gh = host(W), host(v), host(g)
+    amax_t = None
+    amax = None
+    if fmt == "nvfp4":
+        amax = oracle.absmax(Wh)
+        if supply_amax:
+            amax_t = torch.tensor([amax, 0, 0, 0], dtype=torch.float32, device=dev)
+    print(f"[case] {name} shape={tuple(W.shape)} fmt={fmt} bits={bits} group={group} K={len(clips)} "
+          f"w={'bf16' if w_bf16 else 'f32'} ema={ema}", flush=True)
+    out = Q.reconstruct(W, v, g, fmt=fmt, bits=bits, group=group, clips=clips, tensor_amax=amax_t, want_r=want_r)
+    torch.cuda.synchronize()
+    G = 16 if fmt == "nvfp4" else group
+    nb = 4 if fmt == "nvfp4" else bits
+    R, Cc = W.shape
+    rows_idx = np.arange(0, R, row_step)
+    gpr = Cc // G
+    gidx = (rows_idx[:, None] * gpr + np.arange(gpr)[None, :]).ravel()
+    codes = out["codes"].cpu().numpy().reshape(R, Cc * nb // 8)[rows_idx].ravel()
+    gpu = {"codes": codes, "scales": out["scales"].cpu().numpy()[gidx],
+           "best_clip": out["best_clip"].cpu().numpy()[gidx], "err": out["err"].cpu().numpy()[gidx],
+           "r": host(out["r"])[rows_idx] if want_r else None}
+    if fmt == "nvfp4":
+        gpu["tensor_scale"] = out["tensor_scale"].cpu().numpy()[0]
+    else:
+        gpu["zeros"] = out["zeros"].cpu().numpy()[gidx]
+    v_gpu = host(v)[rows_idx] if g is not None else None
+    o = oracle.reconstruct(Wh[rows_idx], vh[rows_idx], fmt=fmt, bits=bits, group=group, clips=clips,
+                           g=None if gh is None else gh[rows_idx], beta2=0.999, tensor_amax=amax,
+                           want_scores=True, want_diag=True, n_threads=THREADS)
+    h = o["v_out"] if g is not None else vh[rows_idx]
+    fails, st = _parity.compare(fmt=fmt, bits=bits, group=group, W=Wh[rows_idx], h=h, o=o, gpu=gpu,
+                                v_out_gpu=v_gpu)
+    record(name, st)
+    assert not fails, "\n".join(fails)
+    # exceptions are rare by construction
+    assert st["near_tie"] + st["near_e4m3"] <= max(2, 0.001 * st["groups"]), dict(st)
+    return out, o
+
+
+# --------------------------------------------------------------------------- configs
+
+def _wl(name):
+    return synth.workloads()[name]
+
+
+def test_c1_single_matrix_full():
+    wl = _wl("c1")
+    (_, r, c), = wl.shapes
+    run_case("c1", r, c, wl.seeds[0], fmt=wl.fmt, bits=wl.bits, group=wl.group, clips=wl.clips,
+             w_bf16=wl.w_bf16, ema=wl.ema)
+
+
+def test_c2_qwen_layer_set_full():
+    wl = _wl("c2")
+    for (name, r, c), seed in zip(wl.shapes, wl.seeds):
+        run_case(f"c2.{name}", r, c, seed, fmt=wl.fmt, bits=wl.bits, group=wl.group, clips=wl.clips,
+                 w_bf16=wl.w_bf16, ema=wl.ema)
+
+
+@pytest.mark.parametrize("wl_name", ["c3", "c4"])
+def test_llama_layer_set_sampled(wl_name):
+    """Full-size matrices in the benchmark's launch configuration; every 61st
+    row is checked against the oracle."""
+    wl = _wl(wl_name)
+    for (name, r, c), seed in zip(wl.shapes, wl.seeds):
+        run_case(f"{wl_name}.{name}", r, c, seed, fmt=wl.fmt, bits=wl.bits, group=wl.group, clips=wl.clips,
+                 w_bf16=wl.w_bf16, ema=wl.ema, row_step=61)
+        torch.cuda.empty_cache()
+
+
+def test_c5_first_and_last_layer_sampled():
+    wl = _wl("c5")
+    for (name, r, c), seed in zip(wl.shapes, wl.seeds):
+        if not (name.startswith("L0.") or name.startswith("L31.")):
+            continue
+        run_case(f"c5.{name}", r, c, seed, fmt=wl.fmt, bits=wl.bits, group=wl.group, clips=wl.clips,
+                 w_bf16=wl.w_bf16, ema=wl.ema, row_step=127)
+        torch.cuda.empty_cache()
+
+
+# --------------------------------------------------------------------------- coverage grid
+
+GRID = []
+for (fmt, bits, group), wb, ema, K in itertools.product(
+        [("int", 4, 128), ("int", 3, 128), ("int", 2, 64), ("int", 4, 64), ("int", 2, 128), ("int", 3, 64),
+         ("nvfp4", 4, 16)],
+        [True, False], ["none", "bf16", "f32"], [1, 5, 8, 12, 15]):
+    # keep the grid small: every format with every K, dtype/EMA combinations rotated
+    if (K + bits + group + int(wb) + ["none", "bf16", "f32"].index(ema)) % 3 != 0 and K not in (8, 12):
+        continue
+    GRID.append((fmt, bits, group, wb, ema, K))
+
+
+@pytest.mark.parametrize("fmt,bits,group,wb,ema,K", GRID)
+def test_grid_ragged(fmt, bits, group, wb, ema, K):
+    """Ragged shapes: the group count is not a multiple of the groups per
+    workgroup, so the last workgroup is partly idle."""
+    cols = 3 * (group if fmt == "int" else 128)
+    rows = 37
+    clips = tuple(synth.clip_grid(1.0, 0.3, K)) if K > 1 else (1.0,)
+    run_case(f"grid.{fmt}{bits}g{group}.{'bf16' if wb else 'f32'}.ema-{ema}.K{K}", rows, cols, 100 + K,
+             fmt=fmt, bits=bits, group=group, clips=clips, w_bf16=wb, ema=ema != "none", g_fp32=ema == "f32")
+
+
+def test_paper_clip_grid_int3():
+    """The paper's own grid: 15 factors 0.30, 0.35, ..., 1.00 (two passes)."""
+    clips = tuple(np.float32(x) for x in np.round(np.arange(1.0, 0.29, -0.05), 2))
+    assert len(clips) == 15
+    run_case("paper-grid.int3", 128, 1024, 7, bits=3, group=128, clips=clips, ema=True)
+
+
+# --------------------------------------------------------------------------- edge cases
+
+def _place(W, v):
+    return W.contiguous().cuda(), v.contiguous().cuda()
+
+
+def test_degenerate_groups():
+    torch.manual_seed(0)
+    W = (torch.randn(8, 512) * 0.02).float()
+    v = torch.rand(8, 512).float()
+    W[0, :128] = 0.25                 # constant group
+    W[1, 128:256] = -1.5              # constant group
+    v[2, :128] = 0.0                  # zero saliency
+    v[3, 128:256] = 0.0
+    v[3, 130] = 3.0                   # all saliency on one weight
+    v[4, 256:384] = 0.0
+    v[4, 300] = 1.0
+    v[4, 301] = 1.0                   # two weights (maybe one code)
+    W[5, 384:512] = torch.linspace(-1, 1, 128)   # uniform ramp
+    W[6, :128] = torch.tensor([0.0, 1.0] * 64)   # two values
+    Wg, vg = _place(W, v)
+    for bits in (2, 3, 4):
+        run_case(f"degenerate.int{bits}", 0, 0, 0, bits=bits, group=128, clips=(1.0, 0.75, 0.5),
+                 W=Wg, v=vg.clone(), w_bf16=False)
+    Wb = Wg.to(torch.bfloat16)
+    run_case("degenerate.int4.bf16", 0, 0, 0, bits=4, group=64, clips=(1.0, 0.75, 0.5), W=Wb, v=vg.clone())
+    # NVFP4: zero blocks and a zero tensor
+    Wn = Wg.clone()
+    Wn[7] = 0.0
+    run_case("degenerate.nvfp4", 0, 0, 0, fmt="nvfp4", clips=(1.0, 0.8, 0.6), W=Wn, v=vg.clone(), w_bf16=False)
+    run_case("zero-tensor.nvfp4", 0, 0, 0, fmt="nvfp4", clips=(1.0, 0.8), W=torch.zeros(2, 64, device="cuda"),
+             v=torch.ones(2, 64, device="cuda"), w_bf16=False)
+
+
+def test_tiny_shapes():
+    for rows, cols, bits, group in [(1, 64, 2, 64), (1, 128, 4, 128), (2, 64, 3, 64), (3, 16, 4, 16)]:
+        fmt = "nvfp4" if group == 16 else "int"
+        run_case(f"tiny.{rows}x{cols}.{fmt}", rows, cols, rows * cols, fmt=fmt, bits=bits, group=group,
+                 clips=(1.0, 0.8), ema=True)
+
+
+def test_nvfp4_supplied_amax_matches_computed():
+    W, v, _ = synth.gen_matrix(64, 512, 9, w_bf16=True, ema=False, device="cuda")
+    a, _ = run_case("nvfp4.amax-computed", 0, 0, 0, fmt="nvfp4", clips=(1.0, 0.8), W=W, v=v.clone())
+    b, _ = run_case("nvfp4.amax-supplied", 0, 0, 0, fmt="nvfp4", clips=(1.0, 0.8), W=W, v=v.clone(),
+                    supply_amax=True)
+    for k in ("codes", "scales", "r", "best_clip", "err"):
+        assert torch.equal(a[k], b[k]), k
+
+
+def test_export_only_without_r_matches():
+    W, v, g = synth.gen_matrix(48, 512, 10, w_bf16=True, ema=True, device="cuda")
+    v2 = v.clone()
+    a = Q.reconstruct(W, v, g, bits=3, group=128, clips=(1.0, 0.8, 0.6))
+    b = Q.reconstruct(W, v2, g, bits=3, group=128, clips=(1.0, 0.8, 0.6), want_r=False)
+    torch.cuda.synchronize()
+    for k in ("codes", "scales", "zeros", "best_clip", "err"):
+        assert torch.equal(a[k], b[k]), k
+    assert torch.equal(v, v2)
+
+
+def test_deterministic_and_guard_bands():
+    """Three runs give identical bytes; nothing is written outside the outputs
+    (sub-byte packing is where an out-of-bounds write would show)."""
+    W, v, g = synth.gen_matrix(37, 384, 11, w_bf16=True, ema=True, device="cuda")
+    v0 = v.clone()
+    for fmt, bits, group in (("int", 3, 128), ("int", 2, 64), ("nvfp4", 4, 16)):
+        d = Q.Descriptor(37, 384, fmt=fmt, bits=bits, group=group, clips=(1.0, 0.9, 0.7), w_dtype=Q.BF16,
+                         g_dtype=Q.BF16, beta2=0.999)
+        ng, cb = Q.quasar_num_groups(d), Q.quasar_codes_bytes(d)
+        PAD = 4096
+
+        def guarded(nbytes):
+            buf = torch.full((nbytes + 2 * PAD,), 0xA5, dtype=torch.uint8, device="cuda")
+            return buf, buf[PAD:PAD + nbytes]
+
+        results = []
+        for _ in range(3):
+            vv = v0.clone()
+            bufs = {}
+            bufs["codes"], codes = guarded(cb)
+            bufs["scales"], scales = guarded(ng * (1 if fmt == "nvfp4" else 4))
+            bufs["zeros"], zeros = guarded(ng * 4)
+            bufs["r"], r = guarded(W.numel() * 2)
+            bufs["best"], best = guarded(ng)
+            bufs["err"], err = guarded(ng * 4)
+            bufs["ts"], ts = guarded(16)
+            bufs["ws"], ws = guarded(256)
+            s = Q.quasar_reconstruct(d, W, vv, g, codes, scales, None if fmt == "nvfp4" else zeros, r, best, err,
+                                     ts if fmt == "nvfp4" else None, None, ws if fmt == "nvfp4" else None,
+                                     256 if fmt == "nvfp4" else 0, torch.cuda.current_stream().cuda_stream)
+            assert s == Q.OK
+            torch.cuda.synchronize()
+            for name, buf in bufs.items():
+                assert torch.all(buf[:PAD] == 0xA5) and torch.all(buf[-PAD:] == 0xA5), name
+            results.append([codes.clone(), scales.clone(), r.clone(), best.clone(), err.clone(), vv.clone()])
+        for a, b in zip(results[0], results[1]):
+            assert torch.equal(a, b)
+        for a, b in zip(results[0], results[2]):
+            assert torch.equal(a, b)
+
+
+def test_error_status_launches_nothing():
+    W, v, _ = synth.gen_matrix(8, 256, 12, w_bf16=True, ema=False, device="cuda")
+    out = Q.alloc_outputs(Q.Descriptor(8, 256, bits=4, group=128, clips=(1.0,)), W)
+    out["codes"].fill_(7)
+    d = Q.Descriptor(8, 256, bits=4, group=128, clips=(1.0, 1.5))  # clip out of range
+    s = Q.quasar_reconstruct(d, W, v, None, out["codes"], out["scales"], out["zeros"], out["r"], None, None, None,
+                             None, None, 0, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert s == Q.ERR_ARG and torch.all(out["codes"] == 7)
