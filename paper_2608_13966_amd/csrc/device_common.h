@@ -18,12 +18,30 @@ __device__ __forceinline__ float uniform_f32(float x) {
 }
 
 // ---- bf16 ------------------------------------------------------------------
-// Round-to-nearest-even fp32 -> bf16 bits; a NaN stays a (quiet) NaN.
-__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
-  uint32_t u = as_u32(f);
-  uint32_t rounded = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-  uint32_t nan = (u >> 16) | 0x40u;
-  return ((u & 0x7fffffffu) > 0x7f800000u) ? nan : rounded;
+// Two fp32 values -> packed bf16 (round to nearest even) in one gfx950
+// instruction (v_cvt_pk_bf16_f32); the low half holds `a`.
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  f32x2 v = {a, b};
+  bf16x2 h = __builtin_convertvector(v, bf16x2);
+  return __builtin_bit_cast(uint32_t, h);
+}
+
+// ---- reciprocal and quotient in fp64 without the IEEE division sequence ------
+// v_rcp_f64 plus Newton steps: within a few ulp of 1/d (d normal, not huge).
+__device__ __forceinline__ double rcp_f64(double d) {
+  double r = __builtin_amdgcn_rcp(d);
+  double e = __builtin_fma(-d, r, 1.0);
+  r = __builtin_fma(r, e, r);
+  e = __builtin_fma(-d, r, 1.0);
+  return __builtin_fma(r, e, r);
+}
+// n / d from a reciprocal, with one residual correction.
+__device__ __forceinline__ double div_f64(double n, double d, double rd) {
+  double q = n * rd;
+  double res = __builtin_fma(-d, q, n);
+  return __builtin_fma(res, rd, q);
 }
 
 // ---- 128-bit global memory access ------------------------------------------
@@ -66,8 +84,7 @@ __device__ __forceinline__ void store16(void* base, int64_t e0, const float (&x)
     for (int c = 0; c < 2; c++) {
       uint32_t w4[4];
 #pragma unroll
-      for (int k = 0; k < 4; k++)
-        w4[k] = f32_to_bf16_bits(x[8 * c + 2 * k]) | (f32_to_bf16_bits(x[8 * c + 2 * k + 1]) << 16);
+      for (int k = 0; k < 4; k++) w4[k] = pack_bf16x2(x[8 * c + 2 * k], x[8 * c + 2 * k + 1]);
       st128(p + 8 * c, make_uint4(w4[0], w4[1], w4[2], w4[3]));
     }
   } else {

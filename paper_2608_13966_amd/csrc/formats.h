@@ -79,4 +79,22 @@ __host__ __device__ inline double e4m3_round(double x, uint32_t* code) {
   return val;
 }
 
+// Nearest non-negative E4M3FN value to an fp32 x (RNE, saturating at 448,
+// subnormal step 2^-9); returns the value and stores the byte in *code.
+// Normal range: round the fp32 mantissa to 3 bits in integer arithmetic;
+// subnormal range: one IEEE addition of 1.5 * 2^14 rounds to a multiple of 2^-9.
+__host__ __device__ inline float e4m3_round_f32(float x, uint32_t* code) {
+  const uint32_t xb = fbits(x);
+  const uint32_t rn = (xb + 0x7ffffu + ((xb >> 20) & 1u)) & 0xfff00000u;
+  const float vs = (x + 24576.0f) - 24576.0f;
+  float v = (x >= 0.015625f) ? bitsf(rn) : vs;
+  v = (x >= 448.0f) ? 448.0f : v;
+  v = (x > 0.0f) ? v : 0.0f;  // also maps NaN to 0
+  const uint32_t vb = fbits(v);
+  const uint32_t cn = ((((vb >> 23) & 0xffu) - 120u) << 3) | ((vb >> 20) & 7u);
+  const uint32_t cs = (uint32_t)(v * 512.0f);
+  *code = (v >= 0.015625f) ? cn : cs;
+  return v;
+}
+
 }  // namespace quasar

@@ -100,7 +100,7 @@ void int_reconstruct_kernel(IntParams p) {
   double Sv = 0.0, Svw = 0.0, Svww = 0.0;
   double best_key = __longlong_as_double(0x7ff0000000000000ll);  // +inf
   float best_a = 0.f, best_b = 0.f, best_err = 0.f;
-  double thr = 0.0;
+  double thr = 0.0, rSv = 0.0;
   double* red = s_red[wave];
 
   // One pass over the lane's 16 weights for clips k0 .. k0+KC-1 (entries past
@@ -152,6 +152,7 @@ void int_reconstruct_kernel(IntParams p) {
       Svw = run_sum<L>(Svw);
       Svww = run_sum<L>(Svww);
       thr = 1e-12 * Sv * Sv * (double)QMAX * (double)QMAX;
+      rSv = rcp_f64(Sv);
     }
 
     // ---- combine the L partials: lane j sums the clips kk = j + L t ---------
@@ -189,10 +190,12 @@ void int_reconstruct_kernel(IntParams p) {
           const float fr = f * rho;
           const float s_rtn = (2.0f * fr) / kQmax;
           a = (double)s_rtn;
-          b = (Sv == 0.0) ? (double)(c - fr) : (Svw - a * A0) / Sv;
+          b = (Sv == 0.0) ? (double)(c - fr) : div_f64(Svw - a * A0, Sv, rSv);
         } else {
-          a = (Sv * A2 - A0 * Svw) / D;
-          b = (Svw - a * A0) / Sv;
+          // quotients from v_rcp_f64 + Newton: within a few ulp of the IEEE
+          // quotient, far below the fp32 rounding of (s, z) that follows
+          a = div_f64(Sv * A2 - A0 * Svw, D, rcp_f64(D));
+          b = div_f64(Svw - a * A0, Sv, rSv);
         }
         const float af = (float)a, bf = (float)b;
         const double ad = (double)af, bd = (double)bf;

@@ -1,6 +1,9 @@
 // nvfp4_kernel.hip -- QUASAR reconstruction for NVFP4 on gfx950 (Sec. 4.2).
 //
 // Tensor level: S_t = amax / (6 * 448) from the tensor absmax (not optimised).
+// E2M1 rounding uses the gfx950 FP4 conversion instructions (round to nearest
+// even, saturating at 6), which agree with the format definition on every
+// finite input; the block scale is rounded to E4M3 from fp32.
 // Per 16-element block: for every clip factor f the search scale f m / 6
 // (m = block absmax) gives E2M1 codes; the block scale is fitted to the same
 // saliency-weighted objective (scale only: s* = sum h q w / sum h q^2) and
@@ -83,25 +86,42 @@ __global__ __launch_bounds__(kThreads) void nvfp4_reconstruct_kernel(Nvfp4Params
 #pragma unroll
     for (int kk = 0; kk < KC; kk++) acc[kk][0] = acc[kk][1] = 0.0;
 #pragma unroll
-    for (int i = 0; i < N; i++) {
-      const double H = (double)v[i], Wd = (double)w[i];
+    for (int i = 0; i < N; i += 2) {
+      const double H0 = (double)v[i], W0 = (double)w[i];
+      const double H1 = (double)v[i + 1], W1 = (double)w[i + 1];
 #pragma unroll
       for (int kk = 0; kk < KC; kk++) {
-        const double Q = (double)e2m1_round(u[i] * cs[kk]);
-        const double HQ = H * Q;
-        acc[kk][0] = __builtin_fma(HQ, Q, acc[kk][0]);
-        acc[kk][1] = __builtin_fma(HQ, Wd, acc[kk][1]);
+        // E2M1 round-to-nearest-even with saturation at 6, two weights per
+        // instruction (v_cvt_scalef32_pk_fp4_f32), and back to fp32
+        const uint32_t pk = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, u[i] * cs[kk], u[i + 1] * cs[kk], 1.0f, 0);
+        const auto qq = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(pk, 1.0f, 0);
+        const double Q0 = (double)qq[0], Q1 = (double)qq[1];
+        const double HQ0 = H0 * Q0, HQ1 = H1 * Q1;
+        acc[kk][0] = __builtin_fma(HQ0, Q0, acc[kk][0]);
+        acc[kk][1] = __builtin_fma(HQ0, W0, acc[kk][1]);
+        acc[kk][0] = __builtin_fma(HQ1, Q1, acc[kk][0]);
+        acc[kk][1] = __builtin_fma(HQ1, W1, acc[kk][1]);
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
     for (int kk = 0; kk < KC; kk++) {
       const int k = k0 + kk;
       if (k < K) {
         const double Sqq = acc[kk][0], Sqw = acc[kk][1];
-        const double sstar = (Sqq == 0.0) ? (double)s_clip[k] * (double)m / 6.0 : Sqw / Sqq;
+        // E4M3 value nearest to s*/S_t, s* = Sqw / Sqq (the search scale f m / 6
+        // when no weight with saliency got a non-zero code)
+        double x;
+        if (Sqq == 0.0) {
+          const double den = 6.0 * st_d;
+          x = div_f64((double)s_clip[k] * (double)m, den, rcp_f64(den));
+        } else {
+          const double den = Sqq * st_d;
+          x = div_f64(Sqw, den, rcp_f64(den));
+        }
         uint32_t ecode;
-        const double ev = e4m3_round(sstar / st_d, &ecode);
-        const float sblk = st * (float)ev;
+        const float ev = e4m3_round_f32((float)x, &ecode);
+        const float sblk = st * ev;
         const double sb = (double)sblk;
         const double score = sb * (sb * Sqq - 2.0 * Sqw) + Sww;
         const double key = make_key(score, k);
@@ -116,29 +136,41 @@ __global__ __launch_bounds__(kThreads) void nvfp4_reconstruct_kernel(Nvfp4Params
   }
 
   int kstar = key_index(best_key);
-  float cstar = s_c6[kstar];
+  const float cstar = s_c6[kstar];
   if (zero) {
     kstar = 0;
     best_s = 0.0f;
     best_e = 0;
     best_err = (float)Sww;
   }
-  uint32_t lo = 0, hi = 0;
+  // codes of the winning clip: four pairs per dword, then zero magnitudes
+  // get a clear sign bit (a zero code is +0)
+  uint32_t cw[2] = {0u, 0u};
+#define QUASAR_PUT(D, SEL)                                                                           \
+  cw[D] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(cw[D], u[8 * D + 2 * SEL] * cstar,                \
+                                                   u[8 * D + 2 * SEL + 1] * cstar, 1.0f, SEL)
+  QUASAR_PUT(0, 0); QUASAR_PUT(0, 1); QUASAR_PUT(0, 2); QUASAR_PUT(0, 3);
+  QUASAR_PUT(1, 0); QUASAR_PUT(1, 1); QUASAR_PUT(1, 2); QUASAR_PUT(1, 3);
+#undef QUASAR_PUT
   float r[N];
 #pragma unroll
-  for (int i = 0; i < N; i++) {
-    const float q = zero ? 0.0f : e2m1_round(u[i] * cstar);
-    const uint32_t code = zero ? 0u : e2m1_code_of(q);
-    if (i < 8)
-      lo |= code << (4 * i);
-    else
-      hi |= code << (4 * (i - 8));
-    // a zero code is +0 (the E2M1 rounding keeps the sign of y)
-    r[i] = (code == 0u) ? 0.0f : best_s * q;
+  for (int d = 0; d < 2; d++) {
+    const uint32_t mag = cw[d] & 0x77777777u;
+    const uint32_t nz = (mag | (mag >> 1) | (mag >> 2)) & 0x11111111u;
+    cw[d] = zero ? 0u : (mag | (cw[d] & (nz << 3)));
   }
+#define QUASAR_GET(D, SEL)                                                            \
+  {                                                                                   \
+    const auto qq = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(cw[D], 1.0f, SEL);       \
+    r[8 * D + 2 * SEL] = best_s * qq[0];                                              \
+    r[8 * D + 2 * SEL + 1] = best_s * qq[1];                                          \
+  }
+  QUASAR_GET(0, 0) QUASAR_GET(0, 1) QUASAR_GET(0, 2) QUASAR_GET(0, 3)
+  QUASAR_GET(1, 0) QUASAR_GET(1, 1) QUASAR_GET(1, 2) QUASAR_GET(1, 3)
+#undef QUASAR_GET
   if (!active) return;
   if (p.r) store16<W_BF16>(p.r, e0, r);
-  *reinterpret_cast<uint2*>(p.codes + bid * 8) = make_uint2(lo, hi);
+  *reinterpret_cast<uint2*>(p.codes + bid * 8) = make_uint2(cw[0], cw[1]);
   p.scales[bid] = (uint8_t)best_e;
   if (p.best_clip) p.best_clip[bid] = (uint8_t)kstar;
   if (p.err) p.err[bid] = best_err;

@@ -26,6 +26,8 @@ def hostlib(tmp_path_factory):
     L.host_e2m1_code_of.restype = C.c_uint
     L.host_e4m3_round.argtypes = [C.c_double, C.POINTER(C.c_uint)]
     L.host_e4m3_round.restype = C.c_double
+    L.host_e4m3_round_f32.argtypes = [C.c_float, C.POINTER(C.c_uint)]
+    L.host_e4m3_round_f32.restype = C.c_float
     return L
 
 
@@ -60,3 +62,21 @@ def test_e4m3_matches_oracle(hostlib):
         ref = oracle.e4m3_code(float(x))
         assert code.value == ref, (x, code.value, ref)
         assert val == oracle.e4m3_value(ref)
+
+
+def test_e4m3_from_fp32_matches_oracle(hostlib):
+    """fp32 inputs are exact in fp64, so the fp32 routine must agree with the
+    oracle's fp64 rounding on every one of them (ties and saturation included)."""
+    rng = np.random.default_rng(5)
+    xs = list(np.exp(rng.uniform(np.log(1e-6), np.log(600), 20000)).astype(np.float32))
+    vals = [oracle.e4m3_value(v) for v in range(0x7F)]
+    for a, b in zip(vals[:-1], vals[1:]):
+        m = np.float32((a + b) / 2)
+        xs += [m, np.nextafter(m, np.float32(0)), np.nextafter(m, np.float32(1e9)), np.float32(a)]
+    xs += [np.float32(v) for v in (0.0, -1.0, 448.0, 464.0, 500.0, 3e38, 2.0 ** -10, 1.5 * 2.0 ** -9, 1e-45)]
+    code = C.c_uint(0)
+    for x in xs:
+        val = hostlib.host_e4m3_round_f32(float(x), C.byref(code))
+        ref = oracle.e4m3_code(float(x))
+        assert code.value == ref, (float(x), code.value, ref)
+        assert val == np.float32(oracle.e4m3_value(ref))
