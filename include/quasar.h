@@ -113,6 +113,15 @@ int quasar_reconstruct(const quasar_desc* desc, const void* W, float* v, const v
                        float* err, float* tensor_scale, const float* tensor_amax, void* workspace,
                        size_t workspace_bytes, void* stream);
 
+/*
+ * Tensor absmax for NVFP4 (Sec. 4.2: the fp32 tensor scale is set from the
+ * tensor's absolute maximum).  Writes max |W| over the whole matrix, as fp32,
+ * to amax_out (device, 1 float, 16-byte aligned), for use as the tensor_amax
+ * argument of quasar_reconstruct.  desc->format must be QUASAR_NVFP4 (the
+ * descriptor's clip fields are validated but unused).  Asynchronous on stream.
+ */
+int quasar_absmax(const quasar_desc* desc, const void* W, float* amax_out, void* stream);
+
 /* Host-only validation: the status quasar_reconstruct would return for these
  * arguments, without launching anything or touching device memory. */
 int quasar_check(const quasar_desc* desc, const void* W, const float* v, const void* g,

@@ -94,6 +94,18 @@ int quasar_check(const quasar_desc* d, const void* W, const float* v, const void
   return QUASAR_OK;
 }
 
+int quasar_absmax(const quasar_desc* d, const void* W, float* amax_out, void* stream) {
+  int s = check_desc(d);
+  if (s != QUASAR_OK) return s;
+  if (d->format != QUASAR_NVFP4) return QUASAR_ERR_FORMAT;
+  if (W == nullptr || amax_out == nullptr) return QUASAR_ERR_ARG;
+  if (!aligned16(W) || !aligned16(amax_out)) return QUASAR_ERR_ALIGN;
+  const hipError_t e = quasar::launch_absmax(W, d->w_dtype == QUASAR_BF16, d->rows * d->cols,
+                                             reinterpret_cast<unsigned*>(amax_out),
+                                             reinterpret_cast<hipStream_t>(stream));
+  return e == hipSuccess ? QUASAR_OK : QUASAR_ERR_DEVICE;
+}
+
 int quasar_reconstruct(const quasar_desc* d, const void* W, float* v, const void* g, uint8_t* codes,
                        void* scales, float* zeros, void* r, uint8_t* best_clip, float* err, float* tensor_scale,
                        const float* tensor_amax, void* workspace, size_t workspace_bytes, void* stream) {

@@ -214,6 +214,7 @@ void int_reconstruct_kernel(IntParams p) {
   };
   pass(0, std::true_type{});
   if constexpr (MULTI) {
+#pragma unroll 1
     for (int k0 = KC; k0 < K; k0 += KC) pass(k0, std::false_type{});
   }
 

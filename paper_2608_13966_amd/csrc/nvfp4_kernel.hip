@@ -3,7 +3,9 @@
 // Tensor level: S_t = amax / (6 * 448) from the tensor absmax (not optimised).
 // E2M1 rounding uses the gfx950 FP4 conversion instructions (round to nearest
 // even, saturating at 6), which agree with the format definition on every
-// finite input; the block scale is rounded to E4M3 from fp32.
+// finite input; the block scale is rounded to E4M3 with the gfx950 FP8
+// conversion (round to nearest even; checked equal to the format definition
+// up to 464, clamped to 448 above).
 // Per 16-element block: for every clip factor f the search scale f m / 6
 // (m = block absmax) gives E2M1 codes; the block scale is fitted to the same
 // saliency-weighted objective (scale only: s* = sum h q w / sum h q^2) and
@@ -21,9 +23,11 @@ namespace quasar {
 namespace {
 
 constexpr int N = 16;
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
-template <bool W_BF16, int EMA, int KC>
-__global__ __launch_bounds__(kThreads) void nvfp4_reconstruct_kernel(Nvfp4Params p) {
+template <bool W_BF16, int EMA, int KC, bool MULTI>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu((KC > 8 || MULTI) ? 3 : 4)))
+void nvfp4_reconstruct_kernel(Nvfp4Params p) {
   __shared__ float s_c6[kMaxClips], s_clip[kMaxClips];
   const int tid = threadIdx.x;
   const int K = p.n_clips;
@@ -38,8 +42,9 @@ __global__ __launch_bounds__(kThreads) void nvfp4_reconstruct_kernel(Nvfp4Params
   if (!active) bid = p.n_blocks - 1;
   const int64_t e0 = bid * N;
 
-  float w[N], v[N];
-  load16<W_BF16>(p.W, e0, w);
+  WRegs<W_BF16> wr;
+  wr.load(p.W, e0);
+  float v[N];
   load16<false>(p.v, e0, v);
   if constexpr (EMA != 0) {
     float g[N];
@@ -57,44 +62,49 @@ __global__ __launch_bounds__(kThreads) void nvfp4_reconstruct_kernel(Nvfp4Params
   const float st = amax / 2688.0f;  // 6 * 448
   float m = 0.0f;
 #pragma unroll
-  for (int i = 0; i < N; i++) m = fmaxf(m, fabsf(w[i]));
+  for (int i = 0; i < N; i++) m = fmaxf(m, fabsf(wr.get(i)));
   const bool zero = (m == 0.0f) || (st == 0.0f);
   const float rm = 1.0f / m;
   float u[N];
 #pragma unroll
-  for (int i = 0; i < N; i++) u[i] = w[i] * rm;
+  for (int i = 0; i < N; i++) u[i] = wr.get(i) * rm;
 
-  double Sww = 0.0;
-#pragma unroll
-  for (int i = 0; i < N; i++) {
-    const double Wd = (double)w[i];
-    Sww = __builtin_fma((double)v[i] * Wd, Wd, Sww);
-  }
-  const double st_d = (double)st;
+  double Sww = 0.0;  // sum h w^2, accumulated in the first pass
+  const float rst = 1.0f / st;
 
   double best_key = __longlong_as_double(0x7ff0000000000000ll);
-  float best_s = 0.0f;
   uint32_t best_e = 0;
-  float best_err = 0.0f;
 
-  for (int k0 = 0; k0 < K; k0 += KC) {
-    float cs[KC];
+  // one pass over the clips when K <= KC (the per-weight values then die as
+  // they are consumed), otherwise passes of KC
+#pragma unroll 1
+  for (int k0 = 0; k0 < (MULTI ? K : 1); k0 += KC) {
+    float cs[KC], fs[KC];
 #pragma unroll
-    for (int kk = 0; kk < KC; kk++)
-      cs[kk] = uniform_f32(s_c6[(k0 + kk) < kMaxClips ? (k0 + kk) : kMaxClips - 1]);
+    for (int kk = 0; kk < KC; kk++) {
+      const int kt = (k0 + kk) < kMaxClips ? (k0 + kk) : kMaxClips - 1;
+      cs[kk] = uniform_f32(s_c6[kt]);
+      fs[kk] = uniform_f32(s_clip[kt]);
+    }
     double acc[KC][2];
 #pragma unroll
     for (int kk = 0; kk < KC; kk++) acc[kk][0] = acc[kk][1] = 0.0;
 #pragma unroll
     for (int i = 0; i < N; i += 2) {
-      const double H0 = (double)v[i], W0 = (double)w[i];
-      const double H1 = (double)v[i + 1], W1 = (double)w[i + 1];
+      float v0 = v[i], v1 = v[i + 1], w0 = wr.get(i), w1 = wr.get(i + 1);
+      if (MULTI) asm volatile("" : "+v"(v0), "+v"(v1), "+v"(w0), "+v"(w1));  // not hoisted across passes
+      const double H0 = (double)v0, W0 = (double)w0;
+      const double H1 = (double)v1, W1 = (double)w1;
+      if (k0 == 0) {
+        Sww = __builtin_fma(H0 * W0, W0, Sww);
+        Sww = __builtin_fma(H1 * W1, W1, Sww);
+      }
 #pragma unroll
       for (int kk = 0; kk < KC; kk++) {
-        // E2M1 round-to-nearest-even with saturation at 6, two weights per
-        // instruction (v_cvt_scalef32_pk_fp4_f32), and back to fp32
+        // E2M1 round-to-nearest-even with saturation at 6 for two weights
+        // (v_cvt_scalef32_pk_fp4_f32) and back to fp32
         const uint32_t pk = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, u[i] * cs[kk], u[i + 1] * cs[kk], 1.0f, 0);
-        const auto qq = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(pk, 1.0f, 0);
+        const f32x2 qq = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(pk, 1.0f, 0);
         const double Q0 = (double)qq[0], Q1 = (double)qq[1];
         const double HQ0 = H0 * Q0, HQ1 = H1 * Q1;
         acc[kk][0] = __builtin_fma(HQ0, Q0, acc[kk][0]);
@@ -104,39 +114,38 @@ __global__ __launch_bounds__(kThreads) void nvfp4_reconstruct_kernel(Nvfp4Params
       }
       __builtin_amdgcn_sched_barrier(0);
     }
+    // Branch-free on purpose: a clip-dependent branch here would let the
+    // compiler sink each clip's moment accumulation into its own block and
+    // serialise the clips (one 16-deep fp64 chain at a time).
 #pragma unroll
     for (int kk = 0; kk < KC; kk++) {
       const int k = k0 + kk;
-      if (k < K) {
-        const double Sqq = acc[kk][0], Sqw = acc[kk][1];
-        // E4M3 value nearest to s*/S_t, s* = Sqw / Sqq (the search scale f m / 6
-        // when no weight with saliency got a non-zero code)
-        double x;
-        if (Sqq == 0.0) {
-          const double den = 6.0 * st_d;
-          x = div_f64((double)s_clip[k] * (double)m, den, rcp_f64(den));
-        } else {
-          const double den = Sqq * st_d;
-          x = div_f64(Sqw, den, rcp_f64(den));
-        }
-        uint32_t ecode;
-        const float ev = e4m3_round_f32((float)x, &ecode);
-        const float sblk = st * ev;
-        const double sb = (double)sblk;
-        const double score = sb * (sb * Sqq - 2.0 * Sqw) + Sww;
-        const double key = make_key(score, k);
-        if (key < best_key) {
-          best_key = key;
-          best_s = sblk;
-          best_e = ecode;
-          best_err = (float)fmax(score, 0.0);
-        }
-      }
+      const double Sqq = acc[kk][0], Sqw = acc[kk][1];
+      // x = s*/S_t with s* = Sqw / Sqq (the search scale f m / 6 when no
+      // weight with saliency has a non-zero code).  fp32 is enough: x only
+      // picks an E4M3 neighbour, and its error (a few 1e-7 relative) can flip
+      // that choice only next to a rounding midpoint.
+      const float xr = (float)Sqw * __builtin_amdgcn_rcpf((float)Sqq * st);
+      const float xz = (fs[kk] * m) * (1.0f / 6.0f) * rst;
+      const float x = (Sqq == 0.0) ? xz : xr;
+      // nearest E4M3FN (RNE; the hardware conversion returns NaN above 464,
+      // hence the clamp to 448, which is also the saturated value)
+      const uint32_t e = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(fminf(x, 448.0f), 0.0f, 0, false) & 0xffu;
+      const float sblk = st * __builtin_amdgcn_cvt_f32_fp8((int)e, 0);
+      const double sb = (double)sblk;
+      const double score = sb * (sb * Sqq - 2.0 * Sqw) + Sww;
+      double key = make_key(score, k);
+      key = (k < K) ? key : __longlong_as_double(0x7ff0000000000000ll);  // padding clips never win
+      const bool better = key < best_key;
+      best_key = better ? key : best_key;
+      best_e = better ? e : best_e;
     }
   }
 
   int kstar = key_index(best_key);
   const float cstar = s_c6[kstar];
+  float best_s = st * __builtin_amdgcn_cvt_f32_fp8((int)best_e, 0);
+  float best_err = (float)__longlong_as_double(__double_as_longlong(best_key) & ~15ll);
   if (zero) {
     kstar = 0;
     best_s = 0.0f;
@@ -209,12 +218,16 @@ __global__ __launch_bounds__(kThreads) void absmax_kernel(const void* W, int64_t
 template <bool W_BF16, int EMA>
 hipError_t launch_kc(const Nvfp4Params& p, hipStream_t s) {
   const int64_t blocks = (p.n_blocks + kThreads - 1) / kThreads;
-  if (p.n_clips > 8 && p.n_clips <= 12)
-    hipLaunchKernelGGL((nvfp4_reconstruct_kernel<W_BF16, EMA, 12>), dim3((unsigned)blocks), dim3(kThreads), 0,
-                       s, p);
+  const dim3 grid((unsigned)blocks), block(kThreads);
+  const int K = p.n_clips;
+  if (K <= 4)
+    hipLaunchKernelGGL((nvfp4_reconstruct_kernel<W_BF16, EMA, 4, false>), grid, block, 0, s, p);
+  else if (K <= 8)
+    hipLaunchKernelGGL((nvfp4_reconstruct_kernel<W_BF16, EMA, 8, false>), grid, block, 0, s, p);
+  else if (K <= 12)
+    hipLaunchKernelGGL((nvfp4_reconstruct_kernel<W_BF16, EMA, 12, false>), grid, block, 0, s, p);
   else
-    hipLaunchKernelGGL((nvfp4_reconstruct_kernel<W_BF16, EMA, 8>), dim3((unsigned)blocks), dim3(kThreads), 0,
-                       s, p);
+    hipLaunchKernelGGL((nvfp4_reconstruct_kernel<W_BF16, EMA, 8, true>), grid, block, 0, s, p);
   return hipGetLastError();
 }
 

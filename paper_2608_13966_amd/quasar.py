@@ -5,7 +5,7 @@ kernels behind ``quasar_reconstruct``.  Tensors are torch tensors on the GPU
 (torch supplies device memory and the current stream); there is no CPU path,
 and a missing library raises instead of falling back.
 
-The functions ``quasar_reconstruct``, ``quasar_check``, ``quasar_num_groups``,
+The functions ``quasar_reconstruct``, ``quasar_absmax``, ``quasar_check``, ``quasar_num_groups``,
 ``quasar_codes_bytes``, ``quasar_workspace_bytes``, ``quasar_status_string`` and
 ``quasar_version`` mirror the C entry points one to one; ``reconstruct`` is a
 convenience wrapper that allocates the outputs and calls ``quasar_reconstruct``.
@@ -26,7 +26,7 @@ F32, BF16 = 0, 1
 INT, NVFP4 = 0, 1
 MAX_CLIPS = 16
 
-EXPORTS = ("quasar_reconstruct", "quasar_check", "quasar_num_groups", "quasar_codes_bytes",
+EXPORTS = ("quasar_reconstruct", "quasar_absmax", "quasar_check", "quasar_num_groups", "quasar_codes_bytes",
            "quasar_workspace_bytes", "quasar_status_string", "quasar_version")
 
 
@@ -58,6 +58,8 @@ def lib():
             vp, dp = C.c_void_p, C.POINTER(Desc)
             L.quasar_reconstruct.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, C.c_size_t, vp]
             L.quasar_reconstruct.restype = C.c_int
+            L.quasar_absmax.argtypes = [dp, vp, vp, vp]
+            L.quasar_absmax.restype = C.c_int
             L.quasar_check.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, C.c_size_t]
             L.quasar_check.restype = C.c_int
             L.quasar_num_groups.argtypes = [dp]
@@ -104,6 +106,10 @@ def quasar_reconstruct(d: Descriptor, W, v, g, codes, scales, zeros, r, best_cli
     return lib().quasar_reconstruct(d.ref, _p(W), _p(v), _p(g), _p(codes), _p(scales), _p(zeros), _p(r),
                                     _p(best_clip), _p(err), _p(tensor_scale), _p(tensor_amax), _p(workspace),
                                     int(workspace_bytes), stream)
+
+
+def quasar_absmax(d: Descriptor, W, amax_out, stream) -> int:
+    return lib().quasar_absmax(d.ref, _p(W), _p(amax_out), stream)
 
 
 def quasar_check(d: Descriptor, W, v, g, codes, scales, zeros, r, best_clip, err, tensor_scale, tensor_amax,

@@ -105,3 +105,15 @@ def test_size_queries():
     assert Q.quasar_num_groups(d) == 8 and Q.quasar_codes_bytes(d) == 64
     assert Q.quasar_workspace_bytes(d, False) == 256 and Q.quasar_workspace_bytes(d, True) == 0
     assert Q.quasar_num_groups(_int_desc(cols=200)) == 0 and Q.quasar_codes_bytes(_int_desc(cols=200)) == 0
+
+
+def test_absmax_entry_point_validation():
+    """quasar_absmax rejects non-NVFP4 descriptors and bad pointers before
+    launching anything."""
+    d_int = _int_desc()
+    assert Q.quasar_absmax(d_int, A, A, None) == Q.ERR_FORMAT
+    nv = _int_desc(fmt="nvfp4")
+    assert Q.quasar_absmax(nv, None, A, None) == Q.ERR_ARG
+    assert Q.quasar_absmax(nv, A, None, None) == Q.ERR_ARG
+    assert Q.quasar_absmax(nv, A + 4, A, None) == Q.ERR_ALIGN
+    assert Q.quasar_absmax(_int_desc(fmt="nvfp4", cols=24), A, A, None) == Q.ERR_SHAPE

@@ -198,6 +198,24 @@ def test_nvfp4_supplied_amax_matches_computed():
         assert torch.equal(a[k], b[k]), k
 
 
+def test_absmax_entry_point():
+    """quasar_absmax writes max |W| (fp32) of the whole matrix; feeding it to
+    quasar_reconstruct gives the same outputs as the in-call absmax pass."""
+    for wb, (r, c) in ((True, (4096, 1024)), (False, (37, 384)), (True, (1, 16))):
+        W, v, _ = synth.gen_matrix(r, c, 13, w_bf16=wb, ema=False, device="cuda")
+        d = Q.Descriptor(r, c, fmt="nvfp4", clips=(1.0, 0.8), w_dtype=Q.BF16 if wb else Q.F32)
+        amax = torch.full((4,), -1.0, dtype=torch.float32, device="cuda")
+        assert Q.quasar_absmax(d, W, amax, torch.cuda.current_stream().cuda_stream) == Q.OK
+        torch.cuda.synchronize()
+        assert float(amax[0]) == oracle.absmax(synth.to_host(W))
+        a = Q.reconstruct(W, v.clone(), fmt="nvfp4", clips=(1.0, 0.8))
+        b = Q.reconstruct(W, v.clone(), fmt="nvfp4", clips=(1.0, 0.8), tensor_amax=amax)
+        torch.cuda.synchronize()
+        for k in ("codes", "scales", "r", "best_clip", "err"):
+            assert torch.equal(a[k], b[k]), k
+        assert float(a["tensor_scale"][0]) == float(b["tensor_scale"][0])  # one fp32 value
+
+
 def test_export_only_without_r_matches():
     W, v, g = synth.gen_matrix(48, 512, 10, w_bf16=True, ema=True, device="cuda")
     v2 = v.clone()
