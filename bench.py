@@ -26,7 +26,34 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0           # MI355X HBM3E, vendor figure
+# non-packed VALU issue rate: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (lane-ops/s)
+PEAK_VALU_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 METRIC = "G weights reconstructed/s and achieved HBM GB/s (% of peak), 1 MI355X"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def source_fingerprint() -> str:
+    """Hash of the HIP sources: counter readings are only valid for the
+    kernels they were taken on."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2608_13966_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_valu_ops_per_weight(wl) -> float:
+    """VALU lane-operations per weight that the method needs as computed here:
+    per clip, the code (scale-shift, round, clamp; NVFP4: scale, E2M1 round)
+    and the moments (one product and three accumulations; NVFP4 two); per
+    weight, the range, the clip-independent moments, the EMA and the emitted
+    code and r."""
+    K = len(wl.clips)
+    if wl.fmt == "nvfp4":
+        return 5.0 * K + 8.0 + (3.0 if wl.ema else 0.0)
+    return 7.0 * K + 9.0 + (3.0 if wl.ema else 0.0)
 
 
 def algorithmic_bytes_per_weight(wl, amax_pass: bool) -> float:
@@ -88,7 +115,8 @@ def main(argv=None):
         W, v, g = synth.gen_matrix(r, c, seed, w_bf16=wl.w_bf16, ema=wl.ema, device=dev)
         d = Q.Descriptor(r, c, fmt=wl.fmt, bits=wl.bits, group=wl.group, clips=wl.clips,
                          w_dtype=Q.BF16 if wl.w_bf16 else Q.F32, g_dtype=Q.BF16, beta2=wl.beta2)
-        out = Q.alloc_outputs(d, W, want_r=True, want_diag=False, has_amax=False)
+        out = Q.alloc_outputs(d, W, want_r=True, want_diag=False, has_amax=wl.fmt == "nvfp4")
+        out["amax"] = torch.zeros(4, dtype=torch.float32, device=dev) if wl.fmt == "nvfp4" else None
         mats.append(dict(name=name, W=W, v=v, g=g, d=d, out=out))
     footprint = sum(m["W"].numel() * (m["W"].element_size() + 4 + (2 if wl.ema else 0)) for m in mats)
     # workloads that fit in the 256 MB last-level cache are rotated over copies
@@ -101,42 +129,57 @@ def main(argv=None):
             for m in base:
                 mm = dict(m)
                 if ci:
+                    o2 = Q.alloc_outputs(m["d"], m["W"], want_r=True, want_diag=False, has_amax=wl.fmt == "nvfp4")
+                    o2["amax"] = None if m["out"]["amax"] is None else torch.zeros_like(m["out"]["amax"])
                     mm = dict(name=m["name"], W=m["W"].clone(), v=m["v"].clone(),
-                              g=None if m["g"] is None else m["g"].clone(), d=m["d"],
-                              out=Q.alloc_outputs(m["d"], m["W"], want_r=True, want_diag=False, has_amax=False))
+                              g=None if m["g"] is None else m["g"].clone(), d=m["d"], out=o2)
                 mats.append(mm)
     torch.cuda.synchronize()
     setup_s = time.time() - t0
     n_per_step = wl.n_weights
     per_step = len(mats) // copies
 
+    def launch_absmax(m):
+        s = Q.quasar_absmax(m["d"], m["W"], m["out"]["amax"], stream.cuda_stream)
+        if s != Q.OK:
+            raise Q.QuasarError(s, "quasar_absmax")
+
     def launch(m):
         o = m["out"]
         s = Q.quasar_reconstruct(m["d"], m["W"], m["v"], m["g"], o["codes"], o["scales"], o["zeros"], o["r"],
-                                 None, None, o["tensor_scale"], None, o["workspace"], o["workspace_bytes"],
+                                 None, None, o["tensor_scale"], o["amax"], o["workspace"], o["workspace_bytes"],
                                  stream.cuda_stream)
         if s != Q.OK:
             raise Q.QuasarError(s)
 
     # ---- warmup ----------------------------------------------------------------
+    nv = wl.fmt == "nvfp4"
     for i in range(args.warmup):
         for m in mats[(i % copies) * per_step:(i % copies + 1) * per_step]:
+            if nv:
+                launch_absmax(m)
             launch(m)
     torch.cuda.synchronize()
 
     # ---- timed steps: whole-step events plus one event pair per launch ---------
     ev_start, ev_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    per_launch = []
+    per_launch, per_absmax = [], []
     torch.cuda.synchronize()
     t_wall = time.time()
     ev_start.record(stream)
     for i in range(args.steps):
         for m in mats[(i % copies) * per_step:(i % copies + 1) * per_step]:
+            if nv:  # NVFP4: the tensor absmax pass, timed on its own
+                a0 = torch.cuda.Event(enable_timing=True)
+                a0.record(stream)
+                launch_absmax(m)
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
             launch(m)
             b.record(stream)
             per_launch.append((a, b, m["W"].numel()))
+            if nv:
+                per_absmax.append((a0, a))
     ev_end.record(stream)
     torch.cuda.synchronize()
     wall = time.time() - t_wall
@@ -150,8 +193,9 @@ def main(argv=None):
     gw_s = n_per_step / (ms_per_step * 1e-3) / 1e9
     gbps = gw_s * bpw
     # dominant kernel: the reconstruct kernel; its algorithmic bytes over the
-    # summed launch durations (for NVFP4 a launch also contains the absmax pass)
-    kbpw = bpw if amax_pass else kernel_bytes_per_weight(wl)
+    # summed launch durations (the NVFP4 absmax pass is timed separately)
+    kbpw = kernel_bytes_per_weight(wl)
+    absmax_us = (1e3 * sum(a.elapsed_time(b) for a, b in per_absmax) / len(per_absmax)) if per_absmax else None
     k_time = sum(launch_ms) * 1e-3
     k_bytes = sum(launch_w) * kbpw
     k_gbps = k_bytes / k_time / 1e9
@@ -201,10 +245,37 @@ def main(argv=None):
                "sample": f"every {step}th row of every matrix of {args.workload} ({sample_w} weights, "
                          f"{t_cpu:.1f} s on {threads} threads, fp64 fit/score mode)"}
 
-    roofline = {"bound": "hbm", "achieved": round(k_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                "frac": round(k_gbps / PEAK_HBM_GBPS, 4), "traffic": None,
-                "kernel": "nvfp4_reconstruct (with absmax pass)" if amax_pass else "int_reconstruct",
-                "bytes_per_weight": kbpw, "avg_launch_us": round(avg_launch_us, 2)}
+    # which roof binds: time per weight at the HBM peak vs at the VALU issue peak
+    ops_w = algorithmic_valu_ops_per_weight(wl)
+    k_wps = sum(launch_w) / k_time
+    t_hbm, t_alu = kbpw / (PEAK_HBM_GBPS * 1e9), ops_w / (PEAK_VALU_TOPS * 1e12)
+    traffic = None
+    traffic_ratio = None
+    try:
+        with open(TRAFFIC_FILE) as f:
+            tr = json.load(f)
+        ent = tr.get("workloads", {}).get(args.workload)
+        if ent and tr.get("source_fingerprint") == source_fingerprint():
+            # measured HBM bytes per weight (calibrated FETCH_SIZE + WRITE_SIZE) per launch
+            traffic = round(ent["bytes_per_weight"] * sum(launch_w) / len(launch_w))
+            traffic_ratio = round(ent["bytes_per_weight"] / kbpw, 4)
+    except (OSError, ValueError, KeyError):
+        pass
+    kname = "nvfp4_reconstruct" if amax_pass else "int_reconstruct"
+    if t_alu > t_hbm:
+        achieved = ops_w * k_wps / 1e12
+        roofline = {"bound": "alu", "achieved": round(achieved, 2), "peak": round(PEAK_VALU_TOPS, 2),
+                    "unit": "T VALU lane-ops/s", "frac": round(achieved / PEAK_VALU_TOPS, 4), "traffic": traffic,
+                    "hbm_GBps": round(k_gbps, 1), "hbm_frac": round(k_gbps / PEAK_HBM_GBPS, 4)}
+    else:
+        roofline = {"bound": "hbm", "achieved": round(k_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                    "frac": round(k_gbps / PEAK_HBM_GBPS, 4), "traffic": traffic,
+                    "valu_Tops": round(ops_w * k_wps / 1e12, 2),
+                    "valu_frac": round(ops_w * k_wps / 1e12 / PEAK_VALU_TOPS, 4)}
+    roofline.update({"kernel": kname, "bytes_per_weight": kbpw, "valu_ops_per_weight": ops_w,
+                     "traffic_over_algorithmic": traffic_ratio, "avg_launch_us": round(avg_launch_us, 2)})
+    if absmax_us is not None:
+        roofline["absmax_avg_launch_us"] = round(absmax_us, 2)
     line = {
         "metric": METRIC, "value": round(gw_s, 3), "unit": "G weights/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
