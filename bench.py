@@ -84,8 +84,9 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-rows", type=int, default=16,
-                    help="oracle timing uses every n-th row of every matrix")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0,
+                    help="CPU time (thread-seconds) the oracle baseline aims to spend; the row stride of "
+                         "its sample is chosen from a short pilot run")
     ap.add_argument("--no-copy-baseline", action="store_true")
     args = ap.parse_args(argv)
 
@@ -188,6 +189,14 @@ def main(argv=None):
     launch_ms = [a.elapsed_time(b) for a, b, _ in per_launch]
     launch_w = [n for _, _, n in per_launch]
 
+    # per-step kernel time (sum of that step's launches) -> spread over steps
+    amax_ms = [a.elapsed_time(b) for a, b in per_absmax]
+    step_k = []
+    for i in range(args.steps):
+        sl = slice(i * per_step, (i + 1) * per_step)
+        step_k.append(sum(launch_ms[sl]) + (sum(amax_ms[sl]) if amax_ms else 0.0))
+    step_pct = [round(float(x), 4) for x in np.percentile(step_k, [10, 50, 90])]
+
     amax_pass = wl.fmt == "nvfp4"
     bpw = algorithmic_bytes_per_weight(wl, amax_pass)
     gw_s = n_per_step / (ms_per_step * 1e-3) / 1e9
@@ -225,25 +234,38 @@ def main(argv=None):
     if not args.no_cpu_baseline:
         import oracle
         threads = min(16, os.cpu_count() or 1)
-        sample_w = 0
-        t_cpu = 0.0
-        step = max(1, args.cpu_sample_rows)
-        for m in mats[:per_step]:
-            rows = np.arange(0, m["W"].shape[0], step)
-            Wh = synth.to_host(m["W"])
-            vh = synth.to_host(m["v"])[rows]
-            gh = None if m["g"] is None else synth.to_host(m["g"])[rows]
-            amax = oracle.absmax(Wh) if wl.fmt == "nvfp4" else None
-            Ws = np.ascontiguousarray(Wh[rows])
+
+        def oracle_rows(m, step):
+            rows = torch.arange(0, m["W"].shape[0], step, device=dev)
+            Ws = synth.to_host(m["W"].index_select(0, rows))
+            vh = synth.to_host(m["v"].index_select(0, rows))
+            gh = None if m["g"] is None else synth.to_host(m["g"].index_select(0, rows))
+            amax = oracle.absmax(synth.to_host(m["W"])) if wl.fmt == "nvfp4" else None
             t1 = time.time()
             oracle.reconstruct(Ws, vh, fmt=wl.fmt, bits=wl.bits, group=wl.group, clips=wl.clips, g=gh,
                                beta2=wl.beta2, tensor_amax=amax, n_threads=threads)
-            t_cpu += time.time() - t1
-            sample_w += Ws.size
+            return Ws.size, time.time() - t1
+
+        # pilot on the largest matrix, then a stride that spends about
+        # --cpu-seconds of thread time over the whole step
+        # (the first pilot call warms the oracle's thread pool and caches; the
+        # second one is timed)
+        big = max(mats[:per_step], key=lambda m: m["W"].numel())
+        pilot_step = max(1, big["W"].shape[0] // 128)
+        oracle_rows(big, pilot_step)
+        pw, pt = oracle_rows(big, pilot_step)
+        rate = pw / max(pt, 1e-6)
+        step = max(1, math.ceil(n_per_step / (rate * args.cpu_seconds / threads)))
+        sample_w, t_cpu = 0, 0.0
+        for m in mats[:per_step]:
+            w_, t_ = oracle_rows(m, step)
+            sample_w += w_
+            t_cpu += t_
         cpu = {"value": round(sample_w / t_cpu / 1e9, 6), "unit": "G weights/s", "cores": threads,
                "kind": "oracle",
-               "sample": f"every {step}th row of every matrix of {args.workload} ({sample_w} weights, "
-                         f"{t_cpu:.1f} s on {threads} threads, fp64 fit/score mode)"}
+               "sample": f"rows 0, {step}, {2 * step}, ... of every matrix of {args.workload} ({sample_w} weights, "
+                         f"{t_cpu:.1f} s wall = {t_cpu * threads:.0f} thread-s on {threads} threads; "
+                         f"fp64 fit/score)"}
 
     # which roof binds: time per weight at the HBM peak vs at the VALU issue peak
     ops_w = algorithmic_valu_ops_per_weight(wl)
@@ -290,6 +312,7 @@ def main(argv=None):
         "algorithmic_bytes_per_weight": bpw,
         "copy_GBps": None if copy_gbps is None else round(copy_gbps, 1),
         "hbm_pct_of_copy": None if copy_gbps is None else round(100 * gbps / copy_gbps, 2),
+        "step_kernel_ms_p10_p50_p90": step_pct,
         "wall_s_timed": round(wall, 3), "setup_s": round(setup_s, 1),
         "roofline": roofline, "cpu_baseline": cpu,
     }

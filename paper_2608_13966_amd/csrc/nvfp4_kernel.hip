@@ -191,16 +191,40 @@ __global__ void absmax_clear_kernel(unsigned* ws) {
   if (threadIdx.x == 0 && blockIdx.x == 0) ws[0] = 0u;
 }
 
+// max |x| over the 16-byte chunk t (8 bf16 or 4 fp32 values)
 template <bool W_BF16>
-__global__ __launch_bounds__(kThreads) void absmax_kernel(const void* W, int64_t n16, unsigned* ws) {
-  __shared__ float s_m[kThreads / 64];
+__device__ __forceinline__ float chunk_absmax(uint4 t) {
+  const uint32_t d[4] = {t.x, t.y, t.z, t.w};
   float m = 0.0f;
-  for (int64_t c = (int64_t)blockIdx.x * kThreads + threadIdx.x; c < n16; c += (int64_t)gridDim.x * kThreads) {
-    float w[N];
-    load16<W_BF16>(W, c * N, w);
 #pragma unroll
-    for (int i = 0; i < N; i++) m = fmaxf(m, fabsf(w[i]));
+  for (int k = 0; k < 4; k++) {
+    if constexpr (W_BF16) {
+      m = fmaxf(m, fmaxf(fabsf(as_f32(d[k] << 16)), fabsf(as_f32(d[k] & 0xffff0000u))));
+    } else {
+      m = fmaxf(m, fabsf(as_f32(d[k])));
+    }
   }
+  return m;
+}
+
+// Grid-stride over 16-byte chunks, consecutive lanes on consecutive chunks
+// (fully coalesced), four independent loads in flight per lane.
+template <bool W_BF16>
+__global__ __launch_bounds__(kThreads) void absmax_kernel(const void* W, int64_t n_chunks, unsigned* ws) {
+  __shared__ float s_m[kThreads / 64];
+  const uint4* src = reinterpret_cast<const uint4*>(W);
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  int64_t c = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  float m0 = 0.0f, m1 = 0.0f, m2 = 0.0f, m3 = 0.0f;
+  for (; c + 3 * stride < n_chunks; c += 4 * stride) {
+    const uint4 t0 = src[c], t1 = src[c + stride], t2 = src[c + 2 * stride], t3 = src[c + 3 * stride];
+    m0 = fmaxf(m0, chunk_absmax<W_BF16>(t0));
+    m1 = fmaxf(m1, chunk_absmax<W_BF16>(t1));
+    m2 = fmaxf(m2, chunk_absmax<W_BF16>(t2));
+    m3 = fmaxf(m3, chunk_absmax<W_BF16>(t3));
+  }
+  for (; c < n_chunks; c += stride) m0 = fmaxf(m0, chunk_absmax<W_BF16>(src[c]));
+  float m = fmaxf(fmaxf(m0, m1), fmaxf(m2, m3));
   m = run_max<16>(m);
   m = fmaxf(m, __shfl_xor(m, 16, 64));
   m = fmaxf(m, __shfl_xor(m, 32, 64));
@@ -247,15 +271,19 @@ hipError_t launch_nvfp4(const Nvfp4Params& p, bool w_bf16, int ema_mode, hipStre
 }
 
 hipError_t launch_absmax(const void* W, bool w_bf16, int64_t n, unsigned* ws, hipStream_t s) {
-  const int64_t n16 = n / N;
-  int64_t blocks = (n16 + kThreads - 1) / kThreads;
-  if (blocks > 2048) blocks = 2048;
+  // n is a multiple of 16 (whole NVFP4 blocks), so W is a whole number of
+  // 16-byte chunks in either dtype
+  const int64_t n_chunks = n / (w_bf16 ? 8 : 4);
+  // at most 4 blocks per CU: enough loads in flight with four per lane, and
+  // few enough blocks that each runs a long grid-stride loop
+  int64_t blocks = (n_chunks + 4 * kThreads - 1) / (4 * kThreads);
+  if (blocks > 1024) blocks = 1024;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(absmax_clear_kernel, dim3(1), dim3(64), 0, s, ws);
   if (w_bf16)
-    hipLaunchKernelGGL(absmax_kernel<true>, dim3((unsigned)blocks), dim3(kThreads), 0, s, W, n16, ws);
+    hipLaunchKernelGGL(absmax_kernel<true>, dim3((unsigned)blocks), dim3(kThreads), 0, s, W, n_chunks, ws);
   else
-    hipLaunchKernelGGL(absmax_kernel<false>, dim3((unsigned)blocks), dim3(kThreads), 0, s, W, n16, ws);
+    hipLaunchKernelGGL(absmax_kernel<false>, dim3((unsigned)blocks), dim3(kThreads), 0, s, W, n_chunks, ws);
   return hipGetLastError();
 }
 
