@@ -247,20 +247,26 @@ def main(argv=None):
             return Ws.size, time.time() - t1
 
         # pilot on the largest matrix, then a stride that spends about
-        # --cpu-seconds of thread time over the whole step
-        # (the first pilot call warms the oracle's thread pool and caches; the
-        # second one is timed)
+        # --cpu-seconds of thread time over the whole step (the first pilot
+        # call warms the oracle's thread pool and caches; the second is timed).
+        # Each call has a fixed cost of some milliseconds, so a sample that
+        # comes out far too short is taken again with a finer stride.
         big = max(mats[:per_step], key=lambda m: m["W"].numel())
-        pilot_step = max(1, big["W"].shape[0] // 128)
+        pilot_step = max(1, big["W"].shape[0] // 32)
         oracle_rows(big, pilot_step)
         pw, pt = oracle_rows(big, pilot_step)
         rate = pw / max(pt, 1e-6)
         step = max(1, math.ceil(n_per_step / (rate * args.cpu_seconds / threads)))
-        sample_w, t_cpu = 0, 0.0
-        for m in mats[:per_step]:
-            w_, t_ = oracle_rows(m, step)
-            sample_w += w_
-            t_cpu += t_
+        for attempt in range(2):
+            sample_w, t_cpu = 0, 0.0
+            for m in mats[:per_step]:
+                w_, t_ = oracle_rows(m, step)
+                sample_w += w_
+                t_cpu += t_
+            spent = t_cpu * threads
+            if attempt == 1 or step == 1 or spent >= 0.5 * args.cpu_seconds:
+                break
+            step = max(1, int(step * spent / args.cpu_seconds))
         cpu = {"value": round(sample_w / t_cpu / 1e9, 6), "unit": "G weights/s", "cores": threads,
                "kind": "oracle",
                "sample": f"rows 0, {step}, {2 * step}, ... of every matrix of {args.workload} ({sample_w} weights, "
