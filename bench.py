@@ -88,6 +88,10 @@ def main(argv=None):
                     help="CPU time (thread-seconds) the oracle baseline aims to spend; the row stride of "
                          "its sample is chosen from a short pilot run")
     ap.add_argument("--no-copy-baseline", action="store_true")
+    ap.add_argument("--weighting", default="h", choices=["h", "h2", "none"],
+                    help="saliency weighting variant (h: the method's default)")
+    ap.add_argument("--param-dtype", default="fp32", choices=["fp32", "fp16", "bf16"],
+                    help="deployed precision of the INT dequantiser (s, z)")
     args = ap.parse_args(argv)
 
     if args.gpus != 1:
@@ -115,7 +119,8 @@ def main(argv=None):
     for (name, r, c), seed in zip(wl.shapes, wl.seeds):
         W, v, g = synth.gen_matrix(r, c, seed, w_bf16=wl.w_bf16, ema=wl.ema, device=dev)
         d = Q.Descriptor(r, c, fmt=wl.fmt, bits=wl.bits, group=wl.group, clips=wl.clips,
-                         w_dtype=Q.BF16 if wl.w_bf16 else Q.F32, g_dtype=Q.BF16, beta2=wl.beta2)
+                         w_dtype=Q.BF16 if wl.w_bf16 else Q.F32, g_dtype=Q.BF16, beta2=wl.beta2,
+                         weighting=args.weighting, param_dtype=args.param_dtype)
         out = Q.alloc_outputs(d, W, want_r=True, want_diag=False, has_amax=wl.fmt == "nvfp4")
         out["amax"] = torch.zeros(4, dtype=torch.float32, device=dev) if wl.fmt == "nvfp4" else None
         mats.append(dict(name=name, W=W, v=v, g=g, d=d, out=out))
@@ -243,7 +248,8 @@ def main(argv=None):
             amax = oracle.absmax(synth.to_host(m["W"])) if wl.fmt == "nvfp4" else None
             t1 = time.time()
             oracle.reconstruct(Ws, vh, fmt=wl.fmt, bits=wl.bits, group=wl.group, clips=wl.clips, g=gh,
-                               beta2=wl.beta2, tensor_amax=amax, n_threads=threads)
+                               beta2=wl.beta2, tensor_amax=amax, n_threads=threads, weighting=args.weighting,
+                               param_dtype=args.param_dtype)
             return Ws.size, time.time() - t1
 
         # pilot on the largest matrix, then a stride that spends about
@@ -313,6 +319,7 @@ def main(argv=None):
                    "group": wl.group, "clips": len(wl.clips), "fused_ema": wl.ema,
                    "io": ("bf16" if wl.w_bf16 else "fp32") + " W and r, fp32 v" + (", bf16 g" if wl.ema else ""),
                    "arithmetic": "fp32 codes, fp64 moments/fit/score",
+                   "weighting": args.weighting, "param_dtype": args.param_dtype,
                    "cache_rotation_copies": copies},
         "hbm_GBps": round(gbps, 1), "hbm_pct_peak": round(100 * gbps / PEAK_HBM_GBPS, 2),
         "algorithmic_bytes_per_weight": bpw,

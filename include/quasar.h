@@ -38,11 +38,13 @@
  *            (48 bytes per 128-group, 24 per 64-group).
  *    NVFP4 code = (sign << 3) | magnitude index, magnitudes 0, 0.5, 1, 1.5, 2,
  *    3, 4, 6; zero is always +0.
- *  - INT: scales = fp32 s, zeros = fp32 z, one each per group ([rows, cols/group]).
+ *  - INT: scales = fp32 s, zeros = fp32 z, one each per group ([rows, cols/group]);
+ *    with param_dtype F16/BF16 they hold values exactly representable there.
  *  - NVFP4: scales = one E4M3FN byte per 16-block ([rows, cols/16]); zeros unused;
  *    tensor_scale = one fp32 S_t; the block's dequantiser is S_t * e4m3.
  *  - r: [rows, cols] in W's dtype (fp32 r = fmaf(s, q, z); bf16 = its
- *    round-to-nearest-even).
+ *    round-to-nearest-even).  A constant group (min = max) has codes 0,
+ *    s = 0 and z = its value in the deployed precision.
  *  - best_clip: u8 index into clip_ratios per group; err: fp32 score of the
  *    chosen candidate per group.
  */
@@ -66,7 +68,14 @@ typedef enum {
   QUASAR_ERR_DEVICE = -6     /* HIP reported an error when launching */
 } quasar_status;
 
-typedef enum { QUASAR_F32 = 0, QUASAR_BF16 = 1 } quasar_dtype;
+typedef enum { QUASAR_F32 = 0, QUASAR_BF16 = 1, QUASAR_F16 = 2 } quasar_dtype;
+
+/* Saliency weighting of the objective (Eq. fisher-obj) and of the fit:
+ * QUASAR_WEIGHT_H    h = v, the method's default (Sec. 4.1.1);
+ * QUASAR_WEIGHT_H2   h = v*v in fp32, the squared weighting compared in App. A.3;
+ * QUASAR_WEIGHT_NONE h = 1, the "scale search only" ablation of Table 5
+ *                    (plain least-squares fit, unweighted score). */
+typedef enum { QUASAR_WEIGHT_H = 0, QUASAR_WEIGHT_H2 = 1, QUASAR_WEIGHT_NONE = 2 } quasar_weighting;
 typedef enum { QUASAR_INT = 0, QUASAR_NVFP4 = 1 } quasar_format;
 
 #define QUASAR_MAX_CLIPS 16
@@ -81,8 +90,17 @@ typedef struct {
   const float* clip_ratios;   /* HOST array of n_clips factors, each in (0, 1]; order breaks ties
                                  (the lowest index wins among equal scores) */
   int32_t n_clips;            /* 1 .. QUASAR_MAX_CLIPS */
-  int32_t g_dtype;            /* quasar_dtype of g when g != NULL */
+  int32_t g_dtype;            /* quasar_dtype of g when g != NULL (F32 or BF16) */
   float beta2;                /* EMA decay when g != NULL, in [0.5, 1) */
+  int32_t weighting;          /* quasar_weighting; 0 = QUASAR_WEIGHT_H */
+  int32_t param_dtype;        /* INT: precision the dequantiser (s, z) is deployed in,
+                                 QUASAR_F32 (0), QUASAR_F16 or QUASAR_BF16.  s and z are
+                                 rounded (from fp32, to nearest even) before r is formed
+                                 and before the candidate is scored, so r is exactly what
+                                 the deployed model computes (Sec. 3.1: the result deploys
+                                 as an ordinary RTN-quantised model).  The scales/zeros
+                                 buffers stay fp32 and hold the rounded values.
+                                 NVFP4: must be QUASAR_F32. */
 } quasar_desc;
 
 /*

@@ -31,6 +31,7 @@ class _Desc(C.Structure):
         ("w_bf16", C.c_int), ("nvfp4", C.c_int), ("bits", C.c_int), ("group", C.c_int),
         ("clips", C.POINTER(C.c_float)), ("n_clips", C.c_int),
         ("g_bf16", C.c_int), ("beta2", C.c_float), ("fp32_mode", C.c_int),
+        ("weighting", C.c_int), ("param_dtype", C.c_int),
     ]
 
 
@@ -62,6 +63,8 @@ def lib():
             L.qor_e4m3_value.restype = C.c_double
             L.qor_f32_to_bf16.argtypes = [C.c_float]
             L.qor_f32_to_bf16.restype = C.c_uint16
+            L.qor_f32_round_f16.argtypes = [C.c_float]
+            L.qor_f32_round_f16.restype = C.c_float
             _lib = L
     return _lib
 
@@ -75,10 +78,18 @@ def absmax(W: np.ndarray) -> float:
     return float(lib().qor_absmax(_ptr(W), int(W.dtype == np.uint16), W.size))
 
 
+WEIGHTINGS = {"h": 0, "h2": 1, "none": 2}
+PARAM_DTYPES = {"fp32": 0, "fp16": 1, "bf16": 2}
+
+
 def reconstruct(W, v, *, fmt="int", bits=4, group=128, clips=(1.0,), g=None, beta2=0.999,
                 tensor_amax=None, fp32_mode=False, want_scores=False, want_diag=False,
-                n_threads=1) -> dict:
+                n_threads=1, weighting="h", param_dtype="fp32") -> dict:
     """Run the oracle over the whole of W.
+
+    ``weighting``: "h" (the saliency), "h2" (its square, fp32) or "none" (h = 1).
+    ``param_dtype``: precision the INT dequantiser (s, z) is deployed in and r
+    is formed from: "fp32", "fp16" or "bf16".
 
     Returns a dict with: ``codes`` (unpacked, one per element), ``codes_packed``,
     ``r`` (W's dtype), ``best`` (u8 per group), ``err`` (fp32 per group), ``v_out``
@@ -106,7 +117,8 @@ def reconstruct(W, v, *, fmt="int", bits=4, group=128, clips=(1.0,), g=None, bet
             raise ValueError("g shape")
     d = _Desc(R, Cc, int(W.dtype == np.uint16), int(nv), nb, G,
               clips_a.ctypes.data_as(C.POINTER(C.c_float)), K,
-              int(g is not None and g.dtype == np.uint16), float(beta2), int(bool(fp32_mode)))
+              int(g is not None and g.dtype == np.uint16), float(beta2), int(bool(fp32_mode)),
+              WEIGHTINGS[weighting], PARAM_DTYPES[param_dtype])
     out = {
         "codes": np.zeros(R * Cc, np.uint8),
         "codes_packed": np.zeros(ngroups * G * nb // 8, np.uint8),
@@ -176,6 +188,10 @@ def e4m3_value(code: int) -> float:
 
 def f32_to_bf16(x: float) -> int:
     return int(lib().qor_f32_to_bf16(float(x)))
+
+
+def f32_round_f16(x: float) -> float:
+    return float(lib().qor_f32_round_f16(float(x)))
 
 
 E2M1_MAGNITUDES = (0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0)

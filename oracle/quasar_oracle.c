@@ -63,6 +63,33 @@ static uint16_t f32_to_bf16_bits(float f) {
 
 uint16_t qor_f32_to_bf16(float f) { return f32_to_bf16_bits(f); }
 
+/* Round-to-nearest-even fp32 -> IEEE binary16 value (returned as a float):
+ * 10 explicit mantissa bits, exponent range 2^-14 .. 2^15, subnormal steps of
+ * 2^-24, values at or beyond 65520 overflow to infinity (as the IEEE
+ * conversion does); NaN stays NaN. */
+static float f32_round_f16(float f) {
+  if (f != f) return f;
+  float a = fabsf(f);
+  if (a >= 65520.0f) return copysignf(INFINITY, f);
+  if (a == 0.0f) return f;
+  int e2;
+  (void)frexpf(a, &e2);                /* a in [2^(e2-1), 2^e2) */
+  int E = e2 - 1;
+  if (E < -14) E = -14;                /* subnormals share the 2^-24 step */
+  double step = ldexp(1.0, E - 10);
+  double n = nearbyint((double)a / step); /* exact quotient (power of two); RNE */
+  return copysignf((float)(n * step), f);
+}
+
+float qor_f32_round_f16(float f) { return f32_round_f16(f); }
+
+/* The deployed precision of the dequantiser (s, z): 0 fp32, 1 fp16, 2 bf16. */
+static float round_param(float x, int param_dtype) {
+  if (param_dtype == 1) return f32_round_f16(x);
+  if (param_dtype == 2) return bf16_bits_to_f32(f32_to_bf16_bits(x));
+  return x;
+}
+
 /* ------------------------------------------------------------------------ */
 /* E2M1 (FP4): 1 sign, 2 exponent, 1 mantissa bit (Sec. 4.2).               */
 /* Magnitudes by index 0..7: 0, 0.5, 1, 1.5, 2, 3, 4, 6.                     */
@@ -182,7 +209,7 @@ static void int_codes(const float* u, int n, float alpha, float beta, float qmax
 
 /* Eq. ridgefit written out in fp64: weighted means, centred sums. */
 static int_fit int_fit_fp64(const float* w, const float* h, const float* q, int n, double qmax,
-                            float s_rtn, float lo) {
+                            float s_rtn, float lo, int param_dtype) {
   int_fit out;
   double sh = 0.0, shq = 0.0, shw = 0.0;
   for (int i = 0; i < n; i++) {
@@ -216,9 +243,11 @@ static int_fit int_fit_fp64(const float* w, const float* h, const float* q, int 
     }
     b = wbar - a * qbar;
   }
-  out.a = (float)a;
-  out.b = (float)b;
-  /* Eq. fisher-obj for the dequantiser actually emitted (fp32 a, b) */
+  /* fp32, then the deployed precision; the score is that of the dequantiser
+   * actually emitted */
+  out.a = round_param((float)a, param_dtype);
+  out.b = round_param((float)b, param_dtype);
+  /* Eq. fisher-obj for the dequantiser actually emitted */
   double s = 0.0;
   for (int i = 0; i < n; i++) {
     double e = (double)out.a * (double)q[i] + (double)out.b - (double)w[i];
@@ -230,7 +259,7 @@ static int_fit int_fit_fp64(const float* w, const float* h, const float* q, int 
 
 /* Literal fp32 reading: raw single-pass moments and solve in fp32. */
 static int_fit int_fit_fp32(const float* w, const float* h, const float* q, int n, float qmax,
-                            float s_rtn, float lo) {
+                            float s_rtn, float lo, int param_dtype) {
   int_fit out;
   float sh = 0.f, shq = 0.f, shqq = 0.f, shw = 0.f, shqw = 0.f;
   for (int i = 0; i < n; i++) {
@@ -257,8 +286,8 @@ static int_fit int_fit_fp32(const float* w, const float* h, const float* q, int 
     }
     b = (shw - a * shq) / sh;
   }
-  out.a = a;
-  out.b = b;
+  out.a = a = round_param(a, param_dtype);
+  out.b = b = round_param(b, param_dtype);
   float s = 0.f;
   for (int i = 0; i < n; i++) {
     float e = fmaf(a, q[i], b) - w[i];
@@ -273,8 +302,8 @@ static int_fit int_fit_fp32(const float* w, const float* h, const float* q, int 
  * non-NULL; diag[0..3] = { S_RTN(f=1 min-max), S_LS(first clip), unused,
  * degenerate flag of the chosen fit } when non-NULL. */
 static void int_group(const float* w, const float* h, int n, int bits, const float* clips, int K,
-                      int fp32_mode, uint8_t* codes, float* a_out, float* b_out, float* r32,
-                      int* best_out, double* err_out, double* scores, double* diag) {
+                      int fp32_mode, int param_dtype, uint8_t* codes, float* a_out, float* b_out,
+                      float* r32, int* best_out, double* err_out, double* scores, double* diag) {
   const int qmax = (1 << bits) - 1;
   const float qmaxf = (float)qmax;
   float mn = w[0], mx = w[0];
@@ -284,17 +313,22 @@ static void int_group(const float* w, const float* h, int n, int bits, const flo
   }
   if (diag) diag[0] = diag[1] = diag[2] = diag[3] = 0.0;
   if (mx == mn) {
-    /* constant group: every code 0, z = w, exact reconstruction */
+    /* constant group: every code 0, s = 0, z = w in the deployed precision
+     * (exact reconstruction at fp32) */
+    const float z = round_param(mn, param_dtype);
+    double s = 0.0;
     for (int i = 0; i < n; i++) {
       codes[i] = 0;
-      r32[i] = w[i];
+      r32[i] = z;
+      const double d = (double)z - (double)w[i];
+      s += (double)h[i] * d * d;
     }
     *a_out = 0.0f;
-    *b_out = mn;
+    *b_out = z;
     *best_out = 0;
-    *err_out = 0.0;
+    *err_out = s;
     if (scores)
-      for (int k = 0; k < K; k++) scores[k] = 0.0;
+      for (int k = 0; k < K; k++) scores[k] = s;
     return;
   }
   /* Alg. 1, first line: centre and half-range */
@@ -316,8 +350,8 @@ static void int_group(const float* w, const float* h, int n, int bits, const flo
     const float fr = f * rho;
     const float s_rtn = (2.0f * fr) / qmaxf;
     const float lo = c - fr;
-    int_fit fk = fp32_mode ? int_fit_fp32(w, h, q, n, qmaxf, s_rtn, lo)
-                           : int_fit_fp64(w, h, q, n, (double)qmax, s_rtn, lo);
+    int_fit fk = fp32_mode ? int_fit_fp32(w, h, q, n, qmaxf, s_rtn, lo, param_dtype)
+                           : int_fit_fp64(w, h, q, n, (double)qmax, s_rtn, lo, param_dtype);
     if (scores) scores[k] = fk.score;
     if (diag && k == 0) diag[1] = fk.score;
     if (k == 0 || fk.score < fbest.score) { /* strict: ties keep the lowest index */
@@ -517,6 +551,8 @@ int qor_reconstruct(const qor_desc* d, int64_t row0, int64_t row1, const void* W
   if (G <= 0 || G > QOR_MAX_GROUP || d->cols % G != 0) return -2;
   if (d->n_clips < 1 || d->n_clips > QOR_MAX_CLIPS) return -1;
   if (!d->nvfp4 && (d->bits < 2 || d->bits > 4)) return -4;
+  if (d->weighting < 0 || d->weighting > 2) return -1;
+  if (d->param_dtype < 0 || d->param_dtype > 2 || (d->nvfp4 && d->param_dtype != 0)) return -4;
   const int bits = d->nvfp4 ? 4 : d->bits;
   const int64_t gpr = d->cols / G; /* groups per row */
   const int K = d->n_clips;
@@ -536,7 +572,9 @@ int qor_reconstruct(const qor_desc* d, int64_t row0, int64_t row1, const void* W
           vi = ema_one(vi, gi, d->beta2);
           if (v_out) v_out[base + i] = vi;
         }
-        h[i] = vi;
+        /* saliency weighting: h (Sec. 4.1.1), h^2 (App. A.3), or none, h = 1
+         * (the scale-search-only ablation of Table 5) */
+        h[i] = d->weighting == 1 ? vi * vi : d->weighting == 2 ? 1.0f : vi;
       }
       int best = 0;
       double e = 0.0;
@@ -548,7 +586,8 @@ int qor_reconstruct(const qor_desc* d, int64_t row0, int64_t row1, const void* W
         if (e4m3) e4m3[gid] = eb;
       } else {
         float a = 0.f, b = 0.f;
-        int_group(w, h, G, bits, d->clips, K, d->fp32_mode, codes, &a, &b, r32, &best, &e, sc, dg);
+        int_group(w, h, G, bits, d->clips, K, d->fp32_mode, d->param_dtype, codes, &a, &b, r32, &best, &e,
+                  sc, dg);
         if (scale) scale[gid] = a;
         if (zero) zero[gid] = b;
       }

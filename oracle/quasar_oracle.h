@@ -28,6 +28,8 @@ typedef struct {
   int g_bf16;          /* gradient dtype when g != NULL: 1 bf16, 0 fp32 */
   float beta2;         /* EMA decay when g != NULL */
   int fp32_mode;       /* 1: literal fp32 accumulation (diagnostic) */
+  int weighting;       /* saliency weight: 0 h = v, 1 h = v*v (fp32), 2 h = 1 */
+  int param_dtype;     /* INT dequantiser precision: 0 fp32, 1 fp16, 2 bf16 (NVFP4: 0) */
 } qor_desc;
 
 /* Reconstruct rows [row0, row1).  Outputs are whole-tensor arrays indexed by
@@ -56,6 +58,7 @@ int qor_e2m1_code(float y);
 int qor_e4m3_code(double x);
 double qor_e4m3_value(int code);
 uint16_t qor_f32_to_bf16(float f);
+float qor_f32_round_f16(float f);
 
 #ifdef __cplusplus
 }

@@ -30,6 +30,10 @@ int check_desc(const quasar_desc* d) {
   // group ids and grid sizes stay far inside int64 / launch limits
   if (d->rows > ((int64_t)1 << 40) / d->cols) return QUASAR_ERR_SHAPE;
   if (d->n_clips < 1 || d->n_clips > QUASAR_MAX_CLIPS) return QUASAR_ERR_ARG;
+  if (d->weighting < QUASAR_WEIGHT_H || d->weighting > QUASAR_WEIGHT_NONE) return QUASAR_ERR_ARG;
+  if (d->param_dtype != QUASAR_F32 && d->param_dtype != QUASAR_F16 && d->param_dtype != QUASAR_BF16)
+    return QUASAR_ERR_FORMAT;
+  if (d->format == QUASAR_NVFP4 && d->param_dtype != QUASAR_F32) return QUASAR_ERR_FORMAT;
   if (d->clip_ratios == nullptr) return QUASAR_ERR_ARG;
   for (int k = 0; k < d->n_clips; k++) {
     const float f = d->clip_ratios[k];
@@ -48,10 +52,11 @@ const char* quasar_version(void) { return "0.1.0"; }
 const char* quasar_status_string(int s) {
   switch (s) {
     case QUASAR_OK: return "ok";
-    case QUASAR_ERR_ARG: return "invalid argument (NULL pointer, n_clips, clip ratio or beta2 out of range)";
+    case QUASAR_ERR_ARG:
+      return "invalid argument (NULL pointer, n_clips, clip ratio, beta2 or weighting out of range)";
     case QUASAR_ERR_SHAPE: return "invalid shape (rows/cols < 1, cols not a multiple of the group, too large)";
     case QUASAR_ERR_ALIGN: return "device pointer not 16-byte aligned";
-    case QUASAR_ERR_FORMAT: return "unsupported format, bits, group size or dtype";
+    case QUASAR_ERR_FORMAT: return "unsupported format, bits, group size, dtype or parameter precision";
     case QUASAR_ERR_WORKSPACE: return "workspace missing or too small";
     case QUASAR_ERR_DEVICE: return "HIP launch error";
     default: return "unknown status";
@@ -80,7 +85,7 @@ int quasar_check(const quasar_desc* d, const void* W, const float* v, const void
   int s = check_desc(d);
   if (s != QUASAR_OK) return s;
   if (g != nullptr) {
-    if (d->g_dtype != QUASAR_F32 && d->g_dtype != QUASAR_BF16) return QUASAR_ERR_FORMAT;
+    if (d->g_dtype != QUASAR_F32 && d->g_dtype != QUASAR_BF16) return QUASAR_ERR_FORMAT;  // no fp16 g
     if (!(d->beta2 >= 0.5f && d->beta2 < 1.0f)) return QUASAR_ERR_ARG;
   }
   if (W == nullptr || v == nullptr || codes == nullptr || scales == nullptr) return QUASAR_ERR_ARG;
@@ -135,6 +140,8 @@ int quasar_reconstruct(const quasar_desc* d, const void* W, float* v, const void
     p.beta2 = beta2;
     p.omb2 = omb2;
     p.n_clips = K;
+    p.weighting = d->weighting;
+    p.param_dtype = d->param_dtype;
     const float qmax = (float)((1 << d->bits) - 1);
     for (int k = 0; k < quasar::kMaxClips; k++) {
       const float f = d->clip_ratios[k < K ? k : K - 1];  // entries past K repeat the last clip
@@ -158,6 +165,7 @@ int quasar_reconstruct(const quasar_desc* d, const void* W, float* v, const void
     p.beta2 = beta2;
     p.omb2 = omb2;
     p.n_clips = K;
+    p.weighting = d->weighting;
     for (int k = 0; k < quasar::kMaxClips; k++) {
       const float f = d->clip_ratios[k < K ? k : K - 1];
       p.clip[k] = f;

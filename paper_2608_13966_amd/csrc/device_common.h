@@ -28,6 +28,20 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, h);
 }
 
+// ---- deployed precision of a dequantiser parameter ---------------------------
+// fp32 -> fp16 or bf16 (round to nearest even; fp16 overflows to infinity as
+// the IEEE conversion does) and back.  mode: 0 fp32 (unchanged), 1 bf16, 2 fp16.
+__device__ __forceinline__ float round_param(float x, int mode) {
+  if (mode == 2) return (float)(_Float16)x;
+  if (mode == 1) return as_f32(pack_bf16x2(x, 0.0f) << 16);
+  return x;
+}
+
+// Saliency weight of one element: h = v, v*v (fp32) or 1.
+__device__ __forceinline__ float weight_of(float v, int weighting) {
+  return weighting == 1 ? v * v : weighting == 2 ? 1.0f : v;
+}
+
 // ---- reciprocal and quotient in fp64 without the IEEE division sequence ------
 // v_rcp_f64 plus Newton steps: within a few ulp of 1/d (d normal, not huge).
 __device__ __forceinline__ double rcp_f64(double d) {

@@ -79,6 +79,11 @@ void int_reconstruct_kernel(IntParams p) {
     }
     if (active) store16<false>(p.v, e0, v);
   }
+  // saliency weighting (uniform branch): h = v, v*v (App. A.3) or 1 (Table 5)
+  if (p.weighting != 0) {
+#pragma unroll
+    for (int i = 0; i < N; i++) v[i] = weight_of(v[i], p.weighting);
+  }
 
   // ---- group range (Alg. 1, first line) ------------------------------------
   float mn = wr.get(0), mx = wr.get(0);
@@ -197,9 +202,11 @@ void int_reconstruct_kernel(IntParams p) {
           a = div_f64(Sv * A2 - A0 * Svw, D, rcp_f64(D));
           b = div_f64(Svw - a * A0, Sv, rSv);
         }
-        const float af = (float)a, bf = (float)b;
+        // fp32, then the deployed precision: the candidate is scored with
+        // the dequantiser that is emitted
+        const float af = round_param((float)a, p.param_dtype), bf = round_param((float)b, p.param_dtype);
         const double ad = (double)af, bd = (double)bf;
-        // Eq. fisher-obj of the emitted fp32 dequantiser, expanded in fp64
+        // Eq. fisher-obj of the emitted dequantiser, expanded in fp64
         const double score =
             Svww + ad * (ad * A1 + 2.0 * bd * A0 - 2.0 * A2) + bd * (bd * Sv - 2.0 * Svw);
         const double key = make_key(score, k);
@@ -231,10 +238,11 @@ void int_reconstruct_kernel(IntParams p) {
   float a = win[0], b = win[1], errv = win[2];
   const float alpha = s_alpha[kstar];
   int kout = kstar;
-  if (constant) {  // every code 0, z = w: exact reconstruction
+  if (constant) {  // every code 0, z = w in the deployed precision (exact at fp32)
     a = 0.0f;
-    b = mn;
-    errv = 0.0f;
+    b = round_param(mn, p.param_dtype);
+    const double d = (double)b - (double)mn;
+    errv = (float)(Sv * d * d);
     kout = 0;
   }
 
@@ -248,7 +256,7 @@ void int_reconstruct_kernel(IntParams p) {
     float q = __builtin_amdgcn_fmed3f(__builtin_rintf(x), 0.0f, kQmax);
     if (constant) q = 0.0f;
     qi[i] = (uint32_t)q;
-    r[i] = constant ? mn : __builtin_fmaf(a, q, b);
+    r[i] = __builtin_fmaf(a, q, b);
   }
   if (!active) return;
   if (p.r) store16<W_BF16>(p.r, e0, r);

@@ -57,6 +57,10 @@ void nvfp4_reconstruct_kernel(Nvfp4Params p) {
     }
     if (active) store16<false>(p.v, e0, v);
   }
+  if (p.weighting != 0) {  // h = v, v*v or 1 (uniform branch)
+#pragma unroll
+    for (int i = 0; i < N; i++) v[i] = weight_of(v[i], p.weighting);
+  }
 
   const float amax = __builtin_nontemporal_load(p.amax);
   const float st = amax / 2688.0f;  // 6 * 448

@@ -24,6 +24,8 @@ struct IntParams {
   int64_t n_groups;
   float beta2, omb2;    // EMA decay and 1 - beta2 (fp32)
   int n_clips;
+  int weighting;        // 0 h = v, 1 h = v*v, 2 h = 1
+  int param_dtype;      // 0 fp32, 1 bf16, 2 fp16 (quasar_dtype values)
   float alpha[kMaxClips];  // qmax / (2 f_k), fp32 division on the host
   float clip[kMaxClips];   // f_k
 };
@@ -43,6 +45,7 @@ struct Nvfp4Params {
   int64_t n_blocks;
   float beta2, omb2;
   int n_clips;
+  int weighting;
   float c6[kMaxClips];  // 6 / f_k, fp32 division on the host
   float clip[kMaxClips];
 };

@@ -22,8 +22,11 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libquasar.so")
 
 OK, ERR_ARG, ERR_SHAPE, ERR_ALIGN, ERR_FORMAT, ERR_WORKSPACE, ERR_DEVICE = 0, -1, -2, -3, -4, -5, -6
-F32, BF16 = 0, 1
+F32, BF16, F16 = 0, 1, 2
 INT, NVFP4 = 0, 1
+WEIGHT_H, WEIGHT_H2, WEIGHT_NONE = 0, 1, 2
+WEIGHTINGS = {"h": WEIGHT_H, "h2": WEIGHT_H2, "none": WEIGHT_NONE}
+PARAM_DTYPES = {"fp32": F32, "fp16": F16, "bf16": BF16}
 MAX_CLIPS = 16
 
 EXPORTS = ("quasar_reconstruct", "quasar_absmax", "quasar_check", "quasar_num_groups", "quasar_codes_bytes",
@@ -39,7 +42,8 @@ class QuasarError(RuntimeError):
 class Desc(C.Structure):
     _fields_ = [("rows", C.c_int64), ("cols", C.c_int64), ("w_dtype", C.c_int32), ("format", C.c_int32),
                 ("bits", C.c_int32), ("group", C.c_int32), ("clip_ratios", C.POINTER(C.c_float)),
-                ("n_clips", C.c_int32), ("g_dtype", C.c_int32), ("beta2", C.c_float)]
+                ("n_clips", C.c_int32), ("g_dtype", C.c_int32), ("beta2", C.c_float),
+                ("weighting", C.c_int32), ("param_dtype", C.c_int32)]
 
 
 _lib = None
@@ -80,12 +84,14 @@ class Descriptor:
     """A quasar_desc plus the host clip array it points to (kept alive here)."""
 
     def __init__(self, rows, cols, *, fmt="int", bits=4, group=128, clips=(1.0,), w_dtype=BF16,
-                 g_dtype=BF16, beta2=0.999):
+                 g_dtype=BF16, beta2=0.999, weighting="h", param_dtype="fp32"):
         self.clips = np.ascontiguousarray(np.asarray(clips, dtype=np.float32))
         nv = fmt == "nvfp4"
+        wt = WEIGHTINGS[weighting] if isinstance(weighting, str) else int(weighting)
+        pd = PARAM_DTYPES[param_dtype] if isinstance(param_dtype, str) else int(param_dtype)
         self.desc = Desc(int(rows), int(cols), int(w_dtype), NVFP4 if nv else INT, 4 if nv else int(bits),
                          16 if nv else int(group), self.clips.ctypes.data_as(C.POINTER(C.c_float)),
-                         int(self.clips.size), int(g_dtype), float(beta2))
+                         int(self.clips.size), int(g_dtype), float(beta2), wt, pd)
 
     @property
     def ref(self):
@@ -173,8 +179,11 @@ def alloc_outputs(d: Descriptor, W, *, want_r=True, want_diag=True, has_amax=Fal
 
 
 def reconstruct(W, v, g=None, *, fmt="int", bits=4, group=128, clips=(1.0,), beta2=0.999, tensor_amax=None,
-                want_r=True, want_diag=True, out=None, stream=None):
+                want_r=True, want_diag=True, out=None, stream=None, weighting="h", param_dtype="fp32"):
     """Reconstruct W (torch tensor [rows, cols], fp32 or bf16, on the GPU).
+
+    ``weighting`` ("h", "h2", "none") and ``param_dtype`` ("fp32", "fp16",
+    "bf16") select the variants documented at quasar_desc in quasar.h.
 
     ``v`` (fp32, same shape) is overwritten with the EMA when ``g`` is given.
     Returns the dict of output tensors (see ``alloc_outputs``).  The call is
@@ -187,7 +196,8 @@ def reconstruct(W, v, g=None, *, fmt="int", bits=4, group=128, clips=(1.0,), bet
         if t is not None and not t.is_contiguous():
             raise ValueError("tensors must be contiguous")
     d = Descriptor(W.shape[0], W.shape[1], fmt=fmt, bits=bits, group=group, clips=clips, w_dtype=_dtype_code(W),
-                   g_dtype=_dtype_code(g) if g is not None else BF16, beta2=beta2)
+                   g_dtype=_dtype_code(g) if g is not None else BF16, beta2=beta2, weighting=weighting,
+                   param_dtype=param_dtype)
     if out is None:
         out = alloc_outputs(d, W, want_r=want_r, want_diag=want_diag, has_amax=tensor_amax is not None)
     if stream is None:

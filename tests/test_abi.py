@@ -60,6 +60,11 @@ def test_valid_int_and_nvfp4_descriptors():
     assert _check(d, tensor_amax=A) == Q.OK
     # optional outputs may be NULL
     assert _check(_int_desc(), r=None, best_clip=None, err=None) == Q.OK
+    # variants: saliency weighting and deployed parameter precision
+    for wt in ("h", "h2", "none"):
+        for pd in ("fp32", "fp16", "bf16"):
+            assert _check(_int_desc(weighting=wt, param_dtype=pd)) == Q.OK
+        assert _check(_int_desc(fmt="nvfp4", weighting=wt), tensor_amax=A) == Q.OK
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -68,7 +73,9 @@ def test_valid_int_and_nvfp4_descriptors():
     (dict(cols=0), Q.ERR_SHAPE), (dict(rows=1 << 30, cols=1 << 20), Q.ERR_SHAPE),
     (dict(clips=()), Q.ERR_ARG), (dict(clips=tuple([1.0] * 17)), Q.ERR_ARG), (dict(clips=(1.0, 0.0)), Q.ERR_ARG),
     (dict(clips=(1.5,)), Q.ERR_ARG), (dict(clips=(-0.5,)), Q.ERR_ARG), (dict(clips=(float("nan"),)), Q.ERR_ARG),
-    (dict(clips=(1e-9,)), Q.ERR_ARG), (dict(w_dtype=7), Q.ERR_FORMAT),
+    (dict(clips=(1e-9,)), Q.ERR_ARG), (dict(w_dtype=7), Q.ERR_FORMAT), (dict(w_dtype=Q.F16), Q.ERR_FORMAT),
+    (dict(weighting=3), Q.ERR_ARG), (dict(weighting=-1), Q.ERR_ARG), (dict(param_dtype=5), Q.ERR_FORMAT),
+    (dict(fmt="nvfp4", param_dtype="fp16"), Q.ERR_FORMAT),
 ])
 def test_invalid_descriptors(kw, status):
     assert _check(_int_desc(**kw)) == status
@@ -87,6 +94,7 @@ def test_invalid_pointers_and_alignment():
         assert _check(_int_desc(beta2=b2), g=A) == Q.ERR_ARG
     assert _check(_int_desc(beta2=0.5), g=A) == Q.OK
     assert _check(_int_desc(g_dtype=3), g=A) == Q.ERR_FORMAT
+    assert _check(_int_desc(g_dtype=Q.F16), g=A) == Q.ERR_FORMAT
     nv = _int_desc(fmt="nvfp4")
     assert _check(nv, tensor_scale=None, workspace=A, workspace_bytes=256) == Q.ERR_ARG
     assert _check(nv) == Q.ERR_WORKSPACE

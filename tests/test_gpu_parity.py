@@ -31,7 +31,8 @@ def host(t):
 
 
 def run_case(name, rows, cols, seed, *, fmt="int", bits=4, group=128, clips=(1.0, 0.9, 0.8), w_bf16=True,
-             ema=False, g_fp32=False, row_step=1, supply_amax=False, want_r=True, W=None, v=None, g=None):
+             ema=False, g_fp32=False, row_step=1, supply_amax=False, want_r=True, W=None, v=None, g=None,
+             weighting="h", param_dtype="fp32"):
     dev = "cuda"
     if W is None:
         W, v, g = synth.gen_matrix(rows, cols, seed, w_bf16=w_bf16, ema=ema, device=dev)
@@ -46,7 +47,8 @@ def run_case(name, rows, cols, seed, *, fmt="int", bits=4, group=128, clips=(1.0
             amax_t = torch.tensor([amax, 0, 0, 0], dtype=torch.float32, device=dev)
     print(f"[case] {name} shape={tuple(W.shape)} fmt={fmt} bits={bits} group={group} K={len(clips)} "
           f"w={'bf16' if w_bf16 else 'f32'} ema={ema}", flush=True)
-    out = Q.reconstruct(W, v, g, fmt=fmt, bits=bits, group=group, clips=clips, tensor_amax=amax_t, want_r=want_r)
+    out = Q.reconstruct(W, v, g, fmt=fmt, bits=bits, group=group, clips=clips, tensor_amax=amax_t, want_r=want_r,
+                        weighting=weighting, param_dtype=param_dtype)
     torch.cuda.synchronize()
     G = 16 if fmt == "nvfp4" else group
     nb = 4 if fmt == "nvfp4" else bits
@@ -65,8 +67,13 @@ def run_case(name, rows, cols, seed, *, fmt="int", bits=4, group=128, clips=(1.0
     v_gpu = host(v)[rows_idx] if g is not None else None
     o = oracle.reconstruct(Wh[rows_idx], vh[rows_idx], fmt=fmt, bits=bits, group=group, clips=clips,
                            g=None if gh is None else gh[rows_idx], beta2=0.999, tensor_amax=amax,
-                           want_scores=True, want_diag=True, n_threads=THREADS)
+                           want_scores=True, want_diag=True, n_threads=THREADS, weighting=weighting,
+                           param_dtype=param_dtype)
     h = o["v_out"] if g is not None else vh[rows_idx]
+    if weighting == "h2":
+        h = (h * h).astype(np.float32)
+    elif weighting == "none":
+        h = np.ones_like(h)
     fails, st = _parity.compare(fmt=fmt, bits=bits, group=group, W=Wh[rows_idx], h=h, o=o, gpu=gpu,
                                 v_out_gpu=v_gpu)
     record(name, st)
@@ -141,6 +148,21 @@ def test_grid_ragged(fmt, bits, group, wb, ema, K):
              fmt=fmt, bits=bits, group=group, clips=clips, w_bf16=wb, ema=ema != "none", g_fp32=ema == "f32")
 
 
+VARIANTS = [(fmt, bits, group, wt, pd) for (fmt, bits, group) in [("int", 4, 128), ("int", 3, 128), ("int", 2, 64),
+                                                                  ("nvfp4", 4, 16)]
+            for wt in ("h", "h2", "none") for pd in ("fp32", "fp16", "bf16")
+            if not (fmt == "nvfp4" and pd != "fp32") and not (wt == "h" and pd == "fp32")]
+
+
+@pytest.mark.parametrize("fmt,bits,group,wt,pd", VARIANTS)
+def test_variants_weighting_and_deployed_precision(fmt, bits, group, wt, pd):
+    """The saliency weightings (h, h^2 of App. A.3, none of Table 5) and the
+    deployed dequantiser precisions, with the fused EMA, on a ragged shape."""
+    clips = tuple(synth.clip_grid(1.0, 0.4, 9))
+    run_case(f"variant.{fmt}{bits}g{group}.{wt}.{pd}", 41, 3 * (group if fmt == "int" else 128), 300 + bits,
+             fmt=fmt, bits=bits, group=group, clips=clips, ema=True, weighting=wt, param_dtype=pd)
+
+
 def test_paper_clip_grid_int3():
     """The paper's own grid: 15 factors 0.30, 0.35, ..., 1.00 (two passes)."""
     clips = tuple(np.float32(x) for x in np.round(np.arange(1.0, 0.29, -0.05), 2))
@@ -174,6 +196,11 @@ def test_degenerate_groups():
                  W=Wg, v=vg.clone(), w_bf16=False)
     Wb = Wg.to(torch.bfloat16)
     run_case("degenerate.int4.bf16", 0, 0, 0, bits=4, group=64, clips=(1.0, 0.75, 0.5), W=Wb, v=vg.clone())
+    # constant groups deploy z in the reduced precision; h = 1 removes the
+    # zero-saliency cases, h^2 squares the single-weight ones
+    for pd, wt in (("fp16", "h"), ("bf16", "h2"), ("fp16", "none")):
+        run_case(f"degenerate.int3.{pd}.{wt}", 0, 0, 0, bits=3, group=128, clips=(1.0, 0.75, 0.5), W=Wg,
+                 v=vg.clone(), w_bf16=False, param_dtype=pd, weighting=wt)
     # NVFP4: zero blocks and a zero tensor
     Wn = Wg.clone()
     Wn[7] = 0.0

@@ -434,3 +434,121 @@ def test_nvfp4_power_of_two_saliency_scaling_is_exact():
     for key in ("codes", "e4m3", "r", "best"):
         assert np.array_equal(o1[key], o2[key]), key
     np.testing.assert_array_equal(o2["scores"], o1["scores"] * 8.0)
+
+
+# ---- variants: saliency weighting (App. A.3, Table 5) and deployed precision --
+
+
+def _f16_points():
+    rng = np.random.default_rng(3)
+    pts = [0.0, -0.0, 1.0, -1.0, 65504.0, 65519.9, 65520.0, -65520.0, 1e6, 2.0 ** -24, 2.0 ** -25,
+           3 * 2.0 ** -26, 2.0 ** -14, 2.0 ** -14 * (1 - 2.0 ** -11), 1 + 2.0 ** -11, 1 + 3 * 2.0 ** -11]
+    pts += list(rng.normal(0, 1, 4000)) + list(rng.normal(0, 1e-4, 2000)) + list(rng.normal(0, 1e4, 2000))
+    pts += list(rng.uniform(-2.0 ** -13, 2.0 ** -13, 2000))
+    return np.asarray(pts, np.float32)
+
+
+def test_fp16_rounding_against_numpy():
+    """The deployed-fp16 rounding is IEEE binary16 round-to-nearest-even,
+    including subnormals, ties and overflow to infinity: numpy's cast."""
+    for x in _f16_points():
+        got = oracle.f32_round_f16(float(x))
+        with np.errstate(over="ignore"):
+            ref = float(np.float32(x).astype(np.float16))
+        assert (got == ref) or (math.isinf(got) and math.isinf(ref) and got == ref), (x, got, ref)
+
+
+def test_weighting_none_equals_unit_saliency():
+    """h = 1 (Table 5's scale-search-only variant) on any saliency gives
+    exactly the result of the default weighting fed v = 1, and with F = {1}
+    the fit is numpy.polyfit's ordinary least squares line."""
+    Wh, vh, _ = small_matrix(6, 256, 41, bf16=True)
+    clips = tuple(synth.clip_grid(1.0, 0.6, 5))
+    a = oracle.reconstruct(Wh, vh, bits=3, group=128, clips=clips, weighting="none", want_scores=True)
+    b = oracle.reconstruct(Wh, np.ones_like(vh), bits=3, group=128, clips=clips, want_scores=True)
+    for k in ("codes", "scale", "zero", "r", "best", "err", "scores"):
+        np.testing.assert_array_equal(a[k], b[k])
+    o = oracle.reconstruct(Wh, vh, bits=3, group=128, clips=(1.0,), weighting="none")
+    wf = w_as_f32(Wh).reshape(-1, 128).astype(np.float64)
+    for gi in range(wf.shape[0]):
+        s, z = np.polyfit(o["codes"].reshape(-1, 128)[gi].astype(np.float64), wf[gi], 1)
+        np.testing.assert_allclose(o["scale"][gi], s, rtol=2e-7)
+        np.testing.assert_allclose(o["zero"][gi], z, rtol=2e-7, atol=1e-8)
+
+
+@pytest.mark.parametrize("fmt", ["int", "nvfp4"])
+def test_weighting_h2_equals_squared_saliency(fmt):
+    """h^2 weighting (App. A.3) is the default weighting fed the fp32 square of
+    the saliency (after the EMA): numpy's float32 product."""
+    Wh, vh, gh = small_matrix(6, 256, 43, ema=True, bf16=True)
+    kw = dict(fmt=fmt, bits=2, group=64, clips=tuple(synth.clip_grid(1.0, 0.6, 6)), g=gh, beta2=0.99)
+    if fmt == "nvfp4":
+        kw["tensor_amax"] = oracle.absmax(Wh)
+    a = oracle.reconstruct(Wh, vh, weighting="h2", want_scores=True, **kw)
+    vp = a["v_out"]
+    np.testing.assert_array_equal(vp, oracle.reconstruct(Wh, vh, **kw)["v_out"])  # EMA unchanged
+    kw.pop("g")
+    b = oracle.reconstruct(Wh, (vp * vp).astype(np.float32), want_scores=True, **kw)
+    for k in ("codes", "r", "best", "err", "scores") + (("e4m3",) if fmt == "nvfp4" else ("scale", "zero")):
+        np.testing.assert_array_equal(a[k], b[k])
+
+
+@pytest.mark.parametrize("pd,bits,group", [("fp16", 4, 128), ("bf16", 3, 128), ("fp16", 2, 64)])
+def test_deployed_precision_dequantiser(pd, bits, group):
+    """Deployed (s, z) in fp16/bf16: they are representable in that format,
+    r is fma(s, q, z) of exactly those values, the reported score is the fp64
+    score of the deployed dequantiser, and the chosen clip minimises the
+    scores recomputed here independently (lstsq fit, fp32 then the deployed
+    rounding by numpy/torch casts, fp64 score)."""
+    qmax = (1 << bits) - 1
+    clips = tuple(synth.clip_grid(1.0, 0.55, 7))
+    Wh, vh, _ = small_matrix(4, 512, 47)
+    o = oracle.reconstruct(Wh, vh, bits=bits, group=group, clips=clips, param_dtype=pd, want_scores=True)
+    s, z = o["scale"], o["zero"]
+    if pd == "fp16":
+        rnd = lambda x: np.float32(x).astype(np.float16).astype(np.float32)
+    else:
+        rnd = lambda x: torch.tensor(np.float32(x)).to(torch.bfloat16).float().numpy()
+    np.testing.assert_array_equal(rnd(s), s)
+    np.testing.assert_array_equal(rnd(z), z)
+    q = o["codes"].reshape(-1, group).astype(np.float64)
+    r_ref = (s[:, None].astype(np.float64) * q + z[:, None]).astype(np.float32)  # exact, then one rounding
+    np.testing.assert_array_equal(o["r"].reshape(-1, group), r_ref)
+    w = Wh.reshape(-1, group).astype(np.float64)
+    h = vh.reshape(-1, group).astype(np.float64)
+    err = (h * (s[:, None] * q + z[:, None] - w) ** 2).sum(1)
+    np.testing.assert_allclose(o["err"], err, rtol=1e-6)
+    checked = 0
+    for gi in range(w.shape[0]):
+        wi, hi = Wh.reshape(-1, group)[gi], vh.reshape(-1, group)[gi]
+        mn, mx = Fraction(float(wi.min())), Fraction(float(wi.max()))
+        c, rho = (mn + mx) / 2, (mx - mn) / 2
+        sc, near = [], False
+        for f in clips:
+            f = Fraction(float(f))
+            qq, dist = X.rtn_codes_exact(wi, c - f * rho, 2 * f * rho / qmax, qmax)
+            if dist.min() < 2e-5:
+                near = True
+                break
+            a_, b_ = X.wls_fit(qq, wi, hi)
+            sc.append(X.score(qq, wi, hi, float(rnd(np.float32(a_))), float(rnd(np.float32(b_)))))
+        if near:
+            continue
+        checked += 1
+        np.testing.assert_allclose(o["scores"][gi], sc, rtol=1e-6)
+        kk, kb = int(np.argmin(sc)), int(o["best"][gi])
+        assert kk == kb or abs(sc[kk] - sc[kb]) <= 1e-6 * sc[kk]
+    assert checked >= 0.85 * w.shape[0]
+
+
+def test_deployed_precision_constant_group():
+    """A constant group deploys z = w rounded to the format; its score is the
+    weighted squared rounding error."""
+    w = np.full(64, 0.1, np.float32)
+    h = np.linspace(1, 2, 64).astype(np.float32)
+    o = run_group(w, h, bits=2, clips=(1.0, 0.8), param_dtype="fp16")
+    z = float(np.float32(0.1).astype(np.float16))
+    assert o["scale"][0] == 0.0 and o["zero"][0] == np.float32(z)
+    assert np.all(o["codes"] == 0) and np.all(o["r"] == np.float32(z))
+    np.testing.assert_allclose(o["err"][0], float((h.astype(np.float64) * (z - np.float64(w[0])) ** 2).sum()),
+                               rtol=1e-6)
