@@ -35,6 +35,11 @@ class _Desc(C.Structure):
     ]
 
 
+class _AdamW(C.Structure):
+    _fields_ = [("lr", C.c_float), ("beta1", C.c_float), ("beta2", C.c_float), ("eps", C.c_float),
+                ("weight_decay", C.c_float), ("step", C.c_int64)]
+
+
 _lib = None
 _lock = threading.Lock()
 
@@ -63,6 +68,11 @@ def lib():
             L.qor_e4m3_value.restype = C.c_double
             L.qor_f32_to_bf16.argtypes = [C.c_float]
             L.qor_f32_to_bf16.restype = C.c_uint16
+            L.qor_adamw_reconstruct.argtypes = [C.POINTER(_Desc), C.POINTER(_AdamW), C.c_int64, C.c_int64,
+                                                vp, vp, vp, vp, C.c_float, vp, vp, vp, vp, vp, vp, vp, vp,
+                                                vp, vp]
+            L.qor_adamw_reconstruct.restype = C.c_int
+            L.qor_adamw_constants.argtypes = [C.POINTER(_AdamW)] + [C.POINTER(C.c_float)] * 5
             L.qor_f32_round_f16.argtypes = [C.c_float]
             L.qor_f32_round_f16.restype = C.c_float
             _lib = L
@@ -157,6 +167,79 @@ def reconstruct(W, v, *, fmt="int", bits=4, group=128, clips=(1.0,), g=None, bet
         with ThreadPoolExecutor(n_threads) as ex:
             list(ex.map(lambda i: run(int(bounds[i]), int(bounds[i + 1])), range(n_threads)))
     out["codes"] = out["codes"].reshape(R, Cc)
+    return out
+
+
+def adamw_constants(*, lr, beta1, beta2, eps, weight_decay, step):
+    """(1 - beta1, 1 - beta2, 1 - lr wd, lr / (1 - beta1^t), 1 / sqrt(1 - beta2^t)) as fp32."""
+    o = _AdamW(lr, beta1, beta2, eps, weight_decay, step)
+    vals = [C.c_float() for _ in range(5)]
+    lib().qor_adamw_constants(C.byref(o), *[C.byref(x) for x in vals])
+    return tuple(np.float32(x.value) for x in vals)
+
+
+def adamw_reconstruct(W, m, v, g, *, lr, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, step=1,
+                      fmt="int", bits=4, group=128, clips=(1.0,), tensor_amax=None, want_scores=False,
+                      want_diag=False, n_threads=1, weighting="h", param_dtype="fp32") -> dict:
+    """One AdamW step on copies of W (fp32 or bf16 bits), m, v (fp32) with
+    gradient g (fp32 or bf16 bits), then the reconstruction of the updated W
+    with the updated v as saliency.  Returns the reconstruct() dict plus
+    ``W_out``, ``m_out``, ``v_out`` and, for NVFP4, ``amax_out`` = max |W_out|.
+    NVFP4 takes its tensor scale from ``tensor_amax`` (required)."""
+    W = np.array(W, copy=True, order="C")
+    m = np.array(m, dtype=np.float32, copy=True, order="C")
+    v = np.array(v, dtype=np.float32, copy=True, order="C")
+    g = np.ascontiguousarray(g)
+    if W.dtype not in (np.float32, np.uint16) or g.dtype not in (np.float32, np.uint16):
+        raise TypeError("W and g must be float32 or uint16 (bf16 bits)")
+    if not (W.shape == m.shape == v.shape == g.shape):
+        raise ValueError("shapes")
+    nv = fmt == "nvfp4"
+    if nv and tensor_amax is None:
+        raise ValueError("NVFP4 needs tensor_amax")
+    R, Cc = W.shape
+    G = 16 if nv else int(group)
+    nb = 4 if nv else int(bits)
+    clips_a = np.ascontiguousarray(np.asarray(clips, dtype=np.float32))
+    K = clips_a.size
+    ngroups = R * Cc // G
+    d = _Desc(R, Cc, int(W.dtype == np.uint16), int(nv), nb, G, clips_a.ctypes.data_as(C.POINTER(C.c_float)), K,
+              int(g.dtype == np.uint16), float(beta2), 0, WEIGHTINGS[weighting], PARAM_DTYPES[param_dtype])
+    o = _AdamW(lr, beta1, beta2, eps, weight_decay, step)
+    out = {"codes": np.zeros(R * Cc, np.uint8), "codes_packed": np.zeros(ngroups * G * nb // 8, np.uint8),
+           "r": np.zeros((R, Cc), W.dtype), "best": np.zeros(ngroups, np.uint8),
+           "err": np.zeros(ngroups, np.float32)}
+    amax = float(tensor_amax) if nv else 0.0
+    if nv:
+        out["e4m3"] = np.zeros(ngroups, np.uint8)
+        out["tensor_scale"] = np.float32(np.float32(amax) / np.float32(2688.0))
+    else:
+        out["scale"] = np.zeros(ngroups, np.float32)
+        out["zero"] = np.zeros(ngroups, np.float32)
+    out["scores"] = np.zeros((ngroups, K), np.float64) if want_scores else None
+    out["diag"] = np.zeros((ngroups, 4), np.float64) if want_diag else None
+    L = lib()
+
+    def run(r0, r1):
+        rc = L.qor_adamw_reconstruct(C.byref(d), C.byref(o), r0, r1, _ptr(W), _ptr(m), _ptr(v), _ptr(g),
+                                     C.c_float(amax), _ptr(out["codes_packed"]), _ptr(out["codes"]),
+                                     _ptr(out.get("scale")), _ptr(out.get("zero")), _ptr(out.get("e4m3")),
+                                     _ptr(out["r"]), _ptr(out["best"]), _ptr(out["err"]), _ptr(out["scores"]),
+                                     _ptr(out["diag"]))
+        if rc != 0:
+            raise ValueError(f"oracle rejected the arguments (status {rc})")
+
+    n_threads = max(1, int(n_threads))
+    if n_threads == 1 or R < 2:
+        run(0, R)
+    else:
+        bounds = np.linspace(0, R, n_threads + 1).astype(np.int64)
+        with ThreadPoolExecutor(n_threads) as ex:
+            list(ex.map(lambda i: run(int(bounds[i]), int(bounds[i + 1])), range(n_threads)))
+    out["codes"] = out["codes"].reshape(R, Cc)
+    out["W_out"], out["m_out"], out["v_out"] = W, m, v
+    if nv:
+        out["amax_out"] = np.float32(absmax(W))
     return out
 
 

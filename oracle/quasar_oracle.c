@@ -18,6 +18,11 @@
  *   - NVFP4 (Sec. 4.2): fp32 tensor scale from the tensor absmax (not
  *     optimised), per block: candidate search scales give E2M1 codes, the
  *     E4M3 block scale is fitted to minimise the same objective, argmin kept.
+ *   - variants: saliency weighting h, h^2 (App. A.3) or 1 (Table 5), and the
+ *     INT dequantiser deployed in fp16/bf16 (rounded before r and the score).
+ *   - one AdamW step (the optimiser every method trains with, Sec. 6.1, whose
+ *     second moment is the saliency, Sec. 4.1.1) followed by the
+ *     reconstruction of the updated weights.
  *
  * Precision (the paper fixes none):
  *   - every step that decides an integer (codes, E2M1 value, E4M3 value,
@@ -606,4 +611,60 @@ int qor_reconstruct(const qor_desc* d, int64_t row0, int64_t row1, const void* W
     }
   }
   return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* AdamW step, then reconstruction of the updated weights                    */
+/* ------------------------------------------------------------------------ */
+
+/* Host-side constants of one AdamW step (fp64, then fp32). */
+void qor_adamw_constants(const qor_adamw* o, float* omb1, float* omb2, float* decay, float* step_size,
+                         float* rbc2) {
+  *omb1 = 1.0f - o->beta1;
+  *omb2 = 1.0f - o->beta2;
+  *decay = (float)(1.0 - (double)o->lr * (double)o->weight_decay);
+  const double bc1 = 1.0 - pow((double)o->beta1, (double)o->step);
+  const double bc2 = 1.0 - pow((double)o->beta2, (double)o->step);
+  *step_size = (float)((double)o->lr / bc1);
+  *rbc2 = (float)(1.0 / sqrt(bc2));
+}
+
+/* One element of AdamW with decoupled weight decay, fp32 in this order:
+ *   m' = fmaf(beta1, m, (1 - beta1) g)
+ *   v' = fmaf(beta2, v, (1 - beta2) (g g))
+ *   d  = fmaf(sqrtf(v'), 1/sqrt(1 - beta2^t), eps)
+ *   w' = fmaf(-lr/(1 - beta1^t), m'/d, w (1 - lr wd))                        */
+static float adamw_one(float w, float* m, float* v, float g, float beta1, float beta2, float omb1, float omb2,
+                       float eps, float decay, float step_size, float rbc2) {
+  const float mm = fmaf(beta1, *m, omb1 * g);
+  const float t = g * g;
+  const float vv = fmaf(beta2, *v, omb2 * t);
+  const float den = fmaf(sqrtf(vv), rbc2, eps);
+  const float upd = mm / den;
+  *m = mm;
+  *v = vv;
+  return fmaf(-step_size, upd, w * decay);
+}
+
+int qor_adamw_reconstruct(const qor_desc* d, const qor_adamw* o, int64_t row0, int64_t row1, void* W,
+                          float* m, float* v, const void* g, float tensor_amax, uint8_t* codes_packed,
+                          uint8_t* codes_unpacked, float* scale, float* zero, uint8_t* e4m3, void* r,
+                          uint8_t* best_clip, float* err, double* scores, double* diag) {
+  if (o->step < 1 || !(o->eps > 0.0f) || !(o->beta1 >= 0.0f && o->beta1 < 1.0f) ||
+      !(o->beta2 >= 0.5f && o->beta2 < 1.0f))
+    return -1;
+  float omb1, omb2, decay, step_size, rbc2;
+  qor_adamw_constants(o, &omb1, &omb2, &decay, &step_size, &rbc2);
+  for (int64_t idx = row0 * d->cols; idx < row1 * d->cols; idx++) {
+    const float gi = d->g_bf16 ? bf16_bits_to_f32(((const uint16_t*)g)[idx]) : ((const float*)g)[idx];
+    const float wn = adamw_one(load_w(W, d->w_bf16, idx), &m[idx], &v[idx], gi, o->beta1, o->beta2, omb1,
+                               omb2, o->eps, decay, step_size, rbc2);
+    if (d->w_bf16)
+      ((uint16_t*)W)[idx] = f32_to_bf16_bits(wn);
+    else
+      ((float*)W)[idx] = wn;
+  }
+  /* the updated second moment is the saliency; no further EMA */
+  return qor_reconstruct(d, row0, row1, W, v, NULL, tensor_amax, NULL, codes_packed, codes_unpacked, scale,
+                         zero, e4m3, r, best_clip, err, scores, diag);
 }

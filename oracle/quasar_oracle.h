@@ -51,6 +51,22 @@ int qor_reconstruct(const qor_desc* d, int64_t row0, int64_t row1, const void* W
                     uint8_t* codes_unpacked, float* scale, float* zero, uint8_t* e4m3, void* r,
                     uint8_t* best_clip, float* err, double* scores, double* diag);
 
+/* One AdamW step (decoupled weight decay, bias-corrected, fp32 recipe in
+ * quasar_oracle.c) on rows [row0, row1) of W, m, v (all updated in place;
+ * g is read in d->g_bf16's dtype), then qor_reconstruct of the updated W with
+ * the updated v as the saliency.  Returns 0 or a negative value. */
+typedef struct {
+  float lr, beta1, beta2, eps, weight_decay;
+  int64_t step; /* t >= 1 */
+} qor_adamw;
+
+void qor_adamw_constants(const qor_adamw* o, float* omb1, float* omb2, float* decay, float* step_size,
+                         float* rbc2);
+int qor_adamw_reconstruct(const qor_desc* d, const qor_adamw* o, int64_t row0, int64_t row1, void* W,
+                          float* m, float* v, const void* g, float tensor_amax, uint8_t* codes_packed,
+                          uint8_t* codes_unpacked, float* scale, float* zero, uint8_t* e4m3, void* r,
+                          uint8_t* best_clip, float* err, double* scores, double* diag);
+
 float qor_absmax(const void* W, int w_bf16, int64_t n);
 void qor_pack_group(const uint8_t* codes, int n, int bits, uint8_t* out);
 void qor_unpack_group(const uint8_t* in, int n, int bits, uint8_t* codes);

@@ -112,3 +112,25 @@ def e4m3_levels():
         v = m * 2.0 ** -9 if e == 0 else (1 + m / 8) * 2.0 ** (e - 7)
         vals.append((v, code))
     return vals
+
+
+def sqrt_fp32(x: float) -> float:
+    """Correctly rounded fp32 square root of the fp32 value x >= 0 (nearest,
+    ties to even), decided with exact rational comparisons of the midpoints."""
+    x = float(np.float32(x))
+    if x == 0.0:
+        return 0.0
+    c = np.float32(math.sqrt(x))
+    cands = [np.nextafter(c, np.float32(0)), c, np.nextafter(c, np.float32(np.inf))]
+    fx = Fraction(x)
+    best = None
+    for r in cands:
+        lo = (Fraction(float(np.nextafter(r, np.float32(0)))) + Fraction(float(r))) / 2
+        hi = (Fraction(float(r)) + Fraction(float(np.nextafter(r, np.float32(np.inf))))) / 2
+        if lo * lo < fx < hi * hi:
+            return float(r)
+        if fx == lo * lo or fx == hi * hi:  # a tie: the even neighbour
+            if int(np.float32(r).view(np.uint32)) % 2 == 0:
+                best = float(r)
+    assert best is not None
+    return best

@@ -552,3 +552,85 @@ def test_deployed_precision_constant_group():
     assert np.all(o["codes"] == 0) and np.all(o["r"] == np.float32(z))
     np.testing.assert_allclose(o["err"][0], float((h.astype(np.float64) * (z - np.float64(w[0])) ** 2).sum()),
                                rtol=1e-6)
+
+
+# ---- AdamW step followed by the reconstruction of the updated weights -------
+
+ADAM = dict(lr=3e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.1)
+
+
+def _adam_inputs(rows, cols, seed, w_bf16=False):
+    W, v, g = synth.gen_matrix(rows, cols, seed, w_bf16=w_bf16, ema=True)
+    gen = torch.Generator().manual_seed(seed + 1)
+    m = (torch.randn(rows, cols, generator=gen) * 1e-4).float()
+    return synth.to_host(W), synth.to_host(m), synth.to_host(v) * np.float32(1e-6), synth.to_host(g)
+
+
+def test_adamw_update_matches_exact_definition():
+    """Every operation of the documented fp32 AdamW recipe, computed here with
+    exact rationals and one correct rounding each (sqrt decided exactly)."""
+    Wh, mh, vh, gh = _adam_inputs(4, 256, 61)
+    step = 3
+    o = oracle.adamw_reconstruct(Wh, mh, vh, gh, step=step, bits=4, group=128, clips=(1.0, 0.8), **ADAM)
+    b1, b2, eps = (np.float32(ADAM[k]) for k in ("beta1", "beta2", "eps"))
+    omb1, omb2, decay, step_size, rbc2 = oracle.adamw_constants(step=step, **ADAM)
+    F = lambda x: Fraction(float(x))
+    R = X.fp32_from_fraction
+    assert omb1 == R(1 - F(b1)) and omb2 == R(1 - F(b2))
+    assert decay == np.float32(1.0 - float(np.float32(ADAM["lr"])) * float(np.float32(ADAM["weight_decay"])))
+    gf = w_as_f32(gh).ravel()
+    for i in range(0, gf.size, 5):
+        g, m, v, w = F(gf[i]), F(mh.ravel()[i]), F(vh.ravel()[i]), F(Wh.ravel()[i])
+        mm = R(F(b1) * m + F(R(F(omb1) * g)))
+        vv = R(F(b2) * v + F(R(F(omb2) * F(R(g * g)))))
+        den = R(F(X.sqrt_fp32(vv)) * F(rbc2) + F(eps))
+        upd = R(F(mm) / F(den))
+        wn = R(-F(step_size) * F(upd) + F(R(w * F(decay))))
+        assert (np.float32(mm), np.float32(vv), np.float32(wn)) == \
+            (o["m_out"].ravel()[i], o["v_out"].ravel()[i], o["W_out"].ravel()[i]), i
+
+
+def test_adamw_matches_torch_optimizer():
+    """Three steps against torch.optim.AdamW (decoupled weight decay, bias
+    correction) on fp32 parameters: same values up to fp32 rounding order.
+    The decays are chosen exact in fp32 (torch forms 1 - beta in double, the
+    recipe here in fp32 from the fp32 beta; with these values both agree)."""
+    Wh, mh, vh, _ = _adam_inputs(8, 256, 62)
+    hp = dict(ADAM, beta1=0.875, beta2=1 - 2.0 ** -10)
+    p = torch.nn.Parameter(torch.from_numpy(Wh.copy()))
+    opt = torch.optim.AdamW([p], lr=hp["lr"], betas=(hp["beta1"], hp["beta2"]), eps=hp["eps"],
+                            weight_decay=hp["weight_decay"], foreach=False)
+    W, m, v = Wh, np.zeros_like(mh), np.zeros_like(vh)
+    gen = torch.Generator().manual_seed(5)
+    for step in (1, 2, 3):
+        g = (torch.randn(Wh.shape, generator=gen) * 1e-3).float()
+        p.grad = g.clone()
+        opt.step()
+        o = oracle.adamw_reconstruct(W, m, v, g.numpy(), step=step, bits=4, group=128, clips=(1.0,), **hp)
+        W, m, v = o["W_out"], o["m_out"], o["v_out"]
+        st = opt.state[p]
+        # (torch forms m by lerp: near-cancelling sums differ by an ulp of the terms)
+        np.testing.assert_allclose(m, st["exp_avg"].numpy(), rtol=2e-6, atol=5e-11)
+        np.testing.assert_allclose(v, st["exp_avg_sq"].numpy(), rtol=2e-6, atol=1e-18)
+        np.testing.assert_allclose(W, p.detach().numpy(), rtol=1e-6, atol=1e-9)
+
+
+@pytest.mark.parametrize("fmt,w_bf16", [("int", False), ("int", True), ("nvfp4", False)])
+def test_adamw_then_reconstruct_composes(fmt, w_bf16):
+    """The fused call equals the update followed by the plain reconstruction
+    of the updated tensors (saliency = the updated second moment), and the
+    NVFP4 by-product is max |W'|."""
+    Wh, mh, vh, gh = _adam_inputs(6, 256, 63, w_bf16=w_bf16)
+    kw = dict(fmt=fmt, bits=3, group=128, clips=tuple(synth.clip_grid(1.0, 0.6, 6)), weighting="h")
+    amax = oracle.absmax(Wh) if fmt == "nvfp4" else None
+    o = oracle.adamw_reconstruct(Wh, mh, vh, gh, step=2, tensor_amax=amax, want_scores=True, **kw, **ADAM)
+    p = oracle.reconstruct(o["W_out"], o["v_out"], tensor_amax=amax, want_scores=True, **kw)
+    for k in ("codes", "r", "best", "err", "scores") + (("e4m3",) if fmt == "nvfp4" else ("scale", "zero")):
+        np.testing.assert_array_equal(o[k], p[k])
+    if w_bf16:
+        assert o["W_out"].dtype == np.uint16
+    if fmt == "nvfp4":
+        assert o["amax_out"] == np.float32(oracle.absmax(o["W_out"]))
+    # the EMA of the second moment is the one pinned above
+    e = oracle.reconstruct(Wh, vh, bits=3, group=128, clips=(1.0,), g=gh, beta2=ADAM["beta2"])
+    np.testing.assert_array_equal(o["v_out"], e["v_out"])
