@@ -10,7 +10,9 @@ already resident in HBM.  Prints ONE JSON line.
 Workloads (paper_2608_13966_amd/synth.py): c1 single fp32 1024x1024 INT4;
 c2 Qwen3-0.6B-shaped layer set INT3; c3 Llama-3.1-8B-shaped layer set INT2
 g64, 12 clips, fused EMA (default); c4 the same set in NVFP4; c5 32 such
-layers INT4 with fused EMA (one simulated training step).
+layers INT4 with fused EMA (one simulated training step); c6 / c7 the
+Llama-3.1-8B set with fp32 master weights, one fused AdamW step followed by
+the INT2 / NVFP4 reconstruction (a step then includes the optimiser update).
 """
 from __future__ import annotations
 
@@ -51,18 +53,25 @@ def algorithmic_valu_ops_per_weight(wl) -> float:
     weight, the range, the clip-independent moments, the EMA and the emitted
     code and r."""
     K = len(wl.clips)
+    # the fused AdamW step: m (2), v (3), sqrt, fma, quotient, w*decay, fma (10);
+    # the plain EMA of v: 3
+    pre = 10.0 if wl.adamw else (3.0 if wl.ema else 0.0)
     if wl.fmt == "nvfp4":
-        return 5.0 * K + 8.0 + (3.0 if wl.ema else 0.0)
-    return 7.0 * K + 9.0 + (3.0 if wl.ema else 0.0)
+        return 5.0 * K + 8.0 + pre
+    return 7.0 * K + 9.0 + pre
 
 
 def algorithmic_bytes_per_weight(wl, amax_pass: bool) -> float:
     """What the method must move per weight: W, v (and g) read once; v' (with
-    the EMA), r, the codes and the per-group parameters written once.  The
+    the EMA), r, the codes and the per-group parameters written once; with the
+    fused AdamW step also m read and written and W written back.  The
     per-group diagnostics (chosen clip, score) are off in the benchmark."""
     wb = 2.0 if wl.w_bf16 else 4.0
     rd = wb + 4.0 + (2.0 if wl.ema else 0.0)
     wr = (4.0 if wl.ema else 0.0) + wb
+    if wl.adamw:  # + m read and written, W written back; r in bf16
+        rd += 4.0
+        wr = 4.0 + 4.0 + wb + 2.0
     if wl.fmt == "nvfp4":
         wr += 0.5 + 1.0 / 16.0
         if amax_pass:
@@ -82,7 +91,7 @@ def main(argv=None):
     ap.add_argument("--gpus", type=int, default=int(os.environ.get("WORLD_SIZE", "1")))
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5", "c6", "c7"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="CPU time (thread-seconds) the oracle baseline aims to spend; the row stride of "
@@ -118,13 +127,20 @@ def main(argv=None):
     mats = []
     for (name, r, c), seed in zip(wl.shapes, wl.seeds):
         W, v, g = synth.gen_matrix(r, c, seed, w_bf16=wl.w_bf16, ema=wl.ema, device=dev)
+        mom = None
+        if wl.adamw:
+            mom, v = synth.gen_adamw_state(r, c, seed, v, device=dev)
         d = Q.Descriptor(r, c, fmt=wl.fmt, bits=wl.bits, group=wl.group, clips=wl.clips,
                          w_dtype=Q.BF16 if wl.w_bf16 else Q.F32, g_dtype=Q.BF16, beta2=wl.beta2,
                          weighting=args.weighting, param_dtype=args.param_dtype)
-        out = Q.alloc_outputs(d, W, want_r=True, want_diag=False, has_amax=wl.fmt == "nvfp4")
+        out = Q.alloc_outputs(d, W, want_r=not wl.adamw, want_diag=False, has_amax=wl.fmt == "nvfp4")
+        if wl.adamw:
+            out["r"] = torch.empty(W.shape, dtype=torch.bfloat16, device=dev)
         out["amax"] = torch.zeros(4, dtype=torch.float32, device=dev) if wl.fmt == "nvfp4" else None
-        mats.append(dict(name=name, W=W, v=v, g=g, d=d, out=out))
-    footprint = sum(m["W"].numel() * (m["W"].element_size() + 4 + (2 if wl.ema else 0)) for m in mats)
+        out["amax2"] = torch.zeros(4, dtype=torch.float32, device=dev) if wl.fmt == "nvfp4" else None
+        mats.append(dict(name=name, W=W, v=v, g=g, m=mom, d=d, out=out))
+    footprint = sum(m["W"].numel() * (m["W"].element_size() + 4 + (2 if wl.ema else 0) + (4 if wl.adamw else 0))
+                    for m in mats)
     # workloads that fit in the 256 MB last-level cache are rotated over copies
     copies = 1
     if footprint < (1 << 30):
@@ -136,9 +152,13 @@ def main(argv=None):
                 mm = dict(m)
                 if ci:
                     o2 = Q.alloc_outputs(m["d"], m["W"], want_r=True, want_diag=False, has_amax=wl.fmt == "nvfp4")
-                    o2["amax"] = None if m["out"]["amax"] is None else torch.zeros_like(m["out"]["amax"])
+                    if wl.adamw:
+                        o2["r"] = torch.empty(m["W"].shape, dtype=torch.bfloat16, device=dev)
+                    for k in ("amax", "amax2"):
+                        o2[k] = None if m["out"][k] is None else torch.zeros_like(m["out"][k])
                     mm = dict(name=m["name"], W=m["W"].clone(), v=m["v"].clone(),
-                              g=None if m["g"] is None else m["g"].clone(), d=m["d"], out=o2)
+                              g=None if m["g"] is None else m["g"].clone(),
+                              m=None if m["m"] is None else m["m"].clone(), d=m["d"], out=o2)
                 mats.append(mm)
     torch.cuda.synchronize()
     setup_s = time.time() - t0
@@ -150,8 +170,22 @@ def main(argv=None):
         if s != Q.OK:
             raise Q.QuasarError(s, "quasar_absmax")
 
+    step_no = [0]
+
     def launch(m):
         o = m["out"]
+        if wl.adamw:
+            # one optimiser step + reconstruction; NVFP4 takes this step's
+            # tensor scale from the previous step's max |W'| by-product
+            opt = Q.AdamW(1e-5, 0.9, wl.beta2, 1e-8, 0.01, step_no[0] + 1)
+            s = Q.quasar_adamw_reconstruct(m["d"], opt, m["W"], m["m"], m["v"], m["g"], o["codes"], o["scales"],
+                                           o["zeros"], o["r"], Q.BF16, None, None, o["tensor_scale"], o["amax"],
+                                           o["amax2"], stream.cuda_stream)
+            if s != Q.OK:
+                raise Q.QuasarError(s, "quasar_adamw_reconstruct")
+            if o["amax"] is not None:
+                o["amax"], o["amax2"] = o["amax2"], o["amax"]
+            return
         s = Q.quasar_reconstruct(m["d"], m["W"], m["v"], m["g"], o["codes"], o["scales"], o["zeros"], o["r"],
                                  None, None, o["tensor_scale"], o["amax"], o["workspace"], o["workspace_bytes"],
                                  stream.cuda_stream)
@@ -159,8 +193,12 @@ def main(argv=None):
             raise Q.QuasarError(s)
 
     # ---- warmup ----------------------------------------------------------------
-    nv = wl.fmt == "nvfp4"
+    nv = wl.fmt == "nvfp4" and not wl.adamw   # the plain NVFP4 path runs its absmax pass every step
+    if wl.adamw and wl.fmt == "nvfp4":
+        for m in mats:
+            launch_absmax(m)                        # the first step's tensor amax
     for i in range(args.warmup):
+        step_no[0] = i
         for m in mats[(i % copies) * per_step:(i % copies + 1) * per_step]:
             if nv:
                 launch_absmax(m)
@@ -174,6 +212,7 @@ def main(argv=None):
     t_wall = time.time()
     ev_start.record(stream)
     for i in range(args.steps):
+        step_no[0] = args.warmup + i
         for m in mats[(i % copies) * per_step:(i % copies + 1) * per_step]:
             if nv:  # NVFP4: the tensor absmax pass, timed on its own
                 a0 = torch.cuda.Event(enable_timing=True)
@@ -202,7 +241,7 @@ def main(argv=None):
         step_k.append(sum(launch_ms[sl]) + (sum(amax_ms[sl]) if amax_ms else 0.0))
     step_pct = [round(float(x), 4) for x in np.percentile(step_k, [10, 50, 90])]
 
-    amax_pass = wl.fmt == "nvfp4"
+    amax_pass = wl.fmt == "nvfp4" and not wl.adamw
     bpw = algorithmic_bytes_per_weight(wl, amax_pass)
     gw_s = n_per_step / (ms_per_step * 1e-3) / 1e9
     gbps = gw_s * bpw
@@ -246,10 +285,16 @@ def main(argv=None):
             vh = synth.to_host(m["v"].index_select(0, rows))
             gh = None if m["g"] is None else synth.to_host(m["g"].index_select(0, rows))
             amax = oracle.absmax(synth.to_host(m["W"])) if wl.fmt == "nvfp4" else None
-            t1 = time.time()
-            oracle.reconstruct(Ws, vh, fmt=wl.fmt, bits=wl.bits, group=wl.group, clips=wl.clips, g=gh,
-                               beta2=wl.beta2, tensor_amax=amax, n_threads=threads, weighting=args.weighting,
-                               param_dtype=args.param_dtype)
+            kw = dict(fmt=wl.fmt, bits=wl.bits, group=wl.group, clips=wl.clips, tensor_amax=amax,
+                      n_threads=threads, weighting=args.weighting, param_dtype=args.param_dtype)
+            if wl.adamw:
+                mh = synth.to_host(m["m"].index_select(0, rows))
+                t1 = time.time()
+                oracle.adamw_reconstruct(Ws, mh, vh, gh, lr=1e-5, beta1=0.9, beta2=wl.beta2, eps=1e-8,
+                                         weight_decay=0.01, step=1, **kw)
+            else:
+                t1 = time.time()
+                oracle.reconstruct(Ws, vh, g=gh, beta2=wl.beta2, **kw)
             return Ws.size, time.time() - t1
 
         # pilot on the largest matrix, then a stride that spends about
@@ -295,7 +340,7 @@ def main(argv=None):
             traffic_ratio = round(ent["bytes_per_weight"] / kbpw, 4)
     except (OSError, ValueError, KeyError):
         pass
-    kname = "nvfp4_reconstruct" if amax_pass else "int_reconstruct"
+    kname = "nvfp4_reconstruct" if wl.fmt == "nvfp4" else "int_reconstruct"
     if t_alu > t_hbm:
         achieved = ops_w * k_wps / 1e12
         roofline = {"bound": "alu", "achieved": round(achieved, 2), "peak": round(PEAK_VALU_TOPS, 2),
@@ -317,7 +362,8 @@ def main(argv=None):
         "config": {"workload": f"{args.workload}: {wl.description}", "matrices": per_step,
                    "weights_per_step": n_per_step, "format": wl.fmt if wl.fmt == "nvfp4" else f"int{wl.bits}",
                    "group": wl.group, "clips": len(wl.clips), "fused_ema": wl.ema,
-                   "io": ("bf16" if wl.w_bf16 else "fp32") + " W and r, fp32 v" + (", bf16 g" if wl.ema else ""),
+                   "io": (("fp32 W (updated), bf16 r, fp32 m and v, bf16 g" if wl.adamw else
+                           ("bf16" if wl.w_bf16 else "fp32") + " W and r, fp32 v" + (", bf16 g" if wl.ema else ""))),
                    "arithmetic": "fp32 codes, fp64 moments/fit/score",
                    "weighting": args.weighting, "param_dtype": args.param_dtype,
                    "cache_rotation_copies": copies},

@@ -140,6 +140,61 @@ int quasar_reconstruct(const quasar_desc* desc, const void* W, float* v, const v
  */
 int quasar_absmax(const quasar_desc* desc, const void* W, float* amax_out, void* stream);
 
+/*
+ * One optimiser step fused with the reconstruction of its result.
+ *
+ * Every method in the paper trains its latent weights with AdamW (Sec. 6.1),
+ * and QUASAR's saliency is AdamW's own second moment (Sec. 4.1.1); at every
+ * step the updated latent weights are reconstructed for the next forward pass
+ * (Sec. 3.1, Alg. 1).  This call does both in one pass over memory: per
+ * element, in fp32 and in this order,
+ *     m' = fmaf(beta1, m, (1 - beta1) g)
+ *     v' = fmaf(beta2, v, (1 - beta2) (g g))
+ *     W' = fmaf(-lr / (1 - beta1^t), m' / fmaf(sqrtf(v'), 1 / sqrt(1 - beta2^t), eps),
+ *               W (1 - lr weight_decay))
+ * (decoupled weight decay, bias-corrected; 1 - beta in fp32, the three
+ * step constants in fp64 then rounded to fp32; sqrtf and the quotient
+ * correctly rounded; a bf16 W' is rounded to nearest even), then the
+ * reconstruction of W' with saliency v' exactly as quasar_reconstruct
+ * (desc->weighting and desc->param_dtype apply; desc->beta2 is ignored).
+ */
+typedef struct {
+  float lr;            /* learning rate, finite, >= 0 */
+  float beta1;         /* first-moment decay, in [0, 1) */
+  float beta2;         /* second-moment decay, in [0.5, 1) */
+  float eps;           /* > 0 */
+  float weight_decay;  /* decoupled, finite */
+  int64_t step;        /* t >= 1, the step being taken (bias corrections) */
+} quasar_adamw;
+
+/*
+ *  W            [rows, cols] latent weights in desc->w_dtype, updated in place
+ *  m, v         [rows, cols] fp32 optimiser moments, updated in place
+ *  g            [rows, cols] gradient in desc->g_dtype (required)
+ *  codes, scales, zeros, best_clip, err, tensor_scale: as quasar_reconstruct
+ *  r            [rows, cols] or NULL, in r_dtype: QUASAR_BF16 (any W) or
+ *               QUASAR_F32 (fp32 W only)
+ *  tensor_amax  NVFP4: required, the amax the tensor scale of this step is
+ *               taken from (e.g. last step's amax_out); the updated tensor's
+ *               own absmax is not known before the pass.  INT: NULL.
+ *  amax_out     NVFP4: optional device fp32, receives max |W'| for the next
+ *               step (cleared and filled by the call).  INT: NULL.
+ * No workspace is needed.  Returns a quasar_status; on error nothing is
+ * launched and W, m, v are untouched.
+ */
+int quasar_adamw_reconstruct(const quasar_desc* desc, const quasar_adamw* opt, void* W, float* m, float* v,
+                             const void* g, uint8_t* codes, void* scales, float* zeros, void* r, int r_dtype,
+                             uint8_t* best_clip, float* err, float* tensor_scale, const float* tensor_amax,
+                             float* amax_out, void* stream);
+
+/* Host-only validation: the status quasar_adamw_reconstruct would return for
+ * these arguments (desc->beta2 is ignored, as there). */
+int quasar_adamw_check(const quasar_desc* desc, const quasar_adamw* opt, const void* W, const float* m,
+                       const float* v, const void* g, const uint8_t* codes, const void* scales,
+                       const float* zeros, const void* r, int r_dtype, const uint8_t* best_clip,
+                       const float* err, const float* tensor_scale, const float* tensor_amax,
+                       const float* amax_out);
+
 /* Host-only validation: the status quasar_reconstruct would return for these
  * arguments, without launching anything or touching device memory. */
 int quasar_check(const quasar_desc* desc, const void* W, const float* v, const void* g,

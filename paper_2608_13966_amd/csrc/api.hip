@@ -3,6 +3,8 @@
 #include <math.h>
 #include <string.h>
 
+#include <cmath>
+
 #include "quasar.h"
 #include "quasar_internal.h"
 
@@ -111,17 +113,19 @@ int quasar_absmax(const quasar_desc* d, const void* W, float* amax_out, void* st
   return e == hipSuccess ? QUASAR_OK : QUASAR_ERR_DEVICE;
 }
 
-int quasar_reconstruct(const quasar_desc* d, const void* W, float* v, const void* g, uint8_t* codes,
-                       void* scales, float* zeros, void* r, uint8_t* best_clip, float* err, float* tensor_scale,
-                       const float* tensor_amax, void* workspace, size_t workspace_bytes, void* stream) {
-  const int s = quasar_check(d, W, v, g, codes, scales, zeros, r, best_clip, err, tensor_scale, tensor_amax,
-                             workspace, workspace_bytes);
-  if (s != QUASAR_OK) return s;
-  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  const int ema_mode = g == nullptr ? 0 : (d->g_dtype == QUASAR_BF16 ? 1 : 2);
+}  // extern "C"
+
+namespace {
+
+// Launch the reconstruction (ema_mode 0-2) or the fused AdamW step plus
+// reconstruction (ema_mode 3-4) after the arguments were validated.
+int launch_path(const quasar_desc* d, const void* W, void* Wu, float* m, float* v, const void* g, int ema_mode,
+                const quasar::AdamWConsts* adam, uint8_t* codes, void* scales, float* zeros, void* r, int r_bf16,
+                uint8_t* best_clip, float* err, float* tensor_scale, const float* tensor_amax, float* amax_out,
+                void* workspace, hipStream_t st) {
   const bool w_bf16 = d->w_dtype == QUASAR_BF16;
   const int K = d->n_clips;
-  const float beta2 = g ? d->beta2 : 0.0f;
+  const float beta2 = ema_mode >= 3 ? d->beta2 : (g ? d->beta2 : 0.0f);
   const float omb2 = 1.0f - beta2;
   hipError_t e;
   if (d->format == QUASAR_INT) {
@@ -148,6 +152,10 @@ int quasar_reconstruct(const quasar_desc* d, const void* W, float* v, const void
       p.clip[k] = f;
       p.alpha[k] = qmax / (2.0f * f);
     }
+    p.Wu = Wu;
+    p.m = m;
+    if (adam) p.adam = *adam;
+    p.r_bf16 = r_bf16;
     e = quasar::launch_int(p, d->bits, d->group, w_bf16, ema_mode, st);
   } else {
     quasar::Nvfp4Params p;
@@ -171,6 +179,15 @@ int quasar_reconstruct(const quasar_desc* d, const void* W, float* v, const void
       p.clip[k] = f;
       p.c6[k] = 6.0f / f;
     }
+    p.Wu = Wu;
+    p.m = m;
+    if (adam) p.adam = *adam;
+    p.r_bf16 = r_bf16;
+    p.amax_out = reinterpret_cast<unsigned*>(amax_out);
+    if (amax_out != nullptr) {
+      e = quasar::launch_clear(p.amax_out, st);
+      if (e != hipSuccess) return QUASAR_ERR_DEVICE;
+    }
     if (tensor_amax != nullptr) {
       p.amax = tensor_amax;
     } else {
@@ -182,6 +199,73 @@ int quasar_reconstruct(const quasar_desc* d, const void* W, float* v, const void
     e = quasar::launch_nvfp4(p, w_bf16, ema_mode, st);
   }
   return e == hipSuccess ? QUASAR_OK : QUASAR_ERR_DEVICE;
+}
+
+}  // namespace
+
+extern "C" {
+
+int quasar_reconstruct(const quasar_desc* d, const void* W, float* v, const void* g, uint8_t* codes,
+                       void* scales, float* zeros, void* r, uint8_t* best_clip, float* err, float* tensor_scale,
+                       const float* tensor_amax, void* workspace, size_t workspace_bytes, void* stream) {
+  const int s = quasar_check(d, W, v, g, codes, scales, zeros, r, best_clip, err, tensor_scale, tensor_amax,
+                             workspace, workspace_bytes);
+  if (s != QUASAR_OK) return s;
+  const int ema_mode = g == nullptr ? 0 : (d->g_dtype == QUASAR_BF16 ? 1 : 2);
+  return launch_path(d, W, nullptr, nullptr, v, g, ema_mode, nullptr, codes, scales, zeros, r,
+                     d->w_dtype == QUASAR_BF16, best_clip, err, tensor_scale, tensor_amax, nullptr, workspace,
+                     reinterpret_cast<hipStream_t>(stream));
+}
+
+int quasar_adamw_check(const quasar_desc* d, const quasar_adamw* opt, const void* W, const float* m,
+                       const float* v, const void* g, const uint8_t* codes, const void* scales, const float* zeros,
+                       const void* r, int r_dtype, const uint8_t* best_clip, const float* err,
+                       const float* tensor_scale, const float* tensor_amax, const float* amax_out) {
+  if (d == nullptr || opt == nullptr) return QUASAR_ERR_ARG;
+  if (g == nullptr || m == nullptr) return QUASAR_ERR_ARG;
+  // the reconstruction's own checks (pointers, alignment, the decay range,
+  // here the optimiser's); the fused step always has its tensor amax, so no
+  // workspace is needed
+  if (d->format == QUASAR_NVFP4 && tensor_amax == nullptr) return QUASAR_ERR_ARG;
+  quasar_desc dd = *d;
+  dd.beta2 = opt->beta2;
+  int s = quasar_check(&dd, W, v, g, codes, scales, zeros, r, best_clip, err, tensor_scale,
+                       d->format == QUASAR_NVFP4 ? tensor_amax : nullptr, nullptr, 0);
+  if (s != QUASAR_OK) return s;
+  if (d->format == QUASAR_INT && (tensor_amax != nullptr || amax_out != nullptr)) return QUASAR_ERR_ARG;
+  if (!aligned16(m) || !aligned16(amax_out)) return QUASAR_ERR_ALIGN;
+  if (r_dtype != QUASAR_F32 && r_dtype != QUASAR_BF16) return QUASAR_ERR_FORMAT;
+  if (d->w_dtype == QUASAR_BF16 && r_dtype != QUASAR_BF16) return QUASAR_ERR_FORMAT;
+  if (opt->step < 1 || !(opt->eps > 0.0f) || !std::isfinite(opt->eps) || !(opt->beta1 >= 0.0f && opt->beta1 < 1.0f) ||
+      !(opt->beta2 >= 0.5f && opt->beta2 < 1.0f) || !std::isfinite(opt->lr) || !(opt->lr >= 0.0f) ||
+      !std::isfinite(opt->weight_decay))
+    return QUASAR_ERR_ARG;
+  return QUASAR_OK;
+}
+
+int quasar_adamw_reconstruct(const quasar_desc* d, const quasar_adamw* opt, void* W, float* m, float* v,
+                             const void* g, uint8_t* codes, void* scales, float* zeros, void* r, int r_dtype,
+                             uint8_t* best_clip, float* err, float* tensor_scale, const float* tensor_amax,
+                             float* amax_out, void* stream) {
+  const int s = quasar_adamw_check(d, opt, W, m, v, g, codes, scales, zeros, r, r_dtype, best_clip, err,
+                                   tensor_scale, tensor_amax, amax_out);
+  if (s != QUASAR_OK) return s;
+  quasar_desc dd = *d;
+  dd.beta2 = opt->beta2;  // the optimiser's decay updates v
+  // host constants, fp64 then fp32 (the same expressions as the oracle's)
+  quasar::AdamWConsts a;
+  a.beta1 = opt->beta1;
+  a.omb1 = 1.0f - opt->beta1;
+  a.eps = opt->eps;
+  a.decay = (float)(1.0 - (double)opt->lr * (double)opt->weight_decay);
+  const double bc1 = 1.0 - pow((double)opt->beta1, (double)opt->step);
+  const double bc2 = 1.0 - pow((double)opt->beta2, (double)opt->step);
+  a.step_size = (float)((double)opt->lr / bc1);
+  a.rbc2 = (float)(1.0 / sqrt(bc2));
+  const int ema_mode = dd.g_dtype == QUASAR_BF16 ? 3 : 4;
+  return launch_path(&dd, W, W, m, v, g, ema_mode, &a, codes, scales, zeros, r, r_dtype == QUASAR_BF16,
+                     best_clip, err, tensor_scale, tensor_amax, amax_out, nullptr,
+                     reinterpret_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

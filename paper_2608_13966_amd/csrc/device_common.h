@@ -126,13 +126,57 @@ struct WRegs<true> {
   __device__ __forceinline__ float get(int i) const {
     return (i & 1) ? as_f32(d[i >> 1] & 0xffff0000u) : as_f32(d[i >> 1] << 16);
   }
+  // replace the weights by w rounded to bf16 (nearest even)
+  __device__ __forceinline__ void set(const float (&w)[16]) {
+#pragma unroll
+    for (int k = 0; k < 8; k++) d[k] = pack_bf16x2(w[2 * k], w[2 * k + 1]);
+  }
+  __device__ __forceinline__ void store(void* base, int64_t e0) const {
+    uint16_t* p = reinterpret_cast<uint16_t*>(base) + e0;
+    st128(p, make_uint4(d[0], d[1], d[2], d[3]));
+    st128(p + 8, make_uint4(d[4], d[5], d[6], d[7]));
+  }
 };
 template <>
 struct WRegs<false> {
   float f[16];
   __device__ __forceinline__ void load(const void* base, int64_t e0) { load16<false>(base, e0, f); }
   __device__ __forceinline__ float get(int i) const { return f[i]; }
+  __device__ __forceinline__ void set(const float (&w)[16]) {
+#pragma unroll
+    for (int i = 0; i < 16; i++) f[i] = w[i];
+  }
+  __device__ __forceinline__ void store(void* base, int64_t e0) const { store16<false>(base, e0, f); }
 };
+
+// Constants of one AdamW step, computed on the host.
+struct AdamWConsts {
+  float beta1, omb1;     // beta1 and 1 - beta1 (fp32)
+  float eps;
+  float decay;           // 1 - lr * weight_decay
+  float step_size;       // lr / (1 - beta1^t)
+  float rbc2;            // 1 / sqrt(1 - beta2^t)
+};
+
+// One AdamW step (decoupled weight decay, bias-corrected) on 16 weights, in
+// place, fp32 in a fixed order:
+//   m' = fmaf(beta1, m, (1 - beta1) g)        v' = fmaf(beta2, v, (1 - beta2) (g g))
+//   w' = fmaf(-step_size, m' / fmaf(sqrtf(v'), rbc2, eps), w * decay)
+// sqrtf and the quotient are the correctly rounded ones.
+__device__ __forceinline__ void adamw16(float (&w)[16], float (&m)[16], float (&v)[16], const float (&g)[16],
+                                        const AdamWConsts& a, float beta2, float omb2) {
+#pragma unroll
+  for (int i = 0; i < 16; i++) {
+    const float mm = __builtin_fmaf(a.beta1, m[i], a.omb1 * g[i]);
+    const float t = g[i] * g[i];
+    const float vv = __builtin_fmaf(beta2, v[i], omb2 * t);
+    const float den = __builtin_fmaf(__builtin_sqrtf(vv), a.rbc2, a.eps);
+    const float upd = mm / den;
+    m[i] = mm;
+    v[i] = vv;
+    w[i] = __builtin_fmaf(-a.step_size, upd, w[i] * a.decay);
+  }
+}
 
 // ---- DPP exchanges (GFX9 encodings; all stay inside a row of 16 lanes) ------
 constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]

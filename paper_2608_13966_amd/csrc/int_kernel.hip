@@ -67,7 +67,7 @@ void int_reconstruct_kernel(IntParams p) {
   wr.load(p.W, e0);
   float v[N];
   load16<false>(p.v, e0, v);
-  if constexpr (EMA != 0) {
+  if constexpr (EMA == 1 || EMA == 2) {
     float g[N];
     load16<EMA == 1>(p.g, e0, g);
 #pragma unroll
@@ -78,6 +78,21 @@ void int_reconstruct_kernel(IntParams p) {
       v[i] = __builtin_fmaf(p.beta2, v[i], u);
     }
     if (active) store16<false>(p.v, e0, v);
+  } else if constexpr (EMA >= 3) {
+    // one AdamW step first; the updated W is reconstructed and the updated
+    // second moment is the saliency
+    float g[N], m[N], w[N];
+    load16<EMA == 3>(p.g, e0, g);
+    load16<false>(p.m, e0, m);
+#pragma unroll
+    for (int i = 0; i < N; i++) w[i] = wr.get(i);
+    adamw16(w, m, v, g, p.adam, p.beta2, p.omb2);
+    wr.set(w);  // bf16 W: rounded here, and the rounded value is reconstructed
+    if (active) {
+      store16<false>(p.v, e0, v);
+      store16<false>(p.m, e0, m);
+      wr.store(p.Wu, e0);
+    }
   }
   // saliency weighting (uniform branch): h = v, v*v (App. A.3) or 1 (Table 5)
   if (p.weighting != 0) {
@@ -259,7 +274,12 @@ void int_reconstruct_kernel(IntParams p) {
     r[i] = __builtin_fmaf(a, q, b);
   }
   if (!active) return;
-  if (p.r) store16<W_BF16>(p.r, e0, r);
+  if (p.r) {
+    if (W_BF16 || p.r_bf16)
+      store16<true>(p.r, e0, r);
+    else
+      store16<false>(p.r, e0, r);
+  }
   if constexpr (BITS == 4) {
     uint32_t lo = 0, hi = 0;
 #pragma unroll
@@ -329,6 +349,8 @@ hipError_t launch_e(const IntParams& p, int bits, int group, int ema_mode, hipSt
   switch (ema_mode) {
     case 1: return launch_b<W_BF16, 1>(p, bits, group, s);
     case 2: return launch_b<W_BF16, 2>(p, bits, group, s);
+    case 3: return launch_b<W_BF16, 3>(p, bits, group, s);
+    case 4: return launch_b<W_BF16, 4>(p, bits, group, s);
     default: return launch_b<W_BF16, 0>(p, bits, group, s);
   }
 }

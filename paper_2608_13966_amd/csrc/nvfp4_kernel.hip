@@ -46,7 +46,7 @@ void nvfp4_reconstruct_kernel(Nvfp4Params p) {
   wr.load(p.W, e0);
   float v[N];
   load16<false>(p.v, e0, v);
-  if constexpr (EMA != 0) {
+  if constexpr (EMA == 1 || EMA == 2) {
     float g[N];
     load16<EMA == 1>(p.g, e0, g);
 #pragma unroll
@@ -56,6 +56,20 @@ void nvfp4_reconstruct_kernel(Nvfp4Params p) {
       v[i] = __builtin_fmaf(p.beta2, v[i], u);
     }
     if (active) store16<false>(p.v, e0, v);
+  } else if constexpr (EMA >= 3) {
+    // one AdamW step first (see int_kernel.hip)
+    float g[N], m[N], w[N];
+    load16<EMA == 3>(p.g, e0, g);
+    load16<false>(p.m, e0, m);
+#pragma unroll
+    for (int i = 0; i < N; i++) w[i] = wr.get(i);
+    adamw16(w, m, v, g, p.adam, p.beta2, p.omb2);
+    wr.set(w);
+    if (active) {
+      store16<false>(p.v, e0, v);
+      store16<false>(p.m, e0, m);
+      wr.store(p.Wu, e0);
+    }
   }
   if (p.weighting != 0) {  // h = v, v*v or 1 (uniform branch)
 #pragma unroll
@@ -181,8 +195,25 @@ void nvfp4_reconstruct_kernel(Nvfp4Params p) {
   QUASAR_GET(0, 0) QUASAR_GET(0, 1) QUASAR_GET(0, 2) QUASAR_GET(0, 3)
   QUASAR_GET(1, 0) QUASAR_GET(1, 1) QUASAR_GET(1, 2) QUASAR_GET(1, 3)
 #undef QUASAR_GET
+  if constexpr (EMA >= 3) {
+    // by-product of the fused step: max |W'| for the next step's tensor scale.
+    // One atomic per wavefront, skipped when the stored maximum is already
+    // larger (|w| >= 0, so fp32 bit patterns order like unsigned integers).
+    if (p.amax_out) {
+      float mw = run_max<16>(m);
+      mw = fmaxf(mw, __shfl_xor(mw, 16, 64));
+      mw = fmaxf(mw, __shfl_xor(mw, 32, 64));
+      if ((tid & 63) == 0 && __float_as_uint(mw) > __builtin_nontemporal_load(p.amax_out))
+        atomicMax(p.amax_out, __float_as_uint(mw));
+    }
+  }
   if (!active) return;
-  if (p.r) store16<W_BF16>(p.r, e0, r);
+  if (p.r) {
+    if (W_BF16 || p.r_bf16)
+      store16<true>(p.r, e0, r);
+    else
+      store16<false>(p.r, e0, r);
+  }
   *reinterpret_cast<uint2*>(p.codes + bid * 8) = make_uint2(cw[0], cw[1]);
   p.scales[bid] = (uint8_t)best_e;
   if (p.best_clip) p.best_clip[bid] = (uint8_t)kstar;
@@ -264,6 +295,8 @@ hipError_t launch_e(const Nvfp4Params& p, int ema_mode, hipStream_t s) {
   switch (ema_mode) {
     case 1: return launch_kc<W_BF16, 1>(p, s);
     case 2: return launch_kc<W_BF16, 2>(p, s);
+    case 3: return launch_kc<W_BF16, 3>(p, s);
+    case 4: return launch_kc<W_BF16, 4>(p, s);
     default: return launch_kc<W_BF16, 0>(p, s);
   }
 }
@@ -272,6 +305,11 @@ hipError_t launch_e(const Nvfp4Params& p, int ema_mode, hipStream_t s) {
 
 hipError_t launch_nvfp4(const Nvfp4Params& p, bool w_bf16, int ema_mode, hipStream_t s) {
   return w_bf16 ? launch_e<true>(p, ema_mode, s) : launch_e<false>(p, ema_mode, s);
+}
+
+hipError_t launch_clear(unsigned* ws, hipStream_t s) {
+  hipLaunchKernelGGL(absmax_clear_kernel, dim3(1), dim3(64), 0, s, ws);
+  return hipGetLastError();
 }
 
 hipError_t launch_absmax(const void* W, bool w_bf16, int64_t n, unsigned* ws, hipStream_t s) {

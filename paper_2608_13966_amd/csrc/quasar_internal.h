@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "device_common.h"
+
 namespace quasar {
 
 constexpr int kMaxClips = 16;
@@ -28,6 +30,12 @@ struct IntParams {
   int param_dtype;      // 0 fp32, 1 bf16, 2 fp16 (quasar_dtype values)
   float alpha[kMaxClips];  // qmax / (2 f_k), fp32 division on the host
   float clip[kMaxClips];   // f_k
+  // fused AdamW step (ema modes 3 and 4): W is updated in place through Wu,
+  // m and v are updated; r may be bf16 while W is fp32
+  void* Wu;
+  float* m;
+  AdamWConsts adam;
+  int r_bf16;
 };
 
 // Per-call parameters of the NVFP4 kernels.
@@ -48,6 +56,11 @@ struct Nvfp4Params {
   int weighting;
   float c6[kMaxClips];  // 6 / f_k, fp32 division on the host
   float clip[kMaxClips];
+  void* Wu;             // fused AdamW step, as IntParams
+  float* m;
+  AdamWConsts adam;
+  int r_bf16;
+  unsigned* amax_out;   // fused step: max |W'| (fp32 bits, atomic max; cleared first) or NULL
 };
 
 // Launchers (return the hipGetLastError() of the launches).
@@ -56,5 +69,8 @@ hipError_t launch_nvfp4(const Nvfp4Params& p, bool w_bf16, int ema_mode, hipStre
 // amax over n elements of W into *ws (as fp32 bits); clears *ws first.
 hipError_t launch_absmax(const void* W, bool w_bf16, int64_t n, unsigned* ws, hipStream_t s);
 
-// ema_mode: 0 = no gradient, 1 = bf16 gradient, 2 = fp32 gradient
+// ema_mode: 0 = no gradient, 1 = EMA from a bf16 gradient, 2 = EMA from an fp32
+// gradient, 3 = AdamW step from a bf16 gradient, 4 = AdamW step from an fp32 gradient
+// clear *ws to 0 (a kernel, so that it may be captured in a graph)
+hipError_t launch_clear(unsigned* ws, hipStream_t s);
 }  // namespace quasar

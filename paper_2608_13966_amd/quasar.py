@@ -29,8 +29,9 @@ WEIGHTINGS = {"h": WEIGHT_H, "h2": WEIGHT_H2, "none": WEIGHT_NONE}
 PARAM_DTYPES = {"fp32": F32, "fp16": F16, "bf16": BF16}
 MAX_CLIPS = 16
 
-EXPORTS = ("quasar_reconstruct", "quasar_absmax", "quasar_check", "quasar_num_groups", "quasar_codes_bytes",
-           "quasar_workspace_bytes", "quasar_status_string", "quasar_version")
+EXPORTS = ("quasar_reconstruct", "quasar_absmax", "quasar_check", "quasar_adamw_reconstruct", "quasar_adamw_check",
+           "quasar_num_groups", "quasar_codes_bytes", "quasar_workspace_bytes", "quasar_status_string",
+           "quasar_version")
 
 
 class QuasarError(RuntimeError):
@@ -44,6 +45,12 @@ class Desc(C.Structure):
                 ("bits", C.c_int32), ("group", C.c_int32), ("clip_ratios", C.POINTER(C.c_float)),
                 ("n_clips", C.c_int32), ("g_dtype", C.c_int32), ("beta2", C.c_float),
                 ("weighting", C.c_int32), ("param_dtype", C.c_int32)]
+
+
+class AdamW(C.Structure):
+    """quasar_adamw: the hyper-parameters of one AdamW step."""
+    _fields_ = [("lr", C.c_float), ("beta1", C.c_float), ("beta2", C.c_float), ("eps", C.c_float),
+                ("weight_decay", C.c_float), ("step", C.c_int64)]
 
 
 _lib = None
@@ -66,6 +73,12 @@ def lib():
             L.quasar_absmax.restype = C.c_int
             L.quasar_check.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, C.c_size_t]
             L.quasar_check.restype = C.c_int
+            ap = C.POINTER(AdamW)
+            L.quasar_adamw_reconstruct.argtypes = [dp, ap, vp, vp, vp, vp, vp, vp, vp, vp, C.c_int, vp, vp, vp, vp,
+                                                   vp, vp]
+            L.quasar_adamw_reconstruct.restype = C.c_int
+            L.quasar_adamw_check.argtypes = [dp, ap, vp, vp, vp, vp, vp, vp, vp, vp, C.c_int, vp, vp, vp, vp, vp]
+            L.quasar_adamw_check.restype = C.c_int
             L.quasar_num_groups.argtypes = [dp]
             L.quasar_num_groups.restype = C.c_int64
             L.quasar_codes_bytes.argtypes = [dp]
@@ -123,6 +136,20 @@ def quasar_check(d: Descriptor, W, v, g, codes, scales, zeros, r, best_clip, err
     return lib().quasar_check(d.ref, _p(W), _p(v), _p(g), _p(codes), _p(scales), _p(zeros), _p(r),
                               _p(best_clip), _p(err), _p(tensor_scale), _p(tensor_amax), _p(workspace),
                               int(workspace_bytes))
+
+
+def quasar_adamw_reconstruct(d: Descriptor, opt: AdamW, W, m, v, g, codes, scales, zeros, r, r_dtype: int,
+                             best_clip, err, tensor_scale, tensor_amax, amax_out, stream) -> int:
+    return lib().quasar_adamw_reconstruct(d.ref, C.byref(opt), _p(W), _p(m), _p(v), _p(g), _p(codes), _p(scales),
+                                          _p(zeros), _p(r), int(r_dtype), _p(best_clip), _p(err),
+                                          _p(tensor_scale), _p(tensor_amax), _p(amax_out), stream)
+
+
+def quasar_adamw_check(d: Descriptor, opt: AdamW, W, m, v, g, codes, scales, zeros, r, r_dtype: int, best_clip,
+                       err, tensor_scale, tensor_amax, amax_out) -> int:
+    return lib().quasar_adamw_check(d.ref, None if opt is None else C.byref(opt), _p(W), _p(m), _p(v), _p(g),
+                                    _p(codes), _p(scales), _p(zeros), _p(r), int(r_dtype), _p(best_clip), _p(err),
+                                    _p(tensor_scale), _p(tensor_amax), _p(amax_out))
 
 
 def quasar_num_groups(d: Descriptor) -> int:
@@ -207,5 +234,42 @@ def reconstruct(W, v, g=None, *, fmt="int", bits=4, group=128, clips=(1.0,), bet
                            stream)
     if s != OK:
         raise QuasarError(s)
+    out["desc"] = d
+    return out
+
+
+def adamw_reconstruct(W, m, v, g, *, lr, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, step=1, fmt="int",
+                      bits=4, group=128, clips=(1.0,), tensor_amax=None, r_dtype=None, want_r=True, want_diag=True,
+                      want_amax_out=False, out=None, stream=None, weighting="h", param_dtype="fp32"):
+    """One fused AdamW step + reconstruction (quasar_adamw_reconstruct).
+
+    W (fp32 or bf16), m and v (fp32) are updated in place; g is the gradient
+    (fp32 or bf16).  r is bf16 unless r_dtype="fp32" (fp32 W only).  NVFP4
+    needs ``tensor_amax`` (device fp32 tensor); ``want_amax_out`` adds
+    ``amax_out`` = max |W'| to the returned dict.
+    """
+    import torch
+    for t in (W, m, v, g):
+        if not t.is_contiguous() or t.shape != W.shape:
+            raise ValueError("W, m, v, g must be contiguous tensors of one shape")
+    if m.dtype != torch.float32 or v.dtype != torch.float32:
+        raise ValueError("m and v must be fp32")
+    d = Descriptor(W.shape[0], W.shape[1], fmt=fmt, bits=bits, group=group, clips=clips, w_dtype=_dtype_code(W),
+                   g_dtype=_dtype_code(g), beta2=beta2, weighting=weighting, param_dtype=param_dtype)
+    rd = BF16 if r_dtype in (None, "bf16") else F32
+    if out is None:
+        out = alloc_outputs(d, W, want_r=False, want_diag=want_diag, has_amax=True)
+        if want_r:
+            out["r"] = torch.empty(W.shape, dtype=torch.bfloat16 if rd == BF16 else torch.float32, device=W.device)
+        out["amax_out"] = (torch.empty(4, dtype=torch.float32, device=W.device)
+                           if (want_amax_out and fmt == "nvfp4") else None)
+    if stream is None:
+        stream = torch.cuda.current_stream(W.device).cuda_stream
+    opt = AdamW(lr, beta1, beta2, eps, weight_decay, int(step))
+    s = quasar_adamw_reconstruct(d, opt, W, m, v, g, out["codes"], out["scales"], out["zeros"], out.get("r"), rd,
+                                 out["best_clip"], out["err"], out["tensor_scale"], tensor_amax,
+                                 out.get("amax_out"), stream)
+    if s != OK:
+        raise QuasarError(s, "quasar_adamw_reconstruct")
     out["desc"] = d
     return out

@@ -57,6 +57,7 @@ class Workload:
     ema: bool
     beta2: float = 0.999
     layers: int = 1
+    adamw: bool = False      # one fused AdamW step (fp32 m, v; the gradient g) before the reconstruction
     extra: dict = field(default_factory=dict)
 
     @property
@@ -93,13 +94,22 @@ def workloads() -> dict:
                        "fused EMA (one simulated training step)",
                        l8x32, l8x32s, "int", 4, 128, tuple(clip_grid(1.0, 0.65, 8)), w_bf16=True,
                        ema=True, layers=32),
+        "c6": Workload("c6", "Llama-3.1-8B-shaped layer set, fp32 master W, one fused AdamW step (fp32 m, v, "
+                       "bf16 g) + INT2 g64 reconstruction, 12 clips 1.0..0.5, bf16 r",
+                       l8, l8s, "int", 2, 64, tuple(clip_grid(1.0, 0.5, 12)), w_bf16=False, ema=True,
+                       adamw=True),
+        "c7": Workload("c7", "Llama-3.1-8B-shaped layer set, fp32 master W, one fused AdamW step (fp32 m, v, "
+                       "bf16 g) + NVFP4 reconstruction, 8 clips 1.0..0.7, bf16 r, tensor amax from the "
+                       "previous step's by-product",
+                       l8, l8s, "nvfp4", 4, 16, tuple(clip_grid(1.0, 0.7, 8)), w_bf16=False, ema=True,
+                       adamw=True),
     }
 
 
 def gen_matrix(rows: int, cols: int, seed: int, *, w_bf16: bool, ema: bool, device="cpu",
                outliers: int = 4):
     """Draw (W, v, g) for one matrix on ``device`` (torch tensors; g is None
-    without an EMA)."""
+    without an EMA).  For the fused optimiser step see ``gen_adamw_state``."""
     gen = torch.Generator(device=device)
     gen.manual_seed(int(seed))
     W = torch.randn(rows, cols, generator=gen, device=device, dtype=torch.float32) * 0.02
@@ -117,6 +127,16 @@ def gen_matrix(rows: int, cols: int, seed: int, *, w_bf16: bool, ema: bool, devi
     if w_bf16:
         W = W.to(torch.bfloat16)
     return W, v, g
+
+
+def gen_adamw_state(rows: int, cols: int, seed: int, v, device="cpu"):
+    """The optimiser state of a fused AdamW workload: m ~ N(0, 1e-4^2) from its
+    own generator (seed + 17), and the second moment v of ``gen_matrix``
+    scaled by 1e-6 (the size of squared gradients of the drawn g)."""
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(seed) + 17)
+    m = torch.randn(rows, cols, generator=gen, device=device, dtype=torch.float32) * 1e-4
+    return m, v * 1e-6
 
 
 def to_host(t):

@@ -125,3 +125,43 @@ def test_absmax_entry_point_validation():
     assert Q.quasar_absmax(nv, A, None, None) == Q.ERR_ARG
     assert Q.quasar_absmax(nv, A + 4, A, None) == Q.ERR_ALIGN
     assert Q.quasar_absmax(_int_desc(fmt="nvfp4", cols=24), A, A, None) == Q.ERR_SHAPE
+
+
+def _adam_check(d, opt=None, **ptrs):
+    if opt is None:
+        opt = Q.AdamW(1e-3, 0.9, 0.999, 1e-8, 0.01, 1)
+    p = dict(W=A, m=A, v=A, g=A, codes=A, scales=A, zeros=A, r=A, r_dtype=Q.BF16, best_clip=A, err=A,
+             tensor_scale=None, tensor_amax=None, amax_out=None)
+    if d.desc.format == Q.NVFP4:
+        p.update(zeros=None, tensor_scale=A, tensor_amax=A)
+    p.update(ptrs)
+    return Q.quasar_adamw_check(d, opt, p["W"], p["m"], p["v"], p["g"], p["codes"], p["scales"], p["zeros"],
+                                p["r"], p["r_dtype"], p["best_clip"], p["err"], p["tensor_scale"],
+                                p["tensor_amax"], p["amax_out"])
+
+
+def test_adamw_entry_point_validation():
+    f32 = _int_desc(w_dtype=Q.F32)
+    assert _adam_check(f32) == Q.OK
+    assert _adam_check(f32, r_dtype=Q.F32) == Q.OK
+    assert _adam_check(_int_desc(beta2=0.0)) == Q.OK          # desc->beta2 is ignored
+    assert _adam_check(_int_desc(), r_dtype=Q.F32) == Q.ERR_FORMAT   # bf16 W needs bf16 r
+    assert _adam_check(f32, r_dtype=Q.F16) == Q.ERR_FORMAT
+    nv = _int_desc(fmt="nvfp4", w_dtype=Q.F32)
+    assert _adam_check(nv) == Q.OK
+    assert _adam_check(nv, amax_out=A) == Q.OK
+    assert _adam_check(nv, tensor_amax=None) == Q.ERR_ARG      # the tensor scale needs an amax
+    assert _adam_check(f32, tensor_amax=A) == Q.ERR_ARG
+    assert _adam_check(f32, amax_out=A) == Q.ERR_ARG
+    assert _adam_check(nv, amax_out=A + 4) == Q.ERR_ALIGN
+    for name in ("m", "g", "W", "v", "codes", "scales"):
+        assert _adam_check(f32, **{name: None}) == Q.ERR_ARG, name
+    assert _adam_check(f32, m=A + 8) == Q.ERR_ALIGN
+    assert Q.quasar_adamw_check(f32, None, A, A, A, A, A, A, A, A, Q.BF16, A, A, None, None, None) == Q.ERR_ARG
+    bad = [dict(step=0), dict(eps=0.0), dict(eps=float("inf")), dict(beta1=1.0), dict(beta1=-0.1),
+           dict(beta2=0.4), dict(beta2=1.0), dict(lr=float("nan")), dict(lr=-1.0), dict(weight_decay=float("inf"))]
+    for b in bad:
+        hp = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01, step=1)
+        hp.update(b)
+        opt = Q.AdamW(hp["lr"], hp["beta1"], hp["beta2"], hp["eps"], hp["weight_decay"], hp["step"])
+        assert _adam_check(f32, opt) == Q.ERR_ARG, b
