@@ -10,7 +10,8 @@ already resident in HBM.  Prints ONE JSON line.
 Workloads (paper_2608_13966_amd/synth.py): c1 single fp32 1024x1024 INT4;
 c2 Qwen3-0.6B-shaped layer set INT3; c3 Llama-3.1-8B-shaped layer set INT2
 g64, 12 clips, fused EMA (default); c4 the same set in NVFP4; c5 32 such
-layers INT4 with fused EMA (one simulated training step); c6 / c7 the
+layers INT4 with fused EMA (one simulated training step); c8 the Llama set
+in the Rubin INT3 LUT format with the paper's 15 clip factors; c6 / c7 the
 Llama-3.1-8B set with fp32 master weights, one fused AdamW step followed by
 the INT2 / NVFP4 reconstruction (a step then includes the optimiser update).
 """
@@ -58,6 +59,9 @@ def algorithmic_valu_ops_per_weight(wl) -> float:
     pre = 10.0 if wl.adamw else (3.0 if wl.ema else 0.0)
     if wl.fmt == "nvfp4":
         return 5.0 * K + 8.0 + pre
+    if wl.fmt == "rubin":
+        # per clip: the code (3), the index address (2), two bin sums (2)
+        return 7.0 * K + 12.0 + pre
     return 7.0 * K + 9.0 + pre
 
 
@@ -76,6 +80,8 @@ def algorithmic_bytes_per_weight(wl, amax_pass: bool) -> float:
         wr += 0.5 + 1.0 / 16.0
         if amax_pass:
             rd += wb  # the tensor absmax pass reads W once more
+    elif wl.fmt == "rubin":
+        wr += 3.0 / 8.0 + 8.0 / 512.0   # 3-bit indices, 8 codebook bytes per 512 weights
     else:
         wr += wl.bits / 8.0 + 8.0 / wl.group
     return rd + wr
@@ -91,7 +97,7 @@ def main(argv=None):
     ap.add_argument("--gpus", type=int, default=int(os.environ.get("WORLD_SIZE", "1")))
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5", "c6", "c7"])
+    ap.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5", "c6", "c7", "c8"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="CPU time (thread-seconds) the oracle baseline aims to spend; the row stride of "
@@ -280,7 +286,11 @@ def main(argv=None):
         threads = min(16, os.cpu_count() or 1)
 
         def oracle_rows(m, step):
-            rows = torch.arange(0, m["W"].shape[0], step, device=dev)
+            if wl.fmt == "rubin":  # whole 8-row blocks
+                brows = torch.arange(0, m["W"].shape[0] // 8, step, device=dev)
+                rows = (brows[:, None] * 8 + torch.arange(8, device=dev)[None, :]).reshape(-1)
+            else:
+                rows = torch.arange(0, m["W"].shape[0], step, device=dev)
             Ws = synth.to_host(m["W"].index_select(0, rows))
             vh = synth.to_host(m["v"].index_select(0, rows))
             gh = None if m["g"] is None else synth.to_host(m["g"].index_select(0, rows))
@@ -292,6 +302,10 @@ def main(argv=None):
                 t1 = time.time()
                 oracle.adamw_reconstruct(Ws, mh, vh, gh, lr=1e-5, beta1=0.9, beta2=wl.beta2, eps=1e-8,
                                          weight_decay=0.01, step=1, **kw)
+            elif wl.fmt == "rubin":
+                t1 = time.time()
+                oracle.rubin_reconstruct(Ws, vh, clips=wl.clips, g=gh, beta2=wl.beta2, weighting=args.weighting,
+                                         n_threads=threads)
             else:
                 t1 = time.time()
                 oracle.reconstruct(Ws, vh, g=gh, beta2=wl.beta2, **kw)
@@ -320,7 +334,8 @@ def main(argv=None):
             step = max(1, int(step * spent / args.cpu_seconds))
         cpu = {"value": round(sample_w / t_cpu / 1e9, 6), "unit": "G weights/s", "cores": threads,
                "kind": "oracle",
-               "sample": f"rows 0, {step}, {2 * step}, ... of every matrix of {args.workload} ({sample_w} weights, "
+               "sample": f"{'block ' if wl.fmt == 'rubin' else ''}rows 0, {step}, {2 * step}, ... of every matrix "
+                         f"of {args.workload} ({sample_w} weights, "
                          f"{t_cpu:.1f} s wall = {t_cpu * threads:.0f} thread-s on {threads} threads; "
                          f"fp64 fit/score)"}
 
@@ -340,7 +355,7 @@ def main(argv=None):
             traffic_ratio = round(ent["bytes_per_weight"] / kbpw, 4)
     except (OSError, ValueError, KeyError):
         pass
-    kname = "nvfp4_reconstruct" if wl.fmt == "nvfp4" else "int_reconstruct"
+    kname = {"nvfp4": "nvfp4_reconstruct", "rubin": "rubin_reconstruct"}.get(wl.fmt, "int_reconstruct")
     if t_alu > t_hbm:
         achieved = ops_w * k_wps / 1e12
         roofline = {"bound": "alu", "achieved": round(achieved, 2), "peak": round(PEAK_VALU_TOPS, 2),
@@ -360,7 +375,8 @@ def main(argv=None):
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f64", "data": "synthetic",
         "config": {"workload": f"{args.workload}: {wl.description}", "matrices": per_step,
-                   "weights_per_step": n_per_step, "format": wl.fmt if wl.fmt == "nvfp4" else f"int{wl.bits}",
+                   "weights_per_step": n_per_step,
+                   "format": {"nvfp4": "nvfp4", "rubin": "rubin-int3-lut"}.get(wl.fmt, f"int{wl.bits}"),
                    "group": wl.group, "clips": len(wl.clips), "fused_ema": wl.ema,
                    "io": (("fp32 W (updated), bf16 r, fp32 m and v, bf16 g" if wl.adamw else
                            ("bf16" if wl.w_bf16 else "fp32") + " W and r, fp32 v" + (", bf16 g" if wl.ema else ""))),

@@ -165,3 +165,23 @@ def test_adamw_entry_point_validation():
         hp.update(b)
         opt = Q.AdamW(hp["lr"], hp["beta1"], hp["beta2"], hp["eps"], hp["weight_decay"], hp["step"])
         assert _adam_check(f32, opt) == Q.ERR_ARG, b
+
+
+def test_rubin_descriptor_validation_and_sizes():
+    d = _int_desc(fmt="rubin", rows=16, cols=128)
+    assert _check(d, zeros=None) == Q.OK
+    assert Q.quasar_num_groups(d) == 4
+    assert Q.quasar_codes_bytes(d) == 4 * 192
+    assert Q.quasar_workspace_bytes(d, 0) == 0
+    assert _check(_int_desc(fmt="rubin", rows=12, cols=128), zeros=None) == Q.ERR_SHAPE
+    assert _check(_int_desc(fmt="rubin", rows=16, cols=96), zeros=None) == Q.ERR_SHAPE
+    assert _check(_int_desc(fmt="rubin", rows=16, cols=128, param_dtype="fp16"), zeros=None) == Q.ERR_FORMAT
+    assert _check(d, zeros=None, tensor_amax=A) == Q.ERR_ARG
+    assert _check(d, zeros=None, scales=None) == Q.ERR_ARG
+    bad = Q.Descriptor(16, 128, fmt="rubin")
+    bad.desc.group = 128
+    assert _check(bad, zeros=None) == Q.ERR_FORMAT
+    bad.desc.group, bad.desc.bits = 512, 4
+    assert _check(bad, zeros=None) == Q.ERR_FORMAT
+    # not fused with the optimiser step
+    assert _adam_check(_int_desc(fmt="rubin", rows=16, cols=128, w_dtype=Q.F32), zeros=None) == Q.ERR_FORMAT

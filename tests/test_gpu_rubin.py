@@ -1,0 +1,138 @@
+"""GPU parity of the Rubin INT3 LUT reconstruction (QUASAR_RUBIN_INT3)
+against the oracle on the same seeded bytes.
+
+Bit-exact: EMA v', chosen clip, codes, codebook bytes, r.  Excused and
+counted: a different clip whose oracle scores are within 1e-6 (plus the
+score's rounding floor), and a codebook byte whose oracle mean lies within
+1e-6 of an E4M3 rounding midpoint (the GPU rounds the mean through fp32);
+r of that index then follows the GPU's entry."""
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_13966_amd import quasar as Q
+from paper_2608_13966_amd import synth
+from tests.test_gpu_parity import THREADS, host, record
+from tests import _exact as X
+
+pytestmark = pytest.mark.gpu
+
+_LEVELS = np.array(sorted({v for v, _ in X.e4m3_levels()} | {-v for v, _ in X.e4m3_levels()}))
+_MIDS = (_LEVELS[1:] + _LEVELS[:-1]) / 2
+
+
+def _blocks(a, rows, cols):
+    return a.reshape(rows // 8, 8, cols // 64, 64).transpose(0, 2, 1, 3).reshape(-1, 512)
+
+
+def _f32(a):
+    return (a.astype(np.uint32) << 16).view(np.float32) if a.dtype == np.uint16 else a
+
+
+def run_rubin(name, W, v, g=None, *, clips, weighting="h", row_step_blocks=1):
+    R, C = W.shape
+    Wh, vh, gh = host(W), host(v), host(g)
+    print(f"[case] {name} shape={(R, C)} K={len(clips)} ema={g is not None} w={weighting}", flush=True)
+    out = Q.reconstruct(W, v, g, fmt="rubin", clips=clips, weighting=weighting)
+    torch.cuda.synchronize()
+    brows = np.arange(0, R // 8, row_step_blocks)
+    rows = (brows[:, None] * 8 + np.arange(8)[None, :]).ravel()
+    bpr = C // 64
+    bidx = (brows[:, None] * bpr + np.arange(bpr)[None, :]).ravel()
+    o = oracle.rubin_reconstruct(Wh[rows], vh[rows], clips=clips, g=None if gh is None else gh[rows], beta2=0.999,
+                                 weighting=weighting, want_scores=True, n_threads=THREADS)
+    fails, st = [], {"groups": len(bidx), "near_tie": 0, "near_e4m3": 0}
+    if g is not None:
+        bad = np.count_nonzero(o["v_out"].view(np.uint32) != host(v)[rows].view(np.uint32))
+        if bad:
+            fails.append(f"EMA v' differs in {bad} elements")
+    h = o["v_out"] if g is not None else vh[rows]
+    h = (h * h).astype(np.float32) if weighting == "h2" else np.ones_like(h) if weighting == "none" else h
+    Rs = len(rows)
+    wb = _blocks(_f32(Wh[rows]), Rs, C).astype(np.float64)
+    hb = _blocks(h, Rs, C).astype(np.float64)
+    ob, gb = o["best"].astype(int), out["best_clip"].cpu().numpy()[bidx].astype(int)
+    floor = 1e-12 * np.sum(hb * wb * wb, axis=1)
+    same = ob == gb
+    for i in np.flatnonzero(~same):
+        so, sg = o["scores"][i, ob[i]], o["scores"][i, gb[i]]
+        if abs(sg - so) <= 1e-6 * so + floor[i]:
+            st["near_tie"] += 1
+        else:
+            fails.append(f"block {i}: clip {gb[i]} vs oracle {ob[i]}, scores {sg} vs {so}")
+    gcodes = out["codes"].cpu().numpy().reshape(-1, 192)[bidx]
+    glut = out["scales"].cpu().numpy().reshape(-1, 8)[bidx]
+    gr = _blocks(host(out["r"])[rows], Rs, C)
+    orr = _blocks(o["r"], Rs, C)
+    qb = _blocks(o["codes"], Rs, C)
+    ge = out["err"].cpu().numpy()[bidx].astype(np.float64)
+    for i in np.flatnonzero(same):
+        if not np.array_equal(gcodes[i], o["codes_packed"].reshape(-1, 192)[i]):
+            fails.append(f"block {i}: codes differ")
+            continue
+        lut_ok = glut[i] == o["lut"][i]
+        for k in np.flatnonzero(~lut_ok):
+            m = qb[i] == k
+            mean = np.sum(hb[i][m] * wb[i][m]) / np.sum(hb[i][m])
+            d = np.min(np.abs(_MIDS - mean) / np.maximum(np.abs(_MIDS), 1e-30))
+            if d <= 1e-6:
+                st["near_e4m3"] += 1
+            else:
+                fails.append(f"block {i}: codebook entry {k} {glut[i][k]:#x} vs {o['lut'][i][k]:#x} (mean {mean})")
+        ok_el = lut_ok[qb[i]]
+        if not np.array_equal(gr[i][ok_el], orr[i][ok_el]):
+            fails.append(f"block {i}: r differs")
+        oe = float(o["err"][i])
+        if abs(ge[i] - oe) > 1e-5 * oe + floor[i] + 1e-37:
+            fails.append(f"block {i}: err {ge[i]} vs {oe}")
+    record(name, st)
+    assert not fails, "\n".join(fails[:20])
+    assert st["near_tie"] + st["near_e4m3"] <= max(2, 0.001 * st["groups"]), st
+
+
+GRID = [(rows, cols, wb, ema, K) for (rows, cols), wb, ema, K in itertools.product(
+    [(8, 64), (16, 192), (40, 128)], [True, False], ["none", "bf16", "f32"], [1, 8, 15])
+    if (rows + cols + int(wb) + K + ["none", "bf16", "f32"].index(ema)) % 2 == 0 or K == 15]
+
+
+@pytest.mark.parametrize("rows,cols,wb,ema,K", GRID)
+def test_rubin_grid(rows, cols, wb, ema, K):
+    W, v, g = synth.gen_matrix(rows, cols, 800 + K + rows, w_bf16=wb, ema=ema != "none", device="cuda")
+    if g is not None and ema == "f32":
+        g = g.float()
+    clips = tuple(synth.clip_grid(1.0, 0.3, K)) if K > 1 else (1.0,)
+    run_rubin(f"rubin.{rows}x{cols}.{'bf16' if wb else 'f32'}.ema-{ema}.K{K}", W, v, g, clips=clips)
+
+
+@pytest.mark.parametrize("weighting", ["h2", "none"])
+def test_rubin_weightings(weighting):
+    W, v, g = synth.gen_matrix(32, 256, 851, w_bf16=True, ema=True, device="cuda")
+    run_rubin(f"rubin.weighting-{weighting}", W, v, g, clips=tuple(synth.clip_grid(1.0, 0.3, 15)),
+              weighting=weighting)
+
+
+def test_rubin_degenerate_blocks():
+    torch.manual_seed(3)
+    W = (torch.randn(16, 256) * 0.02).float()
+    v = torch.rand(16, 256).float()
+    W[0:8, 0:64] = 0.125                    # constant block
+    v[8:16, 64:128] = 0.0                   # no saliency in a block
+    v[0:8, 128:192] = 0.0
+    v[3, 130] = 2.0                         # all saliency on one weight
+    W[8:16, 192:256] = torch.tensor([-0.5, 0.5]).repeat(8, 32)   # two values
+    run_rubin("rubin.degenerate", W.cuda(), v.cuda(), clips=(1.0, 0.8, 0.6, 0.4))
+    run_rubin("rubin.degenerate.bf16", W.to(torch.bfloat16).cuda(), v.cuda(), clips=(1.0, 0.7))
+
+
+def test_rubin_llama_gate_sampled():
+    """A full Llama-3.1-8B gate projection in the benchmark's configuration
+    (bf16 W, fused EMA, the paper's 15-factor grid); every 23rd block row is
+    checked against the oracle."""
+    W, v, g = synth.gen_matrix(14336, 4096, 4, w_bf16=True, ema=True, device="cuda")
+    clips = tuple(np.float32(x) for x in np.round(np.arange(1.0, 0.29, -0.05), 2))
+    run_rubin("rubin.llama-gate", W, v, g, clips=clips, row_step_blocks=23)
+    del W, v, g
+    torch.cuda.empty_cache()
