@@ -94,6 +94,7 @@ def absmax(W: np.ndarray) -> float:
 
 
 WEIGHTINGS = {"h": 0, "h2": 1, "none": 2}
+FORMATS = {"int": 0, "nvfp4": 1, "int_sym": 2}
 PARAM_DTYPES = {"fp32": 0, "fp16": 1, "bf16": 2}
 
 
@@ -105,6 +106,9 @@ def reconstruct(W, v, *, fmt="int", bits=4, group=128, clips=(1.0,), g=None, bet
     ``weighting``: "h" (the saliency), "h2" (its square, fp32) or "none" (h = 1).
     ``param_dtype``: precision the INT dequantiser (s, z) is deployed in and r
     is formed from: "fp32", "fp16" or "bf16".
+    ``fmt``: "int" (asymmetric, codes 0..2^b-1, scale and zero), "int_sym"
+    (symmetric, codes -(2^(b-1)-1)..2^(b-1)-1 stored in two's complement,
+    scale only; ``zero`` is 0) or "nvfp4".
 
     Returns a dict with: ``codes`` (unpacked, one per element), ``codes_packed``,
     ``r`` (W's dtype), ``best`` (u8 per group), ``err`` (fp32 per group), ``v_out``
@@ -130,7 +134,7 @@ def reconstruct(W, v, *, fmt="int", bits=4, group=128, clips=(1.0,), g=None, bet
         g = np.ascontiguousarray(g)
         if g.shape != W.shape:
             raise ValueError("g shape")
-    d = _Desc(R, Cc, int(W.dtype == np.uint16), int(nv), nb, G,
+    d = _Desc(R, Cc, int(W.dtype == np.uint16), FORMATS[fmt], nb, G,
               clips_a.ctypes.data_as(C.POINTER(C.c_float)), K,
               int(g is not None and g.dtype == np.uint16), float(beta2), int(bool(fp32_mode)),
               WEIGHTINGS[weighting], PARAM_DTYPES[param_dtype])
@@ -208,8 +212,8 @@ def adamw_reconstruct(W, m, v, g, *, lr, beta1=0.9, beta2=0.999, eps=1e-8, weigh
     clips_a = np.ascontiguousarray(np.asarray(clips, dtype=np.float32))
     K = clips_a.size
     ngroups = R * Cc // G
-    d = _Desc(R, Cc, int(W.dtype == np.uint16), int(nv), nb, G, clips_a.ctypes.data_as(C.POINTER(C.c_float)), K,
-              int(g.dtype == np.uint16), float(beta2), 0, WEIGHTINGS[weighting], PARAM_DTYPES[param_dtype])
+    d = _Desc(R, Cc, int(W.dtype == np.uint16), FORMATS[fmt], nb, G, clips_a.ctypes.data_as(C.POINTER(C.c_float)),
+              K, int(g.dtype == np.uint16), float(beta2), 0, WEIGHTINGS[weighting], PARAM_DTYPES[param_dtype])
     o = _AdamW(lr, beta1, beta2, eps, weight_decay, step)
     out = {"codes": np.zeros(R * Cc, np.uint8), "codes_packed": np.zeros(ngroups * G * nb // 8, np.uint8),
            "r": np.zeros((R, Cc), W.dtype), "best": np.zeros(ngroups, np.uint8),

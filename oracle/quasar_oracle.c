@@ -20,6 +20,9 @@
  *     E4M3 block scale is fitted to minimise the same objective, argmin kept.
  *   - variants: saliency weighting h, h^2 (App. A.3) or 1 (Table 5), and the
  *     INT dequantiser deployed in fp16/bf16 (rounded before r and the score).
+ *   - symmetric INT-b groups: signed codes on [-f m, f m] (m = group absmax),
+ *     the scale-only weighted fit (the symmetric closed form Sec. 4.1.2
+ *     mentions beside Eq. ridgefit), same objective and selection.
  *   - Rubin INT3 LUT (App. B, Eq. rubin-fit): 8x64 blocks, for each clip the
  *     INT3 codes of the range, an 8-entry E4M3 codebook of saliency-weighted
  *     code means, the candidate with the lowest score kept.
@@ -393,6 +396,78 @@ static void int_group(const float* w, const float* h, int n, int bits, const flo
 }
 
 /* ------------------------------------------------------------------------ */
+/* Symmetric INT-b group: r = s q, q in [-Q, Q], Q = 2^(b-1) - 1              */
+/* ------------------------------------------------------------------------ */
+
+/* Codes of clip f: q = clamp(rint(w / (f m / Q)), -Q, Q), realised in fp32 as
+ * (w * (1/m)) * (Q/f); the scale minimising Eq. fisher-obj for fixed codes is
+ * s* = sum h q w / sum h q^2 (fp64; the RTN scale f m / Q when sum h q^2 = 0),
+ * rounded to fp32 and then to the deployed precision; the score is that of the
+ * emitted s.  An all-zero group has codes 0 and s = 0. */
+static void sym_group(const float* w, const float* h, int n, int bits, const float* clips, int K,
+                      int param_dtype, uint8_t* codes, float* s_out, float* r32, int* best_out, double* err_out,
+                      double* scores) {
+  const int Q = (1 << (bits - 1)) - 1;
+  const float Qf = (float)Q;
+  float m = 0.0f;
+  for (int i = 0; i < n; i++) {
+    const float a = fabsf(w[i]);
+    if (a > m) m = a;
+  }
+  if (m == 0.0f) {
+    for (int i = 0; i < n; i++) {
+      codes[i] = 0;
+      r32[i] = 0.0f;
+    }
+    *s_out = 0.0f;
+    *best_out = 0;
+    *err_out = 0.0;
+    if (scores)
+      for (int k = 0; k < K; k++) scores[k] = 0.0;
+    return;
+  }
+  const float rm = 1.0f / m;
+  float u[QOR_MAX_GROUP], q[QOR_MAX_GROUP], qbest[QOR_MAX_GROUP];
+  for (int i = 0; i < n; i++) u[i] = w[i] * rm;
+  int best = 0;
+  double sbest = 0.0;
+  float abest = 0.0f;
+  for (int k = 0; k < K; k++) {
+    const float cq = Qf / clips[k];
+    double sqq = 0.0, sqw = 0.0;
+    for (int i = 0; i < n; i++) {
+      float x = rintf(u[i] * cq);
+      if (x < -Qf) x = -Qf;
+      if (x > Qf) x = Qf;
+      q[i] = x + 0.0f;
+      sqq += (double)h[i] * (double)q[i] * (double)q[i];
+      sqw += (double)h[i] * (double)q[i] * (double)w[i];
+    }
+    const double sstar = sqq == 0.0 ? (double)((clips[k] * m) / Qf) : sqw / sqq;
+    const float a = round_param((float)sstar, param_dtype);
+    double sc = 0.0;
+    for (int i = 0; i < n; i++) {
+      const double d = (double)a * (double)q[i] - (double)w[i];
+      sc += (double)h[i] * d * d;
+    }
+    if (scores) scores[k] = sc;
+    if (k == 0 || sc < sbest) {
+      best = k;
+      sbest = sc;
+      abest = a;
+      memcpy(qbest, q, sizeof(float) * (size_t)n);
+    }
+  }
+  for (int i = 0; i < n; i++) {
+    codes[i] = (uint8_t)((int)qbest[i] & ((1 << bits) - 1)); /* two's complement in b bits */
+    r32[i] = abest * qbest[i];
+  }
+  *s_out = abest;
+  *best_out = best;
+  *err_out = sbest;
+}
+
+/* ------------------------------------------------------------------------ */
 /* NVFP4 block (Sec. 4.2)                                                    */
 /* ------------------------------------------------------------------------ */
 
@@ -555,13 +630,14 @@ int qor_reconstruct(const qor_desc* d, int64_t row0, int64_t row1, const void* W
                     const void* g, float tensor_amax, float* v_out, uint8_t* codes_packed,
                     uint8_t* codes_unpacked, float* scale, float* zero, uint8_t* e4m3, void* r,
                     uint8_t* best_clip, float* err, double* scores, double* diag) {
-  const int G = d->nvfp4 ? 16 : d->group;
+  const int G = d->nvfp4 == 1 ? 16 : d->group;
+  if (d->nvfp4 < 0 || d->nvfp4 > 2) return -4;
   if (G <= 0 || G > QOR_MAX_GROUP || d->cols % G != 0) return -2;
   if (d->n_clips < 1 || d->n_clips > QOR_MAX_CLIPS) return -1;
-  if (!d->nvfp4 && (d->bits < 2 || d->bits > 4)) return -4;
+  if (d->nvfp4 != 1 && (d->bits < 2 || d->bits > 4)) return -4;
   if (d->weighting < 0 || d->weighting > 2) return -1;
-  if (d->param_dtype < 0 || d->param_dtype > 2 || (d->nvfp4 && d->param_dtype != 0)) return -4;
-  const int bits = d->nvfp4 ? 4 : d->bits;
+  if (d->param_dtype < 0 || d->param_dtype > 2 || (d->nvfp4 == 1 && d->param_dtype != 0)) return -4;
+  const int bits = d->nvfp4 == 1 ? 4 : d->bits;
   const int64_t gpr = d->cols / G; /* groups per row */
   const int K = d->n_clips;
   const float st = tensor_amax / 2688.0f; /* 6 * 448: E2M1 max times E4M3 max */
@@ -588,7 +664,12 @@ int qor_reconstruct(const qor_desc* d, int64_t row0, int64_t row1, const void* W
       double e = 0.0;
       double* sc = scores ? scores + gid * K : NULL;
       double* dg = diag ? diag + gid * 4 : NULL;
-      if (d->nvfp4) {
+      if (d->nvfp4 == 2) {
+        float a = 0.f;
+        sym_group(w, h, G, bits, d->clips, K, d->param_dtype, codes, &a, r32, &best, &e, sc);
+        if (scale) scale[gid] = a;
+        if (zero) zero[gid] = 0.0f;
+      } else if (d->nvfp4) {
         uint8_t eb = 0;
         nvfp4_block(w, h, G, st, d->clips, K, d->fp32_mode, codes, &eb, r32, &best, &e, sc, dg);
         if (e4m3) e4m3[gid] = eb;

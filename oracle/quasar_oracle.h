@@ -20,7 +20,8 @@ extern "C" {
 typedef struct {
   int64_t rows, cols;  /* W is [rows, cols] row-major; groups run along a row */
   int w_bf16;          /* 1: W and r hold bf16 bit patterns; 0: fp32 */
-  int nvfp4;           /* 0: asymmetric INT-b groups; 1: NVFP4 16-blocks */
+  int nvfp4;           /* format: 0 asymmetric INT-b groups; 1 NVFP4 16-blocks;
+                          2 symmetric INT-b groups (codes in two's complement) */
   int bits;            /* INT: 2, 3 or 4 */
   int group;           /* INT: group size (divides cols); ignored for NVFP4 */
   const float* clips;  /* n_clips clip factors in (0, 1]; order = tie-break */

@@ -774,3 +774,92 @@ def test_rubin_layout_and_constant_block():
     assert np.all(o["lut"][1] == c) and np.all(qb[1] == 0) and o["best"][1] == 0
     e = float(np.sum(_blocks(vh, 8, 128)[1].astype(np.float64) * (_e4m3_value(c) - float(np.float32(0.3))) ** 2))
     np.testing.assert_allclose(o["err"][1], e, rtol=1e-6)
+
+
+# ---- symmetric INT-b (the scale-only closed form beside Eq. ridgefit) ---------
+
+
+def _sym_decode(codes, bits):
+    c = codes.astype(np.int64)
+    return np.where(c >= (1 << (bits - 1)), c - (1 << bits), c)
+
+
+@pytest.mark.parametrize("bits,group", [(4, 128), (3, 128), (2, 64)])
+def test_sym_against_exact_recompute(bits, group):
+    """Codes q = clamp(round(w / (f m / Q)), -Q, Q) with exact rationals, the
+    scale-only fit s* = sum h q w / sum h q^2 exactly, fp64 scores: the
+    oracle's scores, choice, scale and codes (boundary cases excused)."""
+    Q = (1 << (bits - 1)) - 1
+    clips = tuple(synth.clip_grid(1.0, 0.5, 6))
+    Wh, vh, _ = small_matrix(8, 512, 80 + bits)
+    o = oracle.reconstruct(Wh, vh, fmt="int_sym", bits=bits, group=group, clips=clips, want_scores=True)
+    w, h = Wh.reshape(-1, group), vh.reshape(-1, group)
+    checked = 0
+    for gi in range(w.shape[0]):
+        m = Fraction(float(np.max(np.abs(w[gi]))))
+        sc, near, fits = [], False, []
+        for f in clips:
+            s_rtn = Fraction(float(f)) * m / Q
+            q = []
+            for x in w[gi]:
+                t = Fraction(float(x)) / s_rtn
+                if abs(abs(t - math.floor(t)) - Fraction(1, 2)) < Fraction(2, 10 ** 5) and abs(t) < Q + 1:
+                    near = True
+                q.append(min(max(X.round_half_even(t), -Q), Q))
+            if near:
+                break
+            q = np.array(q)
+            hq = [Fraction(float(a)) * int(b) for a, b in zip(h[gi], q)]
+            sqq = sum(a * int(b) for a, b in zip(hq, q))
+            sqw = sum(a * Fraction(float(x)) for a, x in zip(hq, w[gi]))
+            s = float(sqw / sqq) if sqq != 0 else float(s_rtn)
+            s = float(np.float32(s))
+            sc.append(X.score(q, w[gi], h[gi], s, 0.0))
+            fits.append((q, s))
+        if near:
+            continue
+        checked += 1
+        np.testing.assert_allclose(o["scores"][gi], sc, rtol=1e-6)
+        kb, kk = int(o["best"][gi]), int(np.argmin(sc))
+        assert kk == kb or abs(sc[kk] - sc[kb]) <= 1e-6 * sc[kk]
+        q, s = fits[kb]
+        assert np.array_equal(_sym_decode(o["codes"].reshape(-1, group)[gi], bits), q)
+        np.testing.assert_allclose(o["scale"][gi], s, rtol=1e-6)
+        assert o["zero"][gi] == 0.0
+    assert checked >= 0.8 * w.shape[0]
+
+
+def test_sym_uniform_saliency_is_least_squares_through_zero():
+    """h = 1, F = {1}: the scale is numpy's least-squares fit of w = s q
+    (no intercept); r = s q exactly."""
+    Wh, _, _ = small_matrix(4, 256, 86)
+    o = oracle.reconstruct(Wh, np.ones_like(Wh), fmt="int_sym", bits=3, group=128, clips=(1.0,))
+    for gi in range(Wh.size // 128):
+        q = _sym_decode(o["codes"].reshape(-1, 128)[gi], 3).astype(np.float64)
+        wv = Wh.reshape(-1, 128)[gi].astype(np.float64)
+        s = np.linalg.lstsq(q[:, None], wv, rcond=None)[0][0]
+        np.testing.assert_allclose(o["scale"][gi], s, rtol=2e-7)
+        np.testing.assert_array_equal(o["r"].reshape(-1, 128)[gi], (np.float64(o["scale"][gi]) * q).astype(np.float32))
+
+
+def test_sym_sign_symmetry_and_never_worse_than_rtn():
+    """Negating W negates every code and keeps scales and scores; the chosen
+    candidate is never worse than symmetric RTN at f = 1 (s = m / Q)."""
+    Wh, vh, _ = small_matrix(6, 256, 87)
+    clips = tuple(synth.clip_grid(1.0, 0.55, 7))
+    a = oracle.reconstruct(Wh, vh, fmt="int_sym", bits=4, group=64, clips=clips, want_scores=True)
+    b = oracle.reconstruct(-Wh, vh, fmt="int_sym", bits=4, group=64, clips=clips, want_scores=True)
+    np.testing.assert_array_equal(_sym_decode(a["codes"], 4), -_sym_decode(b["codes"], 4))
+    np.testing.assert_array_equal(a["scale"], b["scale"])
+    np.testing.assert_array_equal(a["scores"], b["scores"])
+    w, h = Wh.reshape(-1, 64).astype(np.float64), vh.reshape(-1, 64).astype(np.float64)
+    for gi in range(w.shape[0]):
+        m = np.max(np.abs(w[gi]))
+        q = np.clip(np.round(w[gi] / (m / 7)), -7, 7)
+        s_rtn = float(np.sum(h[gi] * (m / 7 * q - w[gi]) ** 2))
+        assert a["scores"][gi, int(a["best"][gi])] <= a["scores"][gi, 0] <= s_rtn * (1 + 1e-6)
+
+
+def test_sym_zero_group():
+    o = run_group(np.zeros(64, np.float32), np.ones(64, np.float32), fmt="int_sym", bits=2, clips=(1.0, 0.5))
+    assert o["scale"][0] == 0.0 and np.all(o["codes"] == 0) and np.all(o["r"] == 0) and o["err"][0] == 0.0
