@@ -11,7 +11,8 @@ Workloads (paper_2608_13966_amd/synth.py): c1 single fp32 1024x1024 INT4;
 c2 Qwen3-0.6B-shaped layer set INT3; c3 Llama-3.1-8B-shaped layer set INT2
 g64, 12 clips, fused EMA (default); c4 the same set in NVFP4; c5 32 such
 layers INT4 with fused EMA (one simulated training step); c8 the Llama set
-in the Rubin INT3 LUT format with the paper's 15 clip factors; c6 / c7 the
+in the Rubin INT3 LUT format with the paper's 15 clip factors; c9 the Llama
+set in symmetric INT4 g128; c6 / c7 the
 Llama-3.1-8B set with fp32 master weights, one fused AdamW step followed by
 the INT2 / NVFP4 reconstruction (a step then includes the optimiser update).
 """
@@ -62,6 +63,9 @@ def algorithmic_valu_ops_per_weight(wl) -> float:
     if wl.fmt == "rubin":
         # per clip: the code (3), the index address (2), two bin sums (2)
         return 7.0 * K + 12.0 + pre
+    if wl.fmt == "int_sym":
+        # per clip: the code (3), one product and two accumulations (3)
+        return 6.0 * K + 9.0 + pre
     return 7.0 * K + 9.0 + pre
 
 
@@ -97,7 +101,7 @@ def main(argv=None):
     ap.add_argument("--gpus", type=int, default=int(os.environ.get("WORLD_SIZE", "1")))
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5", "c6", "c7", "c8"])
+    ap.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5", "c6", "c7", "c8", "c9"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="CPU time (thread-seconds) the oracle baseline aims to spend; the row stride of "
@@ -376,7 +380,8 @@ def main(argv=None):
         "vs_baseline": None, "dtype": "f64", "data": "synthetic",
         "config": {"workload": f"{args.workload}: {wl.description}", "matrices": per_step,
                    "weights_per_step": n_per_step,
-                   "format": {"nvfp4": "nvfp4", "rubin": "rubin-int3-lut"}.get(wl.fmt, f"int{wl.bits}"),
+                   "format": {"nvfp4": "nvfp4", "rubin": "rubin-int3-lut",
+                              "int_sym": f"int{wl.bits}-symmetric"}.get(wl.fmt, f"int{wl.bits}"),
                    "group": wl.group, "clips": len(wl.clips), "fused_ema": wl.ema,
                    "io": (("fp32 W (updated), bf16 r, fp32 m and v, bf16 g" if wl.adamw else
                            ("bf16" if wl.w_bf16 else "fp32") + " W and r, fp32 v" + (", bf16 g" if wl.ema else ""))),

@@ -20,7 +20,7 @@ bool is_rubin(const quasar_desc* d) { return d->format == QUASAR_RUBIN_INT3; }
 int check_desc(const quasar_desc* d) {
   if (d == nullptr) return QUASAR_ERR_ARG;
   if (d->w_dtype != QUASAR_F32 && d->w_dtype != QUASAR_BF16) return QUASAR_ERR_FORMAT;
-  if (d->format == QUASAR_INT) {
+  if (d->format == QUASAR_INT || d->format == QUASAR_INT_SYM) {
     if (d->bits < 2 || d->bits > 4) return QUASAR_ERR_FORMAT;
     if (d->group != 64 && d->group != 128) return QUASAR_ERR_FORMAT;
   } else if (d->format == QUASAR_NVFP4) {
@@ -42,7 +42,8 @@ int check_desc(const quasar_desc* d) {
   if (d->weighting < QUASAR_WEIGHT_H || d->weighting > QUASAR_WEIGHT_NONE) return QUASAR_ERR_ARG;
   if (d->param_dtype != QUASAR_F32 && d->param_dtype != QUASAR_F16 && d->param_dtype != QUASAR_BF16)
     return QUASAR_ERR_FORMAT;
-  if (d->format != QUASAR_INT && d->param_dtype != QUASAR_F32) return QUASAR_ERR_FORMAT;
+  if (d->format != QUASAR_INT && d->format != QUASAR_INT_SYM && d->param_dtype != QUASAR_F32)
+    return QUASAR_ERR_FORMAT;
   if (d->clip_ratios == nullptr) return QUASAR_ERR_ARG;
   for (int k = 0; k < d->n_clips; k++) {
     const float f = d->clip_ratios[k];
@@ -101,7 +102,7 @@ int quasar_check(const quasar_desc* d, const void* W, const float* v, const void
   if (W == nullptr || v == nullptr || codes == nullptr || scales == nullptr) return QUASAR_ERR_ARG;
   if (d->format == QUASAR_INT && zeros == nullptr) return QUASAR_ERR_ARG;
   if (d->format == QUASAR_NVFP4 && tensor_scale == nullptr) return QUASAR_ERR_ARG;
-  if (is_rubin(d) && tensor_amax != nullptr) return QUASAR_ERR_ARG;
+  if (d->format != QUASAR_NVFP4 && tensor_amax != nullptr) return QUASAR_ERR_ARG;
   const void* ptrs[] = {W, v, g, codes, scales, zeros, r, best_clip, err, tensor_scale, tensor_amax, workspace};
   for (const void* p : ptrs)
     if (!aligned16(p)) return QUASAR_ERR_ALIGN;
@@ -137,7 +138,8 @@ int launch_path(const quasar_desc* d, const void* W, void* Wu, float* m, float* 
   const float beta2 = ema_mode >= 3 ? d->beta2 : (g ? d->beta2 : 0.0f);
   const float omb2 = 1.0f - beta2;
   hipError_t e;
-  if (d->format == QUASAR_INT) {
+  if (d->format == QUASAR_INT || d->format == QUASAR_INT_SYM) {
+    const bool sym = d->format == QUASAR_INT_SYM;
     quasar::IntParams p;
     memset(&p, 0, sizeof(p));
     p.W = W;
@@ -155,11 +157,13 @@ int launch_path(const quasar_desc* d, const void* W, void* Wu, float* m, float* 
     p.n_clips = K;
     p.weighting = d->weighting;
     p.param_dtype = d->param_dtype;
+    p.symmetric = sym;
     const float qmax = (float)((1 << d->bits) - 1);
+    const float qsym = (float)((1 << (d->bits - 1)) - 1);
     for (int k = 0; k < quasar::kMaxClips; k++) {
       const float f = d->clip_ratios[k < K ? k : K - 1];  // entries past K repeat the last clip
       p.clip[k] = f;
-      p.alpha[k] = qmax / (2.0f * f);
+      p.alpha[k] = sym ? qsym / f : qmax / (2.0f * f);
     }
     p.Wu = Wu;
     p.m = m;
@@ -259,7 +263,8 @@ int quasar_adamw_check(const quasar_desc* d, const quasar_adamw* opt, const void
   // the reconstruction's own checks (pointers, alignment, the decay range,
   // here the optimiser's); the fused step always has its tensor amax, so no
   // workspace is needed
-  if (d->format == QUASAR_RUBIN_INT3) return QUASAR_ERR_FORMAT;  // not fused with the optimiser step
+  if (d->format == QUASAR_RUBIN_INT3 || d->format == QUASAR_INT_SYM)
+    return QUASAR_ERR_FORMAT;  // not fused with the optimiser step
   if (d->format == QUASAR_NVFP4 && tensor_amax == nullptr) return QUASAR_ERR_ARG;
   quasar_desc dd = *d;
   dd.beta2 = opt->beta2;

@@ -30,14 +30,19 @@ namespace {
 
 constexpr int N = 16;  // weights per lane
 
-template <bool W_BF16, int EMA, int BITS, int G, int KC, bool MULTI>
+// SYM: symmetric groups (r = s q, q in [-Q, Q], Q = 2^(BITS-1) - 1, range
+// [-f m, f m] with m = max |w|, scale-only fit); otherwise asymmetric groups
+// (r = s q + z, q in [0, 2^BITS - 1], range [c - f rho, c + f rho]).
+template <bool W_BF16, int EMA, int BITS, int G, int KC, bool MULTI, bool SYM>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu((KC > 8 || MULTI) ? 3 : 4)))
 void int_reconstruct_kernel(IntParams p) {
   constexpr int L = G / N;          // lanes per group
   constexpr int GPW = 64 / L;       // groups per wavefront
-  constexpr int QMAX = (1 << BITS) - 1;
+  constexpr int QMAX = SYM ? (1 << (BITS - 1)) - 1 : (1 << BITS) - 1;
   constexpr int OWN = (KC + L - 1) / L;  // clips owned per lane per chunk
+  constexpr int NM = SYM ? 2 : 3;        // clip-dependent moments
   constexpr float kQmax = (float)QMAX;
+  constexpr float kQmin = SYM ? -(float)QMAX : 0.0f;
   constexpr float kBeta = 0.5f * (float)QMAX;
 
   __shared__ double s_red[kThreads / 64][64 * KC];
@@ -101,20 +106,38 @@ void int_reconstruct_kernel(IntParams p) {
   }
 
   // ---- group range (Alg. 1, first line) ------------------------------------
-  float mn = wr.get(0), mx = wr.get(0);
+  float mn, mx, c, rho, rrho, nc;
+  bool constant;
+  if constexpr (SYM) {  // m = max |w|
+    mx = 0.0f;
 #pragma unroll
-  for (int i = 1; i < N; i++) {
-    mn = fminf(mn, wr.get(i));
-    mx = fmaxf(mx, wr.get(i));
+    for (int i = 0; i < N; i++) mx = fmaxf(mx, fabsf(wr.get(i)));
+    mx = run_max<L>(mx);
+    mn = 0.0f;
+    constant = (mx == 0.0f);  // an all-zero group
+    c = 0.0f;
+    rho = mx;
+    rrho = 1.0f / mx;
+    nc = 0.0f;
+  } else {
+    mn = wr.get(0);
+    mx = wr.get(0);
+#pragma unroll
+    for (int i = 1; i < N; i++) {
+      mn = fminf(mn, wr.get(i));
+      mx = fmaxf(mx, wr.get(i));
+    }
+    mn = run_min<L>(mn);
+    mx = run_max<L>(mx);
+    constant = (mx == mn);
+    c = 0.5f * (mx + mn);
+    rho = 0.5f * (mx - mn);
+    rrho = 1.0f / rho;
+    nc = -(c * rrho);
   }
-  mn = run_min<L>(mn);
-  mx = run_max<L>(mx);
-  const bool constant = (mx == mn);
-  const float c = 0.5f * (mx + mn);
-  const float rho = 0.5f * (mx - mn);
-  const float rrho = 1.0f / rho;
-  const float nc = -(c * rrho);
-  // normalised position u = fmaf(w, 1/rho, -c/rho), recomputed where used
+  // normalised position, recomputed where used: u = fmaf(w, 1/rho, -c/rho)
+  // and x = fmaf(u, alpha_f, qmax/2) (symmetric: u = w * (1/m), x = u * alpha_f),
+  // then q = clamp(rint(x))
 
   // ---- clip-independent moments (fp64), accumulated in the first pass --------
   double Sv = 0.0, Svw = 0.0, Svww = 0.0;
@@ -144,7 +167,7 @@ void int_reconstruct_kernel(IntParams p) {
         // held across passes)
         asm volatile("" : "+v"(vi), "+v"(wi));
       }
-      const float ui = __builtin_fmaf(wi, rrho, nc);
+      const float ui = SYM ? wi * rrho : __builtin_fmaf(wi, rrho, nc);
       const double V = (double)vi, Wd = (double)wi;
       const double VW = V * Wd;
       if constexpr (FIRST) {
@@ -154,12 +177,12 @@ void int_reconstruct_kernel(IntParams p) {
       }
 #pragma unroll
       for (int kk = 0; kk < KC; kk++) {
-        float x = __builtin_fmaf(ui, al[kk], kBeta);
+        float x = SYM ? ui * al[kk] : __builtin_fmaf(ui, al[kk], kBeta);
         float q = __builtin_rintf(x);
-        q = __builtin_amdgcn_fmed3f(q, 0.0f, kQmax);
+        q = __builtin_amdgcn_fmed3f(q, kQmin, kQmax);
         const double Q = (double)q;
         const double VQ = V * Q;
-        acc[kk][0] += VQ;
+        if constexpr (!SYM) acc[kk][0] += VQ;
         acc[kk][1] = __builtin_fma(VQ, Q, acc[kk][1]);
         acc[kk][2] = __builtin_fma(VW, Q, acc[kk][2]);
       }
@@ -177,8 +200,12 @@ void int_reconstruct_kernel(IntParams p) {
 
     // ---- combine the L partials: lane j sums the clips kk = j + L t ---------
     double own[OWN][3];
+    if constexpr (SYM) {
 #pragma unroll
-    for (int m = 0; m < 3; m++) {
+      for (int t = 0; t < OWN; t++) own[t][0] = 0.0;
+    }
+#pragma unroll
+    for (int m = 3 - NM; m < 3; m++) {
 #pragma unroll
       for (int kk = 0; kk < KC; kk++) red[(slot * KC + kk) * L + j] = acc[kk][m];
       wave_lds_fence();
@@ -199,7 +226,22 @@ void int_reconstruct_kernel(IntParams p) {
     for (int t = 0; t < OWN; t++) {
       const int kk = j + L * t;
       const int k = k0 + kk;
-      if (kk < KC && k < K) {
+      if (SYM && kk < KC && k < K) {
+        // scale-only fit: s* = sum h q w / sum h q^2 (the RTN scale f m / Q
+        // when sum h q^2 = 0); the score of r = s q is Svww + s (s A1 - 2 A2)
+        const double A1 = own[t][1], A2 = own[t][2];
+        const double a = (A1 == 0.0) ? (double)((s_clip[k] * mx) / kQmax) : div_f64(A2, A1, rcp_f64(A1));
+        const float af = round_param((float)a, p.param_dtype);
+        const double ad = (double)af;
+        const double score = Svww + ad * (ad * A1 - 2.0 * A2);
+        const double key = make_key(score, k);
+        if (key < best_key) {
+          best_key = key;
+          best_a = af;
+          best_b = 0.0f;
+          best_err = (float)fmax(score, 0.0);
+        }
+      } else if (kk < KC && k < K) {
         const double A0 = own[t][0], A1 = own[t][1], A2 = own[t][2];
         const double D = Sv * A1 - A0 * A0;
         double a, b;
@@ -255,7 +297,7 @@ void int_reconstruct_kernel(IntParams p) {
   int kout = kstar;
   if (constant) {  // every code 0, z = w in the deployed precision (exact at fp32)
     a = 0.0f;
-    b = round_param(mn, p.param_dtype);
+    b = SYM ? 0.0f : round_param(mn, p.param_dtype);  // symmetric: an all-zero group
     const double d = (double)b - (double)mn;
     errv = (float)(Sv * d * d);
     kout = 0;
@@ -266,12 +308,21 @@ void int_reconstruct_kernel(IntParams p) {
   float r[N];
 #pragma unroll
   for (int i = 0; i < N; i++) {
-    const float ui = __builtin_fmaf(wr.get(i), rrho, nc);
-    float x = __builtin_fmaf(ui, alpha, kBeta);
-    float q = __builtin_amdgcn_fmed3f(__builtin_rintf(x), 0.0f, kQmax);
-    if (constant) q = 0.0f;
-    qi[i] = (uint32_t)q;
-    r[i] = __builtin_fmaf(a, q, b);
+    if constexpr (SYM) {
+      const float ui = wr.get(i) * rrho;
+      // + 0.0f turns a rounded -0 into +0, so a zero code gives r = s * (+0)
+      float q = __builtin_amdgcn_fmed3f(__builtin_rintf(ui * alpha), kQmin, kQmax) + 0.0f;
+      if (constant) q = 0.0f;
+      qi[i] = (uint32_t)(int)q & ((1u << BITS) - 1u);  // two's complement in BITS bits
+      r[i] = a * q;
+    } else {
+      const float ui = __builtin_fmaf(wr.get(i), rrho, nc);
+      float x = __builtin_fmaf(ui, alpha, kBeta);
+      float q = __builtin_amdgcn_fmed3f(__builtin_rintf(x), 0.0f, kQmax);
+      if (constant) q = 0.0f;
+      qi[i] = (uint32_t)q;
+      r[i] = __builtin_fmaf(a, q, b);
+    }
   }
   if (!active) return;
   if (p.r) {
@@ -304,7 +355,7 @@ void int_reconstruct_kernel(IntParams p) {
   }
   if (j == 0) {
     p.scales[gid] = a;
-    p.zeros[gid] = b;
+    if (p.zeros) p.zeros[gid] = b;
     if (p.best_clip) p.best_clip[gid] = (uint8_t)kout;
     if (p.err) p.err[gid] = errv;
   }
@@ -319,14 +370,27 @@ hipError_t launch_kc(const IntParams& p, hipStream_t s) {
   // repeat the last clip and are never selected); passes of 8 beyond that
   const int K = p.n_clips;
   const dim3 grid((unsigned)blocks), block(kThreads);
+  if (p.symmetric) {  // symmetric groups: passes of 8 or 12; not fused with the optimiser step
+    if constexpr (EMA <= 2) {
+      if (K <= 8)
+        hipLaunchKernelGGL((int_reconstruct_kernel<W_BF16, EMA, BITS, G, 8, false, true>), grid, block, 0, s, p);
+      else if (K <= 12)
+        hipLaunchKernelGGL((int_reconstruct_kernel<W_BF16, EMA, BITS, G, 12, false, true>), grid, block, 0, s, p);
+      else
+        hipLaunchKernelGGL((int_reconstruct_kernel<W_BF16, EMA, BITS, G, 8, true, true>), grid, block, 0, s, p);
+      return hipGetLastError();
+    } else {
+      return hipErrorInvalidValue;
+    }
+  }
   if (K <= 4)
-    hipLaunchKernelGGL((int_reconstruct_kernel<W_BF16, EMA, BITS, G, 4, false>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((int_reconstruct_kernel<W_BF16, EMA, BITS, G, 4, false, false>), grid, block, 0, s, p);
   else if (K <= 8)
-    hipLaunchKernelGGL((int_reconstruct_kernel<W_BF16, EMA, BITS, G, 8, false>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((int_reconstruct_kernel<W_BF16, EMA, BITS, G, 8, false, false>), grid, block, 0, s, p);
   else if (K <= 12)
-    hipLaunchKernelGGL((int_reconstruct_kernel<W_BF16, EMA, BITS, G, 12, false>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((int_reconstruct_kernel<W_BF16, EMA, BITS, G, 12, false, false>), grid, block, 0, s, p);
   else
-    hipLaunchKernelGGL((int_reconstruct_kernel<W_BF16, EMA, BITS, G, 8, true>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((int_reconstruct_kernel<W_BF16, EMA, BITS, G, 8, true, false>), grid, block, 0, s, p);
   return hipGetLastError();
 }
 

@@ -28,7 +28,8 @@ struct IntParams {
   int n_clips;
   int weighting;        // 0 h = v, 1 h = v*v, 2 h = 1
   int param_dtype;      // 0 fp32, 1 bf16, 2 fp16 (quasar_dtype values)
-  float alpha[kMaxClips];  // qmax / (2 f_k), fp32 division on the host
+  int symmetric;        // 1: symmetric groups (alpha = Q / f; zeros optional, written 0)
+  float alpha[kMaxClips];  // qmax / (2 f_k) (symmetric: Q / f_k), fp32 division on the host
   float clip[kMaxClips];   // f_k
   // fused AdamW step (ema modes 3 and 4): W is updated in place through Wu,
   // m and v are updated; r may be bf16 while W is fp32

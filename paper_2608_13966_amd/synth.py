@@ -53,7 +53,7 @@ class Workload:
     description: str
     shapes: tuple            # ((name, rows, cols), ...)
     seeds: tuple             # one seed per matrix
-    fmt: str                 # "int" | "nvfp4" | "rubin"
+    fmt: str                 # "int" | "int_sym" | "nvfp4" | "rubin"
     bits: int
     group: int
     clips: tuple
@@ -101,6 +101,9 @@ def workloads() -> dict:
         "c8": Workload("c8", "Llama-3.1-8B-shaped layer set, bf16 W, Rubin INT3 LUT (8x64 blocks, E4M3 "
                        "codebooks), the paper's 15 clip factors 0.30..1.00, fused EMA from a bf16 gradient",
                        l8, l8s, "rubin", 3, 512, tuple(PAPER_CLIPS), w_bf16=True, ema=True),
+        "c9": Workload("c9", "Llama-3.1-8B-shaped layer set, bf16 W, symmetric INT4 g128 (scale-only fit), "
+                       "8 clips 1.0..0.65, fused EMA from a bf16 gradient",
+                       l8, l8s, "int_sym", 4, 128, tuple(clip_grid(1.0, 0.65, 8)), w_bf16=True, ema=True),
         "c6": Workload("c6", "Llama-3.1-8B-shaped layer set, fp32 master W, one fused AdamW step (fp32 m, v, "
                        "bf16 g) + INT2 g64 reconstruction, 12 clips 1.0..0.5, bf16 r",
                        l8, l8s, "int", 2, 64, tuple(clip_grid(1.0, 0.5, 12)), w_bf16=False, ema=True,

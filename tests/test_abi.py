@@ -185,3 +185,15 @@ def test_rubin_descriptor_validation_and_sizes():
     assert _check(bad, zeros=None) == Q.ERR_FORMAT
     # not fused with the optimiser step
     assert _adam_check(_int_desc(fmt="rubin", rows=16, cols=128, w_dtype=Q.F32), zeros=None) == Q.ERR_FORMAT
+
+
+def test_symmetric_int_descriptor_validation():
+    d = _int_desc(fmt="int_sym", bits=4, group=128)
+    assert _check(d) == Q.OK and _check(d, zeros=None) == Q.OK
+    assert _check(_int_desc(fmt="int_sym", bits=2, group=64, param_dtype="bf16"), zeros=None) == Q.OK
+    assert _check(_int_desc(fmt="int_sym", bits=5)) == Q.ERR_FORMAT
+    assert _check(_int_desc(fmt="int_sym", group=32)) == Q.ERR_FORMAT
+    assert _check(d, tensor_amax=A) == Q.ERR_ARG
+    assert _check(_int_desc(), tensor_amax=A) == Q.ERR_ARG
+    assert Q.quasar_codes_bytes(_int_desc(fmt="int_sym", rows=2, cols=256, bits=3)) == 2 * 256 * 3 // 8
+    assert _adam_check(_int_desc(fmt="int_sym", w_dtype=Q.F32)) == Q.ERR_FORMAT

@@ -163,6 +163,43 @@ def test_variants_weighting_and_deployed_precision(fmt, bits, group, wt, pd):
              fmt=fmt, bits=bits, group=group, clips=clips, ema=True, weighting=wt, param_dtype=pd)
 
 
+SYM = [(bits, group, wb, ema, K, wt, pd) for (bits, group, wb, ema, K, wt, pd) in [
+    (4, 128, True, "bf16", 8, "h", "fp32"), (3, 128, True, "none", 12, "h", "fp32"),
+    (2, 64, False, "f32", 15, "h", "fp32"), (4, 64, False, "none", 5, "h2", "fp16"),
+    (3, 64, True, "bf16", 1, "none", "bf16"), (2, 128, True, "bf16", 9, "h", "fp16")]]
+
+
+@pytest.mark.parametrize("bits,group,wb,ema,K,wt,pd", SYM)
+def test_symmetric_int(bits, group, wb, ema, K, wt, pd):
+    """Symmetric INT-b groups (scale-only fit) on ragged shapes."""
+    clips = tuple(synth.clip_grid(1.0, 0.4, K)) if K > 1 else (1.0,)
+    run_case(f"sym.int{bits}g{group}.{'bf16' if wb else 'f32'}.ema-{ema}.K{K}.{wt}.{pd}", 37, 3 * group,
+             400 + bits + K, fmt="int_sym", bits=bits, group=group, clips=clips, w_bf16=wb, ema=ema != "none",
+             g_fp32=ema == "f32", weighting=wt, param_dtype=pd)
+
+
+def test_symmetric_int_llama_gate_sampled():
+    """INT4 g128 symmetric on a full Llama-3.1-8B gate projection with the
+    fused EMA; every 61st row checked."""
+    run_case("sym.llama-gate", 14336, 4096, 4, fmt="int_sym", bits=4, group=128,
+             clips=tuple(synth.clip_grid(1.0, 0.65, 8)), ema=True, row_step=61)
+    torch.cuda.empty_cache()
+
+
+def test_symmetric_int_degenerate():
+    torch.manual_seed(5)
+    W = (torch.randn(4, 256) * 0.02).float()
+    v = torch.rand(4, 256).float()
+    W[0, :128] = 0.0                  # all-zero group
+    W[1, :128] = 0.25                 # constant group: every code +Q at f = 1
+    v[2, 128:] = 0.0                  # no saliency
+    v[3, :128] = 0.0
+    v[3, 5] = 1.0                     # one weight carries all saliency
+    Wg, vg = _place(W, v)
+    run_case("sym.degenerate", 0, 0, 0, fmt="int_sym", bits=3, group=128, clips=(1.0, 0.75, 0.5), W=Wg,
+             v=vg.clone(), w_bf16=False)
+
+
 def test_paper_clip_grid_int3():
     """The paper's own grid: 15 factors 0.30, 0.35, ..., 1.00 (two passes)."""
     clips = tuple(np.float32(x) for x in np.round(np.arange(1.0, 0.29, -0.05), 2))
