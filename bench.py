@@ -111,6 +111,10 @@ def main(argv=None):
                     help="saliency weighting variant (h: the method's default)")
     ap.add_argument("--param-dtype", default="fp32", choices=["fp32", "fp16", "bf16"],
                     help="deployed precision of the INT dequantiser (s, z)")
+    ap.add_argument("--launch", default="batch", choices=["single", "batch"],
+                    help="one kernel launch per matrix, or one quasar_reconstruct_batch launch per run of up "
+                         "to 16 consecutive matrices (reconstruction workloads; the fused optimiser step "
+                         "always launches per matrix)")
     args = ap.parse_args(argv)
 
     if args.gpus != 1:
@@ -202,6 +206,29 @@ def main(argv=None):
         if s != Q.OK:
             raise Q.QuasarError(s)
 
+    # ---- launch plan: per matrix, or batched runs of up to MAX_BATCH matrices ----
+    batched = args.launch == "batch" and not wl.adamw
+    plans = []
+    for ci in range(copies):
+        ms = mats[ci * per_step:(ci + 1) * per_step]
+        grps = [ms[i:i + Q.MAX_BATCH] for i in range(0, len(ms), Q.MAX_BATCH)] if batched else [[m] for m in ms]
+        plan = []
+        for grp in grps:
+            arr = None
+            if len(grp) > 1:
+                arr = (Q.Matrix * len(grp))(*[Q.matrix(m["W"], m["v"], m["g"], m["out"], m["out"]["amax"])
+                                              for m in grp])
+            plan.append((grp, arr, sum(m["W"].numel() for m in grp)))
+        plans.append(plan)
+
+    def launch_group(grp, arr):
+        if arr is None:
+            launch(grp[0])
+            return
+        s = Q.lib().quasar_reconstruct_batch(grp[0]["d"].ref, arr, len(grp), stream.cuda_stream)
+        if s != Q.OK:
+            raise Q.QuasarError(s, "quasar_reconstruct_batch")
+
     # ---- warmup ----------------------------------------------------------------
     nv = wl.fmt == "nvfp4" and not wl.adamw   # the plain NVFP4 path runs its absmax pass every step
     if wl.adamw and wl.fmt == "nvfp4":
@@ -209,10 +236,11 @@ def main(argv=None):
             launch_absmax(m)                        # the first step's tensor amax
     for i in range(args.warmup):
         step_no[0] = i
-        for m in mats[(i % copies) * per_step:(i % copies + 1) * per_step]:
+        for grp, arr, _ in plans[i % copies]:
             if nv:
-                launch_absmax(m)
-            launch(m)
+                for m in grp:
+                    launch_absmax(m)
+            launch_group(grp, arr)
     torch.cuda.synchronize()
 
     # ---- timed steps: whole-step events plus one event pair per launch ---------
@@ -223,16 +251,17 @@ def main(argv=None):
     ev_start.record(stream)
     for i in range(args.steps):
         step_no[0] = args.warmup + i
-        for m in mats[(i % copies) * per_step:(i % copies + 1) * per_step]:
-            if nv:  # NVFP4: the tensor absmax pass, timed on its own
+        for grp, arr, nw in plans[i % copies]:
+            if nv:  # NVFP4: the tensor absmax passes, timed on their own
                 a0 = torch.cuda.Event(enable_timing=True)
                 a0.record(stream)
-                launch_absmax(m)
+                for m in grp:
+                    launch_absmax(m)
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
-            launch(m)
+            launch_group(grp, arr)
             b.record(stream)
-            per_launch.append((a, b, m["W"].numel()))
+            per_launch.append((a, b, nw))
             if nv:
                 per_absmax.append((a0, a))
     ev_end.record(stream)
@@ -246,8 +275,9 @@ def main(argv=None):
     # per-step kernel time (sum of that step's launches) -> spread over steps
     amax_ms = [a.elapsed_time(b) for a, b in per_absmax]
     step_k = []
+    per_step_launches = len(plans[0])
     for i in range(args.steps):
-        sl = slice(i * per_step, (i + 1) * per_step)
+        sl = slice(i * per_step_launches, (i + 1) * per_step_launches)
         step_k.append(sum(launch_ms[sl]) + (sum(amax_ms[sl]) if amax_ms else 0.0))
     step_pct = [round(float(x), 4) for x in np.percentile(step_k, [10, 50, 90])]
 
@@ -387,7 +417,9 @@ def main(argv=None):
                            ("bf16" if wl.w_bf16 else "fp32") + " W and r, fp32 v" + (", bf16 g" if wl.ema else ""))),
                    "arithmetic": "fp32 codes, fp64 moments/fit/score",
                    "weighting": args.weighting, "param_dtype": args.param_dtype,
-                   "cache_rotation_copies": copies},
+                   "cache_rotation_copies": copies,
+                   "launch": "batched (up to 16 matrices per launch)" if batched else "one launch per matrix",
+                   "launches_per_step": per_step_launches},
         "hbm_GBps": round(gbps, 1), "hbm_pct_peak": round(100 * gbps / PEAK_HBM_GBPS, 2),
         "algorithmic_bytes_per_weight": bpw,
         "copy_GBps": None if copy_gbps is None else round(copy_gbps, 1),

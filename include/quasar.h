@@ -216,6 +216,41 @@ int quasar_adamw_check(const quasar_desc* desc, const quasar_adamw* opt, const v
                        const float* err, const float* tensor_scale, const float* tensor_amax,
                        const float* amax_out);
 
+/*
+ * Several matrices in one launch (e.g. the seven projections of a
+ * transformer layer): the same computation as one quasar_reconstruct per
+ * matrix, with identical results, but a single grid, so small matrices do not
+ * each pay a launch and the tail of one overlaps the others.
+ *
+ * desc gives everything the matrices share (format, bits, group, clips,
+ * dtypes, beta2, weighting, param_dtype); its rows/cols are ignored.  Each
+ * quasar_matrix gives a matrix's shape and buffers, with the meaning and
+ * requirements of the same-named quasar_reconstruct arguments.  Either every
+ * g is NULL or none is.  NVFP4 needs every tensor_amax (no workspace path).
+ * 1 <= n_mats <= QUASAR_MAX_BATCH.  Returns a quasar_status; on error nothing
+ * is launched.
+ */
+#define QUASAR_MAX_BATCH 16
+typedef struct {
+  int64_t rows, cols;
+  const void* W;
+  float* v;
+  const void* g;
+  uint8_t* codes;
+  void* scales;
+  float* zeros;
+  void* r;
+  uint8_t* best_clip;
+  float* err;
+  float* tensor_scale;
+  const float* tensor_amax;
+} quasar_matrix;
+
+int quasar_reconstruct_batch(const quasar_desc* desc, const quasar_matrix* mats, int n_mats, void* stream);
+
+/* Host-only validation: the status quasar_reconstruct_batch would return. */
+int quasar_batch_check(const quasar_desc* desc, const quasar_matrix* mats, int n_mats);
+
 /* Host-only validation: the status quasar_reconstruct would return for these
  * arguments, without launching anything or touching device memory. */
 int quasar_check(const quasar_desc* desc, const void* W, const float* v, const void* g,

@@ -132,7 +132,7 @@ namespace {
 int launch_path(const quasar_desc* d, const void* W, void* Wu, float* m, float* v, const void* g, int ema_mode,
                 const quasar::AdamWConsts* adam, uint8_t* codes, void* scales, float* zeros, void* r, int r_bf16,
                 uint8_t* best_clip, float* err, float* tensor_scale, const float* tensor_amax, float* amax_out,
-                void* workspace, hipStream_t st) {
+                void* workspace, hipStream_t st, const quasar::BatchTable* batch = nullptr) {
   const bool w_bf16 = d->w_dtype == QUASAR_BF16;
   const int K = d->n_clips;
   const float beta2 = ema_mode >= 3 ? d->beta2 : (g ? d->beta2 : 0.0f);
@@ -169,6 +169,7 @@ int launch_path(const quasar_desc* d, const void* W, void* Wu, float* m, float* 
     p.m = m;
     if (adam) p.adam = *adam;
     p.r_bf16 = r_bf16;
+    if (batch) p.batch = *batch;
     e = quasar::launch_int(p, d->bits, d->group, w_bf16, ema_mode, st);
   } else if (is_rubin(d)) {
     quasar::RubinParams p;
@@ -193,6 +194,7 @@ int launch_path(const quasar_desc* d, const void* W, void* Wu, float* m, float* 
       p.clip[k] = f;
       p.alpha[k] = 7.0f / (2.0f * f);
     }
+    if (batch) p.batch = *batch;
     e = quasar::launch_rubin(p, w_bf16, ema_mode, st);
   } else {
     quasar::Nvfp4Params p;
@@ -221,6 +223,7 @@ int launch_path(const quasar_desc* d, const void* W, void* Wu, float* m, float* 
     if (adam) p.adam = *adam;
     p.r_bf16 = r_bf16;
     p.amax_out = reinterpret_cast<unsigned*>(amax_out);
+    if (batch) p.batch = *batch;
     if (amax_out != nullptr) {
       e = quasar::launch_clear(p.amax_out, st);
       if (e != hipSuccess) return QUASAR_ERR_DEVICE;
@@ -252,6 +255,73 @@ int quasar_reconstruct(const quasar_desc* d, const void* W, float* v, const void
   return launch_path(d, W, nullptr, nullptr, v, g, ema_mode, nullptr, codes, scales, zeros, r,
                      d->w_dtype == QUASAR_BF16, best_clip, err, tensor_scale, tensor_amax, nullptr, workspace,
                      reinterpret_cast<hipStream_t>(stream));
+}
+
+int quasar_batch_check(const quasar_desc* d, const quasar_matrix* mats, int n_mats) {
+  if (d == nullptr || mats == nullptr || n_mats < 1 || n_mats > QUASAR_MAX_BATCH) return QUASAR_ERR_ARG;
+  const bool ema = mats[0].g != nullptr;
+  int64_t total = 0;
+  for (int i = 0; i < n_mats; i++) {
+    const quasar_matrix& x = mats[i];
+    if ((x.g != nullptr) != ema) return QUASAR_ERR_ARG;  // one EMA mode per launch
+    if (d->format == QUASAR_NVFP4 && x.tensor_amax == nullptr) return QUASAR_ERR_ARG;
+    quasar_desc dd = *d;
+    dd.rows = x.rows;
+    dd.cols = x.cols;
+    const int s = quasar_check(&dd, x.W, x.v, x.g, x.codes, x.scales, x.zeros, x.r, x.best_clip, x.err,
+                               x.tensor_scale, x.tensor_amax, nullptr, 0);
+    if (s != QUASAR_OK) return s;
+    const int64_t upb = d->format == QUASAR_NVFP4 ? quasar::nvfp4_units_per_block()
+                        : is_rubin(d)              ? quasar::rubin_units_per_block()
+                                                   : quasar::int_units_per_block(d->group);
+    total += (quasar_num_groups(&dd) + upb - 1) / upb;
+  }
+  if (total >= ((int64_t)1 << 31)) return QUASAR_ERR_SHAPE;  // one grid
+  return QUASAR_OK;
+}
+
+int quasar_reconstruct_batch(const quasar_desc* d, const quasar_matrix* mats, int n_mats, void* stream) {
+  const int s = quasar_batch_check(d, mats, n_mats);
+  if (s != QUASAR_OK) return s;
+  quasar::BatchTable bt;
+  memset(&bt, 0, sizeof(bt));
+  bt.n = n_mats;
+  const int64_t upb = d->format == QUASAR_NVFP4 ? quasar::nvfp4_units_per_block()
+                      : is_rubin(d)              ? quasar::rubin_units_per_block()
+                                                 : quasar::int_units_per_block(d->group);
+  for (int i = 0; i < n_mats; i++) {
+    const quasar_matrix& x = mats[i];
+    quasar_desc dd = *d;
+    dd.rows = x.rows;
+    dd.cols = x.cols;
+    quasar::MatrixSlot& ms = bt.s[i];
+    ms.W = x.W;
+    ms.v = x.v;
+    ms.g = x.g;
+    ms.codes = x.codes;
+    ms.scales = x.scales;
+    ms.zeros = x.zeros;
+    ms.r = x.r;
+    ms.best_clip = x.best_clip;
+    ms.err = x.err;
+    ms.tensor_scale = x.tensor_scale;
+    ms.amax = x.tensor_amax;
+    ms.n_units = quasar_num_groups(&dd);
+    ms.block0 = bt.total_blocks;
+    ms.cols = x.cols;
+    ms.blocks_per_row = x.cols / 64;
+    bt.total_blocks += (ms.n_units + upb - 1) / upb;
+  }
+  // the shared fields come from the descriptor; slot 0 also fills the
+  // single-matrix fields
+  quasar_desc d0 = *d;
+  d0.rows = mats[0].rows;
+  d0.cols = mats[0].cols;
+  const quasar_matrix& x = mats[0];
+  const int ema_mode = x.g == nullptr ? 0 : (d->g_dtype == QUASAR_BF16 ? 1 : 2);
+  return launch_path(&d0, x.W, nullptr, nullptr, x.v, x.g, ema_mode, nullptr, x.codes, x.scales, x.zeros, x.r,
+                     d->w_dtype == QUASAR_BF16, x.best_clip, x.err, x.tensor_scale, x.tensor_amax, nullptr, nullptr,
+                     reinterpret_cast<hipStream_t>(stream), n_mats > 1 ? &bt : nullptr);
 }
 
 int quasar_adamw_check(const quasar_desc* d, const quasar_adamw* opt, const void* W, const float* m,

@@ -60,21 +60,41 @@ void int_reconstruct_kernel(IntParams p) {
   }
   __syncthreads();
 
-  int64_t gid = ((int64_t)blockIdx.x * (kThreads / 64) + wave) * GPW + slot;
-  const bool active = gid < p.n_groups;
-  if (!active) gid = p.n_groups - 1;  // recompute the last group; nothing is stored
+  // this workgroup's matrix: the call's own, or in a batched launch the slot
+  // it falls in (uniform); the parameter block itself is only read
+  int64_t blk = blockIdx.x;
+  struct {
+    const void* W;
+    float* v;
+    const void* g;
+    uint8_t* codes;
+    float* scales;
+    float* zeros;
+    void* r;
+    uint8_t* best_clip;
+    float* err;
+    int64_t n_groups;
+  } mtx = {p.W, p.v, p.g, p.codes, p.scales, p.zeros, p.r, p.best_clip, p.err, p.n_groups};
+  if (p.batch.n > 1) {
+    const MatrixSlot& ms = batch_slot<IntParams>(blk);
+    mtx = {ms.W, ms.v, ms.g, ms.codes, static_cast<float*>(ms.scales), ms.zeros, ms.r, ms.best_clip, ms.err,
+         ms.n_units};
+  }
+  int64_t gid = (blk * (kThreads / 64) + wave) * GPW + slot;
+  const bool active = gid < mtx.n_groups;
+  if (!active) gid = mtx.n_groups - 1;  // recompute the last group; nothing is stored
   const int64_t e0 = gid * G + (int64_t)j * N;
 
   // ---- load (each byte of W, v, g once) ------------------------------------
   // W stays in its storage format in registers (bf16: 8 dwords) and is widened
   // on use, which keeps the kernel inside 128 VGPRs (4 waves per SIMD).
   WRegs<W_BF16> wr;
-  wr.load(p.W, e0);
+  wr.load(mtx.W, e0);
   float v[N];
-  load16<false>(p.v, e0, v);
+  load16<false>(mtx.v, e0, v);
   if constexpr (EMA == 1 || EMA == 2) {
     float g[N];
-    load16<EMA == 1>(p.g, e0, g);
+    load16<EMA == 1>(mtx.g, e0, g);
 #pragma unroll
     for (int i = 0; i < N; i++) {
       // v' = beta2 v + (1 - beta2) g^2 in the oracle's fp32 order
@@ -82,19 +102,19 @@ void int_reconstruct_kernel(IntParams p) {
       float u = p.omb2 * t;
       v[i] = __builtin_fmaf(p.beta2, v[i], u);
     }
-    if (active) store16<false>(p.v, e0, v);
+    if (active) store16<false>(mtx.v, e0, v);
   } else if constexpr (EMA >= 3) {
     // one AdamW step first; the updated W is reconstructed and the updated
     // second moment is the saliency
     float g[N], m[N], w[N];
-    load16<EMA == 3>(p.g, e0, g);
+    load16<EMA == 3>(mtx.g, e0, g);
     load16<false>(p.m, e0, m);
 #pragma unroll
     for (int i = 0; i < N; i++) w[i] = wr.get(i);
     adamw16(w, m, v, g, p.adam, p.beta2, p.omb2);
     wr.set(w);  // bf16 W: rounded here, and the rounded value is reconstructed
     if (active) {
-      store16<false>(p.v, e0, v);
+      store16<false>(mtx.v, e0, v);
       store16<false>(p.m, e0, m);
       wr.store(p.Wu, e0);
     }
@@ -325,11 +345,11 @@ void int_reconstruct_kernel(IntParams p) {
     }
   }
   if (!active) return;
-  if (p.r) {
+  if (mtx.r) {
     if (W_BF16 || p.r_bf16)
-      store16<true>(p.r, e0, r);
+      store16<true>(mtx.r, e0, r);
     else
-      store16<false>(p.r, e0, r);
+      store16<false>(mtx.r, e0, r);
   }
   if constexpr (BITS == 4) {
     uint32_t lo = 0, hi = 0;
@@ -338,34 +358,34 @@ void int_reconstruct_kernel(IntParams p) {
       lo |= qi[i] << (4 * i);
       hi |= qi[8 + i] << (4 * i);
     }
-    *reinterpret_cast<uint2*>(p.codes + gid * (G / 2) + j * 8) = make_uint2(lo, hi);
+    *reinterpret_cast<uint2*>(mtx.codes + gid * (G / 2) + j * 8) = make_uint2(lo, hi);
   } else if constexpr (BITS == 2) {
     uint32_t x = 0;
 #pragma unroll
     for (int i = 0; i < N; i++) x |= qi[i] << (2 * i);
-    *reinterpret_cast<uint32_t*>(p.codes + gid * (G / 4) + j * 4) = x;
+    *reinterpret_cast<uint32_t*>(mtx.codes + gid * (G / 4) + j * 4) = x;
   } else {  // BITS == 3: 48 bits per lane at byte offset 6 j of the group's stream
     uint64_t x = 0;
 #pragma unroll
     for (int i = 0; i < N; i++) x |= (uint64_t)qi[i] << (3 * i);
-    uint16_t* dst = reinterpret_cast<uint16_t*>(p.codes + gid * (3 * G / 8) + j * 6);
+    uint16_t* dst = reinterpret_cast<uint16_t*>(mtx.codes + gid * (3 * G / 8) + j * 6);
     dst[0] = (uint16_t)x;
     dst[1] = (uint16_t)(x >> 16);
     dst[2] = (uint16_t)(x >> 32);
   }
   if (j == 0) {
-    p.scales[gid] = a;
-    if (p.zeros) p.zeros[gid] = b;
-    if (p.best_clip) p.best_clip[gid] = (uint8_t)kout;
-    if (p.err) p.err[gid] = errv;
+    mtx.scales[gid] = a;
+    if (mtx.zeros) mtx.zeros[gid] = b;
+    if (mtx.best_clip) mtx.best_clip[gid] = (uint8_t)kout;
+    if (mtx.err) mtx.err[gid] = errv;
   }
 }
 
 template <bool W_BF16, int EMA, int BITS, int G>
 hipError_t launch_kc(const IntParams& p, hipStream_t s) {
-  constexpr int L = G / N;
-  constexpr int groups_per_block = kThreads / L;
-  const int64_t blocks = (p.n_groups + groups_per_block - 1) / groups_per_block;
+  constexpr int64_t groups_per_block = int_units_per_block(G);
+  const int64_t blocks =
+      p.batch.n > 1 ? p.batch.total_blocks : (p.n_groups + groups_per_block - 1) / groups_per_block;
   // clips per pass: one pass of 4, 8 or 12 clips when K <= 12 (entries past K
   // repeat the last clip and are never selected); passes of 8 beyond that
   const int K = p.n_clips;

@@ -37,36 +37,56 @@ void nvfp4_reconstruct_kernel(Nvfp4Params p) {
   }
   __syncthreads();
 
-  int64_t bid = (int64_t)blockIdx.x * kThreads + tid;
-  const bool active = bid < p.n_blocks;
-  if (!active) bid = p.n_blocks - 1;
+  // this workgroup's matrix (see int_kernel.hip)
+  int64_t blk = blockIdx.x;
+  struct {
+    const void* W;
+    float* v;
+    const void* g;
+    uint8_t* codes;
+    uint8_t* scales;
+    void* r;
+    uint8_t* best_clip;
+    float* err;
+    float* tensor_scale;
+    const float* amax;
+    int64_t n_blocks;
+  } mtx = {p.W, p.v, p.g, p.codes, p.scales, p.r, p.best_clip, p.err, p.tensor_scale, p.amax, p.n_blocks};
+  if (p.batch.n > 1) {
+    const MatrixSlot& ms = batch_slot<Nvfp4Params>(blk);
+    mtx = {ms.W, ms.v, ms.g, ms.codes, static_cast<uint8_t*>(ms.scales), ms.r, ms.best_clip, ms.err,
+         ms.tensor_scale, ms.amax, ms.n_units};
+  }
+  int64_t bid = blk * kThreads + tid;
+  const bool active = bid < mtx.n_blocks;
+  if (!active) bid = mtx.n_blocks - 1;
   const int64_t e0 = bid * N;
 
   WRegs<W_BF16> wr;
-  wr.load(p.W, e0);
+  wr.load(mtx.W, e0);
   float v[N];
-  load16<false>(p.v, e0, v);
+  load16<false>(mtx.v, e0, v);
   if constexpr (EMA == 1 || EMA == 2) {
     float g[N];
-    load16<EMA == 1>(p.g, e0, g);
+    load16<EMA == 1>(mtx.g, e0, g);
 #pragma unroll
     for (int i = 0; i < N; i++) {
       float t = g[i] * g[i];
       float u = p.omb2 * t;
       v[i] = __builtin_fmaf(p.beta2, v[i], u);
     }
-    if (active) store16<false>(p.v, e0, v);
+    if (active) store16<false>(mtx.v, e0, v);
   } else if constexpr (EMA >= 3) {
     // one AdamW step first (see int_kernel.hip)
     float g[N], m[N], w[N];
-    load16<EMA == 3>(p.g, e0, g);
+    load16<EMA == 3>(mtx.g, e0, g);
     load16<false>(p.m, e0, m);
 #pragma unroll
     for (int i = 0; i < N; i++) w[i] = wr.get(i);
     adamw16(w, m, v, g, p.adam, p.beta2, p.omb2);
     wr.set(w);
     if (active) {
-      store16<false>(p.v, e0, v);
+      store16<false>(mtx.v, e0, v);
       store16<false>(p.m, e0, m);
       wr.store(p.Wu, e0);
     }
@@ -76,7 +96,7 @@ void nvfp4_reconstruct_kernel(Nvfp4Params p) {
     for (int i = 0; i < N; i++) v[i] = weight_of(v[i], p.weighting);
   }
 
-  const float amax = __builtin_nontemporal_load(p.amax);
+  const float amax = __builtin_nontemporal_load(mtx.amax);
   const float st = amax / 2688.0f;  // 6 * 448
   float m = 0.0f;
 #pragma unroll
@@ -208,17 +228,17 @@ void nvfp4_reconstruct_kernel(Nvfp4Params p) {
     }
   }
   if (!active) return;
-  if (p.r) {
+  if (mtx.r) {
     if (W_BF16 || p.r_bf16)
-      store16<true>(p.r, e0, r);
+      store16<true>(mtx.r, e0, r);
     else
-      store16<false>(p.r, e0, r);
+      store16<false>(mtx.r, e0, r);
   }
-  *reinterpret_cast<uint2*>(p.codes + bid * 8) = make_uint2(cw[0], cw[1]);
-  p.scales[bid] = (uint8_t)best_e;
-  if (p.best_clip) p.best_clip[bid] = (uint8_t)kstar;
-  if (p.err) p.err[bid] = best_err;
-  if (bid == 0) p.tensor_scale[0] = st;
+  *reinterpret_cast<uint2*>(mtx.codes + bid * 8) = make_uint2(cw[0], cw[1]);
+  mtx.scales[bid] = (uint8_t)best_e;
+  if (mtx.best_clip) mtx.best_clip[bid] = (uint8_t)kstar;
+  if (mtx.err) mtx.err[bid] = best_err;
+  if (bid == 0) mtx.tensor_scale[0] = st;
 }
 
 // ---- tensor absmax ----------------------------------------------------------
@@ -276,7 +296,7 @@ __global__ __launch_bounds__(kThreads) void absmax_kernel(const void* W, int64_t
 
 template <bool W_BF16, int EMA>
 hipError_t launch_kc(const Nvfp4Params& p, hipStream_t s) {
-  const int64_t blocks = (p.n_blocks + kThreads - 1) / kThreads;
+  const int64_t blocks = p.batch.n > 1 ? p.batch.total_blocks : (p.n_blocks + kThreads - 1) / kThreads;
   const dim3 grid((unsigned)blocks), block(kThreads);
   const int K = p.n_clips;
   if (K <= 4)

@@ -12,6 +12,55 @@ namespace quasar {
 constexpr int kMaxClips = 16;
 constexpr int kThreads = 256;   // 4 wavefronts of 64 lanes per workgroup
 
+constexpr int kMaxBatch = 16;  // matrices per batched launch
+
+// One matrix of a batched launch: its buffers, its work units (groups or
+// blocks) and the first workgroup of the grid that works on it.
+struct MatrixSlot {
+  const void* W;
+  float* v;
+  const void* g;
+  uint8_t* codes;
+  void* scales;
+  float* zeros;
+  void* r;
+  uint8_t* best_clip;
+  float* err;
+  float* tensor_scale;
+  const float* amax;
+  int64_t n_units;
+  int64_t block0;
+  int64_t cols;
+  int64_t blocks_per_row;
+};
+
+// n > 1: the launch covers n matrices; workgroup b works on the last slot with
+// block0 <= b (uniform per workgroup), which replaces the single-matrix fields.
+struct BatchTable {
+  int n;
+  int64_t total_blocks;
+  MatrixSlot s[kMaxBatch];
+};
+
+// The slot workgroup `blk` works on (n > 1), with blk made local to it.  The
+// table is read straight from the kernel-argument segment (the parameter
+// block is a kernel's first argument): indexing the by-value copy with a
+// run-time slot would force that copy into scratch memory.
+template <typename Params>
+__device__ __forceinline__ const MatrixSlot& batch_slot(int64_t& blk) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  const Params* kp = reinterpret_cast<const Params*>(__builtin_amdgcn_kernarg_segment_ptr());
+#else
+  const Params* kp = nullptr;  // the host pass never runs device code
+#endif
+  const BatchTable& b = kp->batch;
+  int mi = 0;
+#pragma unroll 1
+  while (mi + 1 < b.n && blk >= b.s[mi + 1].block0) mi++;
+  blk -= b.s[mi].block0;
+  return b.s[mi];
+}
+
 // Per-call parameters of the INT-b kernel (passed by value as the kernel argument).
 struct IntParams {
   const void* W;        // [rows, cols] fp32 or bf16
@@ -37,6 +86,7 @@ struct IntParams {
   float* m;
   AdamWConsts adam;
   int r_bf16;
+  BatchTable batch;
 };
 
 // Per-call parameters of the NVFP4 kernels.
@@ -62,6 +112,7 @@ struct Nvfp4Params {
   AdamWConsts adam;
   int r_bf16;
   unsigned* amax_out;   // fused step: max |W'| (fp32 bits, atomic max; cleared first) or NULL
+  BatchTable batch;
 };
 
 // Per-call parameters of the Rubin INT3 LUT kernel (blocks of 8 rows x 64 columns).
@@ -80,7 +131,13 @@ struct RubinParams {
   int weighting;
   float alpha[kMaxClips];  // 7 / (2 f_k)
   float clip[kMaxClips];
+  BatchTable batch;
 };
+
+// Work units (groups / blocks) one workgroup of each kernel covers.
+constexpr int64_t int_units_per_block(int group) { return kThreads / (group / 16); }
+constexpr int64_t nvfp4_units_per_block() { return kThreads; }
+constexpr int64_t rubin_units_per_block() { return kThreads / 64; }
 
 // Launchers (return the hipGetLastError() of the launches).
 hipError_t launch_rubin(const RubinParams& p, bool w_bf16, int ema_mode, hipStream_t s);

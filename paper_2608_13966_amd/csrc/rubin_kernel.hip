@@ -53,16 +53,34 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
   }
   __syncthreads();
 
-  int64_t bid = (int64_t)blockIdx.x * kWaves + wave;
-  const bool active = bid < p.n_blocks;  // uniform per wavefront
+  // this workgroup's matrix (see int_kernel.hip)
+  int64_t blk = blockIdx.x;
+  struct {
+    const void* W;
+    float* v;
+    const void* g;
+    uint8_t* codes;
+    uint8_t* lut;
+    void* r;
+    uint8_t* best_clip;
+    float* err;
+    int64_t n_blocks, cols, blocks_per_row;
+  } mtx = {p.W, p.v, p.g, p.codes, p.lut, p.r, p.best_clip, p.err, p.n_blocks, p.cols, p.blocks_per_row};
+  if (p.batch.n > 1) {
+    const MatrixSlot& ms = batch_slot<RubinParams>(blk);
+    mtx = {ms.W, ms.v, ms.g, ms.codes, static_cast<uint8_t*>(ms.scales), ms.r, ms.best_clip, ms.err, ms.n_units,
+         ms.cols, ms.blocks_per_row};
+  }
+  int64_t bid = blk * kWaves + wave;
+  const bool active = bid < mtx.n_blocks;  // uniform per wavefront
   if (!active) return;                   // no block-wide barrier follows
-  const int64_t rb = bid / p.blocks_per_row, cb = bid - rb * p.blocks_per_row;
-  const int64_t e0 = (rb * 8 + (lane >> 3)) * p.cols + cb * 64 + (lane & 7) * NE;
+  const int64_t rb = bid / mtx.blocks_per_row, cb = bid - rb * mtx.blocks_per_row;
+  const int64_t e0 = (rb * 8 + (lane >> 3)) * mtx.cols + cb * 64 + (lane & 7) * NE;
 
   // ---- load (each byte once), optional fused EMA, weighting ------------------
   float w[NE], v[NE];
   if constexpr (W_BF16) {
-    const uint4 t = ld128(reinterpret_cast<const uint16_t*>(p.W) + e0);
+    const uint4 t = ld128(reinterpret_cast<const uint16_t*>(mtx.W) + e0);
     const uint32_t d[4] = {t.x, t.y, t.z, t.w};
 #pragma unroll
     for (int k = 0; k < 4; k++) {
@@ -70,20 +88,20 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
       w[2 * k + 1] = as_f32(d[k] & 0xffff0000u);
     }
   } else {
-    const float* wp = reinterpret_cast<const float*>(p.W) + e0;
+    const float* wp = reinterpret_cast<const float*>(mtx.W) + e0;
     const uint4 a = ld128(wp), b = ld128(wp + 4);
     w[0] = as_f32(a.x); w[1] = as_f32(a.y); w[2] = as_f32(a.z); w[3] = as_f32(a.w);
     w[4] = as_f32(b.x); w[5] = as_f32(b.y); w[6] = as_f32(b.z); w[7] = as_f32(b.w);
   }
   {
-    const uint4 a = ld128(p.v + e0), b = ld128(p.v + e0 + 4);
+    const uint4 a = ld128(mtx.v + e0), b = ld128(mtx.v + e0 + 4);
     v[0] = as_f32(a.x); v[1] = as_f32(a.y); v[2] = as_f32(a.z); v[3] = as_f32(a.w);
     v[4] = as_f32(b.x); v[5] = as_f32(b.y); v[6] = as_f32(b.z); v[7] = as_f32(b.w);
   }
   if constexpr (EMA != 0) {
     float g[NE];
     if constexpr (EMA == 1) {
-      const uint4 t = ld128(reinterpret_cast<const uint16_t*>(p.g) + e0);
+      const uint4 t = ld128(reinterpret_cast<const uint16_t*>(mtx.g) + e0);
       const uint32_t d[4] = {t.x, t.y, t.z, t.w};
 #pragma unroll
       for (int k = 0; k < 4; k++) {
@@ -91,7 +109,7 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
         g[2 * k + 1] = as_f32(d[k] & 0xffff0000u);
       }
     } else {
-      const float* gp = reinterpret_cast<const float*>(p.g) + e0;
+      const float* gp = reinterpret_cast<const float*>(mtx.g) + e0;
       const uint4 a = ld128(gp), b = ld128(gp + 4);
       g[0] = as_f32(a.x); g[1] = as_f32(a.y); g[2] = as_f32(a.z); g[3] = as_f32(a.w);
       g[4] = as_f32(b.x); g[5] = as_f32(b.y); g[6] = as_f32(b.z); g[7] = as_f32(b.w);
@@ -102,8 +120,8 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
       const float u = p.omb2 * t;
       v[i] = __builtin_fmaf(p.beta2, v[i], u);
     }
-    st128(p.v + e0, make_uint4(as_u32(v[0]), as_u32(v[1]), as_u32(v[2]), as_u32(v[3])));
-    st128(p.v + e0 + 4, make_uint4(as_u32(v[4]), as_u32(v[5]), as_u32(v[6]), as_u32(v[7])));
+    st128(mtx.v + e0, make_uint4(as_u32(v[0]), as_u32(v[1]), as_u32(v[2]), as_u32(v[3])));
+    st128(mtx.v + e0 + 4, make_uint4(as_u32(v[4]), as_u32(v[5]), as_u32(v[6]), as_u32(v[7])));
   }
   if (p.weighting != 0) {
 #pragma unroll
@@ -243,31 +261,32 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
     r[i] = lut[q];
   }
   // 24 bits per lane at byte offset 3 lane of the block's 192-byte stream
-  uint8_t* cp = p.codes + bid * 192 + lane * 3;
+  uint8_t* cp = mtx.codes + bid * 192 + lane * 3;
   cp[0] = (uint8_t)bits;
   cp[1] = (uint8_t)(bits >> 8);
   cp[2] = (uint8_t)(bits >> 16);
-  if (p.r) {
+  if (mtx.r) {
     if constexpr (W_BF16) {
-      st128(reinterpret_cast<uint16_t*>(p.r) + e0,
+      st128(reinterpret_cast<uint16_t*>(mtx.r) + e0,
             make_uint4(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]), pack_bf16x2(r[4], r[5]),
                        pack_bf16x2(r[6], r[7])));
     } else {
-      float* rp = reinterpret_cast<float*>(p.r) + e0;
+      float* rp = reinterpret_cast<float*>(mtx.r) + e0;
       st128(rp, make_uint4(as_u32(r[0]), as_u32(r[1]), as_u32(r[2]), as_u32(r[3])));
       st128(rp + 4, make_uint4(as_u32(r[4]), as_u32(r[5]), as_u32(r[6]), as_u32(r[7])));
     }
   }
-  if (lane < 8) p.lut[bid * 8 + lane] = (uint8_t)lut_byte;
+  if (lane < 8) mtx.lut[bid * 8 + lane] = (uint8_t)lut_byte;
   if (lane == 0) {
-    if (p.best_clip) p.best_clip[bid] = (uint8_t)(constant ? 0 : kstar);
-    if (p.err) p.err[bid] = err;
+    if (mtx.best_clip) mtx.best_clip[bid] = (uint8_t)(constant ? 0 : kstar);
+    if (mtx.err) mtx.err[bid] = err;
   }
 }
 
 template <bool W_BF16>
 hipError_t launch_e(const RubinParams& p, int ema_mode, hipStream_t s) {
-  const dim3 grid((unsigned)((p.n_blocks + kWaves - 1) / kWaves)), block(kThreads);
+  const int64_t blocks = p.batch.n > 1 ? p.batch.total_blocks : (p.n_blocks + kWaves - 1) / kWaves;
+  const dim3 grid((unsigned)blocks), block(kThreads);
   switch (ema_mode) {
     case 1: hipLaunchKernelGGL((rubin_reconstruct_kernel<W_BF16, 1>), grid, block, 0, s, p); break;
     case 2: hipLaunchKernelGGL((rubin_reconstruct_kernel<W_BF16, 2>), grid, block, 0, s, p); break;

@@ -30,8 +30,9 @@ PARAM_DTYPES = {"fp32": F32, "fp16": F16, "bf16": BF16}
 MAX_CLIPS = 16
 
 EXPORTS = ("quasar_reconstruct", "quasar_absmax", "quasar_check", "quasar_adamw_reconstruct", "quasar_adamw_check",
-           "quasar_num_groups", "quasar_codes_bytes", "quasar_workspace_bytes", "quasar_status_string",
-           "quasar_version")
+           "quasar_reconstruct_batch", "quasar_batch_check", "quasar_num_groups", "quasar_codes_bytes",
+           "quasar_workspace_bytes", "quasar_status_string", "quasar_version")
+MAX_BATCH = 16
 
 
 class QuasarError(RuntimeError):
@@ -45,6 +46,14 @@ class Desc(C.Structure):
                 ("bits", C.c_int32), ("group", C.c_int32), ("clip_ratios", C.POINTER(C.c_float)),
                 ("n_clips", C.c_int32), ("g_dtype", C.c_int32), ("beta2", C.c_float),
                 ("weighting", C.c_int32), ("param_dtype", C.c_int32)]
+
+
+class Matrix(C.Structure):
+    """quasar_matrix: one matrix of a batched call."""
+    _fields_ = [("rows", C.c_int64), ("cols", C.c_int64), ("W", C.c_void_p), ("v", C.c_void_p), ("g", C.c_void_p),
+                ("codes", C.c_void_p), ("scales", C.c_void_p), ("zeros", C.c_void_p), ("r", C.c_void_p),
+                ("best_clip", C.c_void_p), ("err", C.c_void_p), ("tensor_scale", C.c_void_p),
+                ("tensor_amax", C.c_void_p)]
 
 
 class AdamW(C.Structure):
@@ -79,6 +88,11 @@ def lib():
             L.quasar_adamw_reconstruct.restype = C.c_int
             L.quasar_adamw_check.argtypes = [dp, ap, vp, vp, vp, vp, vp, vp, vp, vp, C.c_int, vp, vp, vp, vp, vp]
             L.quasar_adamw_check.restype = C.c_int
+            mp = C.POINTER(Matrix)
+            L.quasar_reconstruct_batch.argtypes = [dp, mp, C.c_int, vp]
+            L.quasar_reconstruct_batch.restype = C.c_int
+            L.quasar_batch_check.argtypes = [dp, mp, C.c_int]
+            L.quasar_batch_check.restype = C.c_int
             L.quasar_num_groups.argtypes = [dp]
             L.quasar_num_groups.restype = C.c_int64
             L.quasar_codes_bytes.argtypes = [dp]
@@ -156,6 +170,23 @@ def quasar_adamw_check(d: Descriptor, opt: AdamW, W, m, v, g, codes, scales, zer
     return lib().quasar_adamw_check(d.ref, None if opt is None else C.byref(opt), _p(W), _p(m), _p(v), _p(g),
                                     _p(codes), _p(scales), _p(zeros), _p(r), int(r_dtype), _p(best_clip), _p(err),
                                     _p(tensor_scale), _p(tensor_amax), _p(amax_out))
+
+
+def matrix(W, v, g, out, tensor_amax=None) -> Matrix:
+    """A quasar_matrix for tensors W, v, g (or None) and an alloc_outputs dict."""
+    return Matrix(W.shape[0], W.shape[1], _p(W), _p(v), _p(g), _p(out["codes"]), _p(out["scales"]),
+                  _p(out["zeros"]), _p(out["r"]), _p(out["best_clip"]), _p(out["err"]), _p(out["tensor_scale"]),
+                  _p(tensor_amax))
+
+
+def quasar_reconstruct_batch(d: Descriptor, mats, stream) -> int:
+    arr = (Matrix * len(mats))(*mats)
+    return lib().quasar_reconstruct_batch(d.ref, arr, len(mats), stream)
+
+
+def quasar_batch_check(d: Descriptor, mats) -> int:
+    arr = (Matrix * max(1, len(mats)))(*mats)
+    return lib().quasar_batch_check(d.ref, arr, len(mats))
 
 
 def quasar_num_groups(d: Descriptor) -> int:
@@ -288,3 +319,32 @@ def adamw_reconstruct(W, m, v, g, *, lr, beta1=0.9, beta2=0.999, eps=1e-8, weigh
         raise QuasarError(s, "quasar_adamw_reconstruct")
     out["desc"] = d
     return out
+
+
+def reconstruct_batch(items, *, fmt="int", bits=4, group=128, clips=(1.0,), beta2=0.999, want_r=True,
+                      want_diag=True, stream=None, weighting="h", param_dtype="fp32"):
+    """One batched call (quasar_reconstruct_batch) over ``items``: a list of
+    (W, v, g) or (W, v, g, tensor_amax) with one W dtype and one g dtype (or
+    every g None).  Returns one output dict per matrix, as reconstruct()."""
+    import torch
+    W0, g0 = items[0][0], items[0][2]
+    d = Descriptor(W0.shape[0], W0.shape[1], fmt=fmt, bits=bits, group=group, clips=clips,
+                   w_dtype=_dtype_code(W0), g_dtype=_dtype_code(g0) if g0 is not None else BF16, beta2=beta2,
+                   weighting=weighting, param_dtype=param_dtype)
+    outs, mats = [], []
+    for it in items:
+        W, v, g = it[0], it[1], it[2]
+        amax = it[3] if len(it) > 3 else None
+        dd = Descriptor(W.shape[0], W.shape[1], fmt=fmt, bits=bits, group=group, clips=clips,
+                        w_dtype=_dtype_code(W), g_dtype=_dtype_code(g) if g is not None else BF16, beta2=beta2,
+                        weighting=weighting, param_dtype=param_dtype)
+        o = alloc_outputs(dd, W, want_r=want_r, want_diag=want_diag, has_amax=True)
+        o["desc"] = dd
+        outs.append(o)
+        mats.append(matrix(W, v, g, o, amax))
+    if stream is None:
+        stream = torch.cuda.current_stream(W0.device).cuda_stream
+    s = quasar_reconstruct_batch(d, mats, stream)
+    if s != OK:
+        raise QuasarError(s, "quasar_reconstruct_batch")
+    return outs

@@ -197,3 +197,27 @@ def test_symmetric_int_descriptor_validation():
     assert _check(_int_desc(), tensor_amax=A) == Q.ERR_ARG
     assert Q.quasar_codes_bytes(_int_desc(fmt="int_sym", rows=2, cols=256, bits=3)) == 2 * 256 * 3 // 8
     assert _adam_check(_int_desc(fmt="int_sym", w_dtype=Q.F32)) == Q.ERR_FORMAT
+
+
+def _mat(rows=64, cols=256, **kw):
+    m = dict(rows=rows, cols=cols, W=A, v=A, g=None, codes=A, scales=A, zeros=A, r=A, best_clip=None, err=None,
+             tensor_scale=None, tensor_amax=None)
+    m.update(kw)
+    return Q.Matrix(*[m[k] for k, _ in Q.Matrix._fields_])
+
+
+def test_batch_entry_point_validation():
+    d = _int_desc()
+    assert Q.quasar_batch_check(d, [_mat(), _mat(rows=8, cols=128), _mat(rows=3, cols=384)]) == Q.OK
+    assert Q.quasar_batch_check(d, []) == Q.ERR_ARG
+    assert Q.quasar_batch_check(d, [_mat()] * 17) == Q.ERR_ARG
+    assert Q.quasar_batch_check(d, [_mat(), _mat(g=A)]) == Q.ERR_ARG          # mixed EMA modes
+    assert Q.quasar_batch_check(d, [_mat(), _mat(cols=200)]) == Q.ERR_SHAPE
+    assert Q.quasar_batch_check(d, [_mat(), _mat(W=A + 8)]) == Q.ERR_ALIGN
+    assert Q.quasar_batch_check(d, [_mat(zeros=None)]) == Q.ERR_ARG
+    nv = _int_desc(fmt="nvfp4")
+    assert Q.quasar_batch_check(nv, [_mat(zeros=None, tensor_scale=A, tensor_amax=A)] * 3) == Q.OK
+    assert Q.quasar_batch_check(nv, [_mat(zeros=None, tensor_scale=A)]) == Q.ERR_ARG  # amax required
+    rb = _int_desc(fmt="rubin")
+    assert Q.quasar_batch_check(rb, [_mat(zeros=None), _mat(rows=16, cols=64, zeros=None)]) == Q.OK
+    assert Q.quasar_batch_check(rb, [_mat(rows=12, zeros=None)]) == Q.ERR_SHAPE
