@@ -207,6 +207,7 @@ def main(argv=None):
             raise Q.QuasarError(s)
 
     # ---- launch plan: per matrix, or batched runs of up to MAX_BATCH matrices ----
+    nv = wl.fmt == "nvfp4" and not wl.adamw   # the plain NVFP4 path runs its absmax pass every step
     batched = args.launch == "batch" and not wl.adamw
     plans = []
     for ci in range(copies):
@@ -218,19 +219,30 @@ def main(argv=None):
             if len(grp) > 1:
                 arr = (Q.Matrix * len(grp))(*[Q.matrix(m["W"], m["v"], m["g"], m["out"], m["out"]["amax"])
                                               for m in grp])
+                if nv:  # the group's absmax passes in one launch as well
+                    arr = (arr, Q._ptr_array([m["out"]["amax"] for m in grp]))
             plan.append((grp, arr, sum(m["W"].numel() for m in grp)))
         plans.append(plan)
+
+    def absmax_group(grp, arr):
+        if arr is None:
+            for m in grp:
+                launch_absmax(m)
+            return
+        s = Q.lib().quasar_absmax_batch(grp[0]["d"].ref, arr[0], len(grp), arr[1], stream.cuda_stream)
+        if s != Q.OK:
+            raise Q.QuasarError(s, "quasar_absmax_batch")
 
     def launch_group(grp, arr):
         if arr is None:
             launch(grp[0])
             return
-        s = Q.lib().quasar_reconstruct_batch(grp[0]["d"].ref, arr, len(grp), stream.cuda_stream)
+        mats_arr = arr[0] if nv else arr
+        s = Q.lib().quasar_reconstruct_batch(grp[0]["d"].ref, mats_arr, len(grp), stream.cuda_stream)
         if s != Q.OK:
             raise Q.QuasarError(s, "quasar_reconstruct_batch")
 
     # ---- warmup ----------------------------------------------------------------
-    nv = wl.fmt == "nvfp4" and not wl.adamw   # the plain NVFP4 path runs its absmax pass every step
     if wl.adamw and wl.fmt == "nvfp4":
         for m in mats:
             launch_absmax(m)                        # the first step's tensor amax
@@ -238,8 +250,7 @@ def main(argv=None):
         step_no[0] = i
         for grp, arr, _ in plans[i % copies]:
             if nv:
-                for m in grp:
-                    launch_absmax(m)
+                absmax_group(grp, arr)
             launch_group(grp, arr)
     torch.cuda.synchronize()
 
@@ -252,11 +263,10 @@ def main(argv=None):
     for i in range(args.steps):
         step_no[0] = args.warmup + i
         for grp, arr, nw in plans[i % copies]:
-            if nv:  # NVFP4: the tensor absmax passes, timed on their own
+            if nv:  # NVFP4: the tensor absmax pass(es), timed on their own
                 a0 = torch.cuda.Event(enable_timing=True)
                 a0.record(stream)
-                for m in grp:
-                    launch_absmax(m)
+                absmax_group(grp, arr)
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
             launch_group(grp, arr)

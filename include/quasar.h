@@ -251,6 +251,22 @@ int quasar_reconstruct_batch(const quasar_desc* desc, const quasar_matrix* mats,
 /* Host-only validation: the status quasar_reconstruct_batch would return. */
 int quasar_batch_check(const quasar_desc* desc, const quasar_matrix* mats, int n_mats);
 
+/*
+ * Tensor absmax (Sec. 4.2, as quasar_absmax) of up to QUASAR_MAX_BATCH NVFP4
+ * matrices in one launch, e.g. ahead of quasar_reconstruct_batch.  Of each
+ * quasar_matrix only rows, cols and W are read (desc gives the format and W's
+ * dtype).  amax_out is a host array of n_mats device pointers (each 16-byte
+ * aligned, 1 fp32): amax_out[i] receives max |W| of mats[i] (cleared first,
+ * then filled by the pass).  Asynchronous on stream; on error nothing is
+ * launched.
+ */
+int quasar_absmax_batch(const quasar_desc* desc, const quasar_matrix* mats, int n_mats, float* const* amax_out,
+                        void* stream);
+
+/* Host-only validation: the status quasar_absmax_batch would return. */
+int quasar_absmax_batch_check(const quasar_desc* desc, const quasar_matrix* mats, int n_mats,
+                              float* const* amax_out);
+
 /* Host-only validation: the status quasar_reconstruct would return for these
  * arguments, without launching anything or touching device memory. */
 int quasar_check(const quasar_desc* desc, const void* W, const float* v, const void* g,

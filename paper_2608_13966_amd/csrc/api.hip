@@ -123,6 +123,45 @@ int quasar_absmax(const quasar_desc* d, const void* W, float* amax_out, void* st
   return e == hipSuccess ? QUASAR_OK : QUASAR_ERR_DEVICE;
 }
 
+int quasar_absmax_batch_check(const quasar_desc* d, const quasar_matrix* mats, int n_mats,
+                              float* const* amax_out) {
+  if (d == nullptr || mats == nullptr || amax_out == nullptr || n_mats < 1 || n_mats > QUASAR_MAX_BATCH)
+    return QUASAR_ERR_ARG;
+  int64_t total = 0;
+  for (int i = 0; i < n_mats; i++) {
+    quasar_desc dd = *d;
+    dd.rows = mats[i].rows;
+    dd.cols = mats[i].cols;
+    const int s = check_desc(&dd);
+    if (s != QUASAR_OK) return s;
+    if (dd.format != QUASAR_NVFP4) return QUASAR_ERR_FORMAT;
+    if (mats[i].W == nullptr || amax_out[i] == nullptr) return QUASAR_ERR_ARG;
+    if (!aligned16(mats[i].W) || !aligned16(amax_out[i])) return QUASAR_ERR_ALIGN;
+    total += quasar::absmax_blocks(dd.rows * dd.cols / (dd.w_dtype == QUASAR_BF16 ? 8 : 4));
+  }
+  if (total >= ((int64_t)1 << 31)) return QUASAR_ERR_SHAPE;  // one grid
+  return QUASAR_OK;
+}
+
+int quasar_absmax_batch(const quasar_desc* d, const quasar_matrix* mats, int n_mats, float* const* amax_out,
+                        void* stream) {
+  const int s = quasar_absmax_batch_check(d, mats, n_mats, amax_out);
+  if (s != QUASAR_OK) return s;
+  const bool w_bf16 = d->w_dtype == QUASAR_BF16;
+  quasar::AbsmaxTable t;
+  memset(&t, 0, sizeof(t));
+  t.n = n_mats;
+  for (int i = 0; i < n_mats; i++) {
+    t.W[i] = mats[i].W;
+    t.out[i] = reinterpret_cast<unsigned*>(amax_out[i]);
+    // cols % 16 == 0: a whole number of 16-byte chunks in either dtype
+    t.n_chunks[i] = mats[i].rows * mats[i].cols / (w_bf16 ? 8 : 4);
+    t.block0[i + 1] = t.block0[i] + quasar::absmax_blocks(t.n_chunks[i]);
+  }
+  const hipError_t e = quasar::launch_absmax(t, w_bf16, reinterpret_cast<hipStream_t>(stream));
+  return e == hipSuccess ? QUASAR_OK : QUASAR_ERR_DEVICE;
+}
+
 }  // extern "C"
 
 namespace {

@@ -15,6 +15,8 @@
 //
 // One lane owns one block: 16 weights in registers, no cross-lane reduction.
 // Moments and score in fp64 (see int_kernel.hip for why).
+#include <cstring>
+
 #include "device_common.h"
 #include "formats.h"
 #include "quasar_internal.h"
@@ -246,7 +248,15 @@ __global__ void absmax_clear_kernel(unsigned* ws) {
   if (threadIdx.x == 0 && blockIdx.x == 0) ws[0] = 0u;
 }
 
-// max |x| over the 16-byte chunk t (8 bf16 or 4 fp32 values)
+// every output of an absmax launch to 0 (a kernel, so that it may be captured)
+__global__ void absmax_clear_all_kernel(AbsmaxTable t) {
+#pragma unroll
+  for (int i = 0; i < kMaxBatch; i++)
+    if (i < t.n && threadIdx.x == 0) t.out[i][0] = 0u;
+}
+
+// max |x| over the 16-byte chunk t (8 bf16 or 4 fp32 values); NaNs are
+// ignored, as by fmaxf
 template <bool W_BF16>
 __device__ __forceinline__ float chunk_absmax(uint4 t) {
   const uint32_t d[4] = {t.x, t.y, t.z, t.w};
@@ -262,35 +272,49 @@ __device__ __forceinline__ float chunk_absmax(uint4 t) {
   return m;
 }
 
-// Grid-stride over 16-byte chunks, consecutive lanes on consecutive chunks
-// (fully coalesced), four independent loads in flight per lane.
+// One workgroup per span of kAbsChunks 16-byte chunks of one matrix: lane t
+// loads chunks t, t + 256, ... (each load instruction reads 1 KB contiguous per
+// wavefront), all kAbsSpan loads in flight at once; then a DPP / LDS maximum
+// and one atomicMax on the fp32 bit pattern per workgroup.
+constexpr int64_t kAbsChunks = (int64_t)kThreads * kAbsSpan;
+
 template <bool W_BF16>
-__global__ __launch_bounds__(kThreads) void absmax_kernel(const void* W, int64_t n_chunks, unsigned* ws) {
+__global__ __launch_bounds__(kThreads) void absmax_kernel(AbsmaxTable t) {
   __shared__ float s_m[kThreads / 64];
-  const uint4* src = reinterpret_cast<const uint4*>(W);
-  const int64_t stride = (int64_t)gridDim.x * kThreads;
-  int64_t c = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  float m0 = 0.0f, m1 = 0.0f, m2 = 0.0f, m3 = 0.0f;
-  for (; c + 3 * stride < n_chunks; c += 4 * stride) {
-    const uint4 t0 = src[c], t1 = src[c + stride], t2 = src[c + 2 * stride], t3 = src[c + 3 * stride];
-    m0 = fmaxf(m0, chunk_absmax<W_BF16>(t0));
-    m1 = fmaxf(m1, chunk_absmax<W_BF16>(t1));
-    m2 = fmaxf(m2, chunk_absmax<W_BF16>(t2));
-    m3 = fmaxf(m3, chunk_absmax<W_BF16>(t3));
+  // the table is read from the kernel-argument segment (see batch_slot)
+#if defined(__HIP_DEVICE_COMPILE__)
+  const AbsmaxTable* kt = reinterpret_cast<const AbsmaxTable*>(__builtin_amdgcn_kernarg_segment_ptr());
+#else
+  const AbsmaxTable* kt = nullptr;
+#endif
+  int64_t blk = blockIdx.x;
+  int mi = 0;
+#pragma unroll 1
+  while (mi + 1 < kt->n && blk >= kt->block0[mi + 1]) mi++;
+  blk -= kt->block0[mi];
+  const uint4* src = reinterpret_cast<const uint4*>(kt->W[mi]);
+  const int64_t n_chunks = kt->n_chunks[mi];
+  const int64_t c0 = blk * kAbsChunks + threadIdx.x;
+  uint4 buf[kAbsSpan];
+#pragma unroll
+  for (int u = 0; u < kAbsSpan; u++) {
+    const int64_t c = c0 + (int64_t)u * kThreads;
+    buf[u] = c < n_chunks ? src[c] : make_uint4(0u, 0u, 0u, 0u);
   }
-  for (; c < n_chunks; c += stride) m0 = fmaxf(m0, chunk_absmax<W_BF16>(src[c]));
-  float m = fmaxf(fmaxf(m0, m1), fmaxf(m2, m3));
+  float m = 0.0f;
+#pragma unroll
+  for (int u = 0; u < kAbsSpan; u++) m = fmaxf(m, chunk_absmax<W_BF16>(buf[u]));
   m = run_max<16>(m);
   m = fmaxf(m, __shfl_xor(m, 16, 64));
   m = fmaxf(m, __shfl_xor(m, 32, 64));
   if ((threadIdx.x & 63) == 0) s_m[threadIdx.x >> 6] = m;
   __syncthreads();
   if (threadIdx.x == 0) {
-    float t = s_m[0];
+    float x = s_m[0];
 #pragma unroll
-    for (int i = 1; i < kThreads / 64; i++) t = fmaxf(t, s_m[i]);
+    for (int i = 1; i < kThreads / 64; i++) x = fmaxf(x, s_m[i]);
     // |w| >= 0: the fp32 bit patterns order like unsigned integers
-    atomicMax(ws, __float_as_uint(t));
+    atomicMax(kt->out[mi], __float_as_uint(x));
   }
 }
 
@@ -332,21 +356,27 @@ hipError_t launch_clear(unsigned* ws, hipStream_t s) {
   return hipGetLastError();
 }
 
+hipError_t launch_absmax(const AbsmaxTable& t, bool w_bf16, hipStream_t s) {
+  hipLaunchKernelGGL(absmax_clear_all_kernel, dim3(1), dim3(64), 0, s, t);
+  const dim3 grid((unsigned)t.block0[t.n]), block(kThreads);
+  if (w_bf16)
+    hipLaunchKernelGGL(absmax_kernel<true>, grid, block, 0, s, t);
+  else
+    hipLaunchKernelGGL(absmax_kernel<false>, grid, block, 0, s, t);
+  return hipGetLastError();
+}
+
 hipError_t launch_absmax(const void* W, bool w_bf16, int64_t n, unsigned* ws, hipStream_t s) {
+  AbsmaxTable t;
+  memset(&t, 0, sizeof(t));
+  t.n = 1;
+  t.W[0] = W;
+  t.out[0] = ws;
   // n is a multiple of 16 (whole NVFP4 blocks), so W is a whole number of
   // 16-byte chunks in either dtype
-  const int64_t n_chunks = n / (w_bf16 ? 8 : 4);
-  // at most 4 blocks per CU: enough loads in flight with four per lane, and
-  // few enough blocks that each runs a long grid-stride loop
-  int64_t blocks = (n_chunks + 4 * kThreads - 1) / (4 * kThreads);
-  if (blocks > 1024) blocks = 1024;
-  if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(absmax_clear_kernel, dim3(1), dim3(64), 0, s, ws);
-  if (w_bf16)
-    hipLaunchKernelGGL(absmax_kernel<true>, dim3((unsigned)blocks), dim3(kThreads), 0, s, W, n_chunks, ws);
-  else
-    hipLaunchKernelGGL(absmax_kernel<false>, dim3((unsigned)blocks), dim3(kThreads), 0, s, W, n_chunks, ws);
-  return hipGetLastError();
+  t.n_chunks[0] = n / (w_bf16 ? 8 : 4);
+  t.block0[1] = absmax_blocks(t.n_chunks[0]);
+  return launch_absmax(t, w_bf16, s);
 }
 
 }  // namespace quasar

@@ -143,6 +143,23 @@ constexpr int64_t rubin_units_per_block() { return kThreads / 64; }
 hipError_t launch_rubin(const RubinParams& p, bool w_bf16, int ema_mode, hipStream_t s);
 hipError_t launch_int(const IntParams& p, int bits, int group, bool w_bf16, int ema_mode, hipStream_t s);
 hipError_t launch_nvfp4(const Nvfp4Params& p, bool w_bf16, int ema_mode, hipStream_t s);
+// Tensor absmax of up to kMaxBatch matrices in one launch: matrix i (W[i],
+// n_chunks[i] 16-byte chunks) is covered by workgroups [block0[i], block0[i+1])
+// and its max |W| lands in *out[i] as fp32 bits (cleared first).
+struct AbsmaxTable {
+  int n;
+  const void* W[kMaxBatch];
+  unsigned* out[kMaxBatch];
+  int64_t n_chunks[kMaxBatch];
+  int64_t block0[kMaxBatch + 1];
+};
+// 16-byte chunks one lane of the absmax kernel loads, and the workgroups it
+// needs for a matrix of n_chunks chunks
+constexpr int kAbsSpan = 16;
+constexpr int64_t absmax_blocks(int64_t n_chunks) {
+  return (n_chunks + (int64_t)kThreads * kAbsSpan - 1) / ((int64_t)kThreads * kAbsSpan);
+}
+hipError_t launch_absmax(const AbsmaxTable& t, bool w_bf16, hipStream_t s);
 // amax over n elements of W into *ws (as fp32 bits); clears *ws first.
 hipError_t launch_absmax(const void* W, bool w_bf16, int64_t n, unsigned* ws, hipStream_t s);
 

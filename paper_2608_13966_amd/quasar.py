@@ -30,7 +30,8 @@ PARAM_DTYPES = {"fp32": F32, "fp16": F16, "bf16": BF16}
 MAX_CLIPS = 16
 
 EXPORTS = ("quasar_reconstruct", "quasar_absmax", "quasar_check", "quasar_adamw_reconstruct", "quasar_adamw_check",
-           "quasar_reconstruct_batch", "quasar_batch_check", "quasar_num_groups", "quasar_codes_bytes",
+           "quasar_reconstruct_batch", "quasar_batch_check", "quasar_absmax_batch", "quasar_absmax_batch_check",
+           "quasar_num_groups", "quasar_codes_bytes",
            "quasar_workspace_bytes", "quasar_status_string", "quasar_version")
 MAX_BATCH = 16
 
@@ -93,6 +94,11 @@ def lib():
             L.quasar_reconstruct_batch.restype = C.c_int
             L.quasar_batch_check.argtypes = [dp, mp, C.c_int]
             L.quasar_batch_check.restype = C.c_int
+            pp = C.POINTER(vp)
+            L.quasar_absmax_batch.argtypes = [dp, mp, C.c_int, pp, vp]
+            L.quasar_absmax_batch.restype = C.c_int
+            L.quasar_absmax_batch_check.argtypes = [dp, mp, C.c_int, pp]
+            L.quasar_absmax_batch_check.restype = C.c_int
             L.quasar_num_groups.argtypes = [dp]
             L.quasar_num_groups.restype = C.c_int64
             L.quasar_codes_bytes.argtypes = [dp]
@@ -187,6 +193,21 @@ def quasar_reconstruct_batch(d: Descriptor, mats, stream) -> int:
 def quasar_batch_check(d: Descriptor, mats) -> int:
     arr = (Matrix * max(1, len(mats)))(*mats)
     return lib().quasar_batch_check(d.ref, arr, len(mats))
+
+
+def _ptr_array(ts):
+    return (C.c_void_p * max(1, len(ts)))(*[_p(t) for t in ts])
+
+
+def quasar_absmax_batch(d: Descriptor, mats, amax_out, stream) -> int:
+    """amax_out: one device fp32 tensor (or None) per matrix."""
+    arr = (Matrix * max(1, len(mats)))(*mats)
+    return lib().quasar_absmax_batch(d.ref, arr, len(mats), _ptr_array(amax_out), stream)
+
+
+def quasar_absmax_batch_check(d: Descriptor, mats, amax_out) -> int:
+    arr = (Matrix * max(1, len(mats)))(*mats)
+    return lib().quasar_absmax_batch_check(d.ref, arr, len(mats), _ptr_array(amax_out))
 
 
 def quasar_num_groups(d: Descriptor) -> int:
@@ -321,16 +342,41 @@ def adamw_reconstruct(W, m, v, g, *, lr, beta1=0.9, beta2=0.999, eps=1e-8, weigh
     return out
 
 
+def absmax_batch(Ws, *, stream=None):
+    """max |W| of each NVFP4 matrix in ``Ws`` (one dtype) in one batched pass
+    (quasar_absmax_batch); returns one device fp32 tensor [4] per matrix,
+    the value in element 0."""
+    import torch
+    W0 = Ws[0]
+    d = Descriptor(W0.shape[0], W0.shape[1], fmt="nvfp4", w_dtype=_dtype_code(W0))
+    outs = [torch.zeros(4, dtype=torch.float32, device=W0.device) for _ in Ws]
+    mats = [Matrix(W.shape[0], W.shape[1], _p(W)) for W in Ws]
+    if stream is None:
+        stream = torch.cuda.current_stream(W0.device).cuda_stream
+    s = quasar_absmax_batch(d, mats, outs, stream)
+    if s != OK:
+        raise QuasarError(s, "quasar_absmax_batch")
+    return outs
+
+
 def reconstruct_batch(items, *, fmt="int", bits=4, group=128, clips=(1.0,), beta2=0.999, want_r=True,
                       want_diag=True, stream=None, weighting="h", param_dtype="fp32"):
     """One batched call (quasar_reconstruct_batch) over ``items``: a list of
     (W, v, g) or (W, v, g, tensor_amax) with one W dtype and one g dtype (or
-    every g None).  Returns one output dict per matrix, as reconstruct()."""
+    every g None).  NVFP4 items without a tensor_amax get theirs from one
+    batched absmax pass first.  Returns one output dict per matrix, as
+    reconstruct()."""
     import torch
     W0, g0 = items[0][0], items[0][2]
     d = Descriptor(W0.shape[0], W0.shape[1], fmt=fmt, bits=bits, group=group, clips=clips,
                    w_dtype=_dtype_code(W0), g_dtype=_dtype_code(g0) if g0 is not None else BF16, beta2=beta2,
                    weighting=weighting, param_dtype=param_dtype)
+    if fmt == "nvfp4" and any(len(it) < 4 or it[3] is None for it in items):
+        need = [i for i, it in enumerate(items) if len(it) < 4 or it[3] is None]
+        am = absmax_batch([items[i][0] for i in need], stream=stream)
+        items = list(items)
+        for i, a in zip(need, am):
+            items[i] = (items[i][0], items[i][1], items[i][2], a)
     outs, mats = [], []
     for it in items:
         W, v, g = it[0], it[1], it[2]

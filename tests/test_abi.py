@@ -221,3 +221,18 @@ def test_batch_entry_point_validation():
     rb = _int_desc(fmt="rubin")
     assert Q.quasar_batch_check(rb, [_mat(zeros=None), _mat(rows=16, cols=64, zeros=None)]) == Q.OK
     assert Q.quasar_batch_check(rb, [_mat(rows=12, zeros=None)]) == Q.ERR_SHAPE
+
+
+def test_absmax_batch_validation():
+    nv = _int_desc(fmt="nvfp4")
+    mats = [_mat(), _mat(rows=1, cols=16), _mat(rows=5, cols=48)]
+    assert Q.quasar_absmax_batch_check(nv, mats, [A] * 3) == Q.OK
+    assert Q.quasar_absmax_batch_check(nv, [], []) == Q.ERR_ARG
+    assert Q.quasar_absmax_batch_check(nv, [_mat()] * 17, [A] * 17) == Q.ERR_ARG
+    assert Q.quasar_absmax_batch_check(nv, mats, [A, None, A]) == Q.ERR_ARG    # an output missing
+    assert Q.quasar_absmax_batch_check(nv, mats, [A, A, A + 4]) == Q.ERR_ALIGN
+    assert Q.quasar_absmax_batch_check(nv, [_mat(W=A + 8)], [A]) == Q.ERR_ALIGN
+    assert Q.quasar_absmax_batch_check(nv, [_mat(W=None)], [A]) == Q.ERR_ARG
+    assert Q.quasar_absmax_batch_check(nv, [_mat(cols=24)], [A]) == Q.ERR_SHAPE  # not whole 16-blocks
+    assert Q.quasar_absmax_batch_check(nv, [_mat(rows=0)], [A]) == Q.ERR_SHAPE
+    assert Q.quasar_absmax_batch_check(_int_desc(), [_mat()], [A]) == Q.ERR_FORMAT

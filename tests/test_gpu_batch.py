@@ -136,3 +136,37 @@ def test_batch_llama_layer_shapes():
                  oracle_check=False)
     del mats
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("w_bf16", [True, False])
+def test_absmax_batch_exact(w_bf16):
+    """The batched tensor absmax equals max |W| exactly (it is a maximum), for
+    matrices that end inside a workgroup's span, a maximum planted at the first
+    or last element or negative, and a matrix of zeros."""
+    shapes = [(1, 16), (7, 272), (33, 1040), (4096, 4096), (3, 4096 * 16 + 16), (2, 32)]
+    Ws = []
+    for i, (r, c) in enumerate(shapes):
+        W, _, _ = synth.gen_matrix(r, c, 900 + i, w_bf16=w_bf16, ema=False, device="cuda")
+        Ws.append(W)
+    Ws[1].view(-1)[-1] = -3.5            # largest magnitude, last element, negative
+    Ws[2].view(-1)[0] = 7.25             # first element
+    Ws[5].zero_()
+    print(f"[case] absmax batch of {len(Ws)} w={'bf16' if w_bf16 else 'f32'}", flush=True)
+    outs = Q.absmax_batch(Ws)
+    torch.cuda.synchronize()
+    for i, (W, o) in enumerate(zip(Ws, outs)):
+        want = W.float().abs().max().reshape(1).view(torch.int32).item()
+        got = o[:1].view(torch.int32).item()
+        assert got == want, f"matrix {i} {tuple(W.shape)}: amax bits {got:#x} vs {want:#x}"
+
+
+def test_batch_nvfp4_amax_from_batched_pass():
+    """reconstruct_batch with no tensor amax takes it from one batched absmax
+    pass; the results equal single-matrix calls that compute their own."""
+    shapes = [(6, 64), (33, 256), (16, 512)]
+    mats = _draw(shapes, 1103, w_bf16=True, ema=False)
+    singles = [Q.reconstruct(W, v.clone(), g, fmt="nvfp4", clips=(1.0, 0.9, 0.8)) for W, v, g in mats]
+    outs = Q.reconstruct_batch([(W, v.clone(), g) for W, v, g in mats], fmt="nvfp4", clips=(1.0, 0.9, 0.8))
+    torch.cuda.synchronize()
+    for i, (a, b) in enumerate(zip(singles, outs)):
+        _same(f"nvfp4.auto.{i}", a, b)
