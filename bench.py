@@ -111,6 +111,11 @@ def main(argv=None):
                     help="saliency weighting variant (h: the method's default)")
     ap.add_argument("--param-dtype", default="fp32", choices=["fp32", "fp16", "bf16"],
                     help="deployed precision of the INT dequantiser (s, z)")
+    ap.add_argument("--cpu-detail", action="store_true",
+                    help="also time the oracle's literal fp32 mode and one thread (reported in cpu_baseline)")
+    ap.add_argument("--diagnostics", action="store_true",
+                    help="report the chosen-clip histogram (GPU, whole step) and the mean score ratio to "
+                         "min-max RTN at clip 1.0 (oracle sample)")
     ap.add_argument("--launch", default="batch", choices=["single", "batch"],
                     help="one kernel launch per matrix, or one quasar_reconstruct_batch launch per run of up "
                          "to 16 consecutive matrices (reconstruction workloads; the fused optimiser step "
@@ -329,7 +334,8 @@ def main(argv=None):
         import oracle
         threads = min(16, os.cpu_count() or 1)
 
-        def oracle_rows(m, step):
+        def oracle_rows(m, step, n_threads=None, fp32_mode=False, diag_out=None):
+            nthr = threads if n_threads is None else n_threads
             if wl.fmt == "rubin":  # whole 8-row blocks
                 brows = torch.arange(0, m["W"].shape[0] // 8, step, device=dev)
                 rows = (brows[:, None] * 8 + torch.arange(8, device=dev)[None, :]).reshape(-1)
@@ -340,7 +346,7 @@ def main(argv=None):
             gh = None if m["g"] is None else synth.to_host(m["g"].index_select(0, rows))
             amax = oracle.absmax(synth.to_host(m["W"])) if wl.fmt == "nvfp4" else None
             kw = dict(fmt=wl.fmt, bits=wl.bits, group=wl.group, clips=wl.clips, tensor_amax=amax,
-                      n_threads=threads, weighting=args.weighting, param_dtype=args.param_dtype)
+                      n_threads=nthr, weighting=args.weighting, param_dtype=args.param_dtype)
             if wl.adamw:
                 mh = synth.to_host(m["m"].index_select(0, rows))
                 t1 = time.time()
@@ -349,10 +355,13 @@ def main(argv=None):
             elif wl.fmt == "rubin":
                 t1 = time.time()
                 oracle.rubin_reconstruct(Ws, vh, clips=wl.clips, g=gh, beta2=wl.beta2, weighting=args.weighting,
-                                         n_threads=threads)
+                                         n_threads=nthr)
             else:
                 t1 = time.time()
-                oracle.reconstruct(Ws, vh, g=gh, beta2=wl.beta2, **kw)
+                o = oracle.reconstruct(Ws, vh, g=gh, beta2=wl.beta2, fp32_mode=fp32_mode,
+                                       want_diag=diag_out is not None, **kw)
+                if diag_out is not None:
+                    diag_out.append((o["err"].astype(np.float64), o["diag"][:, 0]))
             return Ws.size, time.time() - t1
 
         # pilot on the largest matrix, then a stride that spends about
@@ -376,12 +385,29 @@ def main(argv=None):
             if attempt == 1 or step == 1 or spent >= 0.5 * args.cpu_seconds:
                 break
             step = max(1, int(step * spent / args.cpu_seconds))
+        detail = {}
+        if args.cpu_detail and wl.fmt in ("int", "nvfp4", "int_sym") and not wl.adamw:
+            # the same sample with the literal fp32 accumulation mode, and a
+            # sparser sample on one thread
+            fw, ft = 0, 0.0
+            for m in mats[:per_step]:
+                w_, t_ = oracle_rows(m, step, fp32_mode=True)
+                fw += w_
+                ft += t_
+            detail["fp32_mode_value"] = round(fw / ft / 1e9, 6)
+            sw, stt = 0, 0.0
+            for m in mats[:per_step]:
+                w_, t_ = oracle_rows(m, step * 16, n_threads=1)
+                sw += w_
+                stt += t_
+            detail["single_thread_value"] = round(sw / stt / 1e9, 6)
+            detail["single_thread_sample"] = f"rows 0, {16 * step}, ... of every matrix ({sw} weights, {stt:.1f} s)"
         cpu = {"value": round(sample_w / t_cpu / 1e9, 6), "unit": "G weights/s", "cores": threads,
                "kind": "oracle",
                "sample": f"{'block ' if wl.fmt == 'rubin' else ''}rows 0, {step}, {2 * step}, ... of every matrix "
                          f"of {args.workload} ({sample_w} weights, "
                          f"{t_cpu:.1f} s wall = {t_cpu * threads:.0f} thread-s on {threads} threads; "
-                         f"fp64 fit/score)"}
+                         f"fp64 fit/score)", **detail}
 
     # which roof binds: time per weight at the HBM peak vs at the VALU issue peak
     ops_w = algorithmic_valu_ops_per_weight(wl)
@@ -438,6 +464,31 @@ def main(argv=None):
         "wall_s_timed": round(wall, 3), "setup_s": round(setup_s, 1),
         "roofline": roofline, "cpu_baseline": cpu,
     }
+    if args.diagnostics and not wl.adamw:
+        # chosen-clip histogram over every group of one step (GPU), on copies
+        # of v so that the timed state is untouched
+        hist = np.zeros(len(wl.clips), dtype=np.int64)
+        for m in mats[:per_step]:
+            o = Q.reconstruct(m["W"], m["v"].clone(), m["g"], fmt=wl.fmt, bits=wl.bits, group=wl.group,
+                              clips=wl.clips, beta2=wl.beta2, want_r=False, want_diag=True,
+                              weighting=args.weighting, param_dtype=args.param_dtype)
+            hist += np.bincount(o["best_clip"].cpu().numpy(), minlength=len(wl.clips))[:len(wl.clips)]
+            del o
+        clips_arr = np.asarray(wl.clips, dtype=np.float32)
+        diag = {"best_clip_histogram": hist.tolist(),
+                "frac_groups_clip_below_1": round(float(hist[clips_arr < 1.0].sum() / hist.sum()), 6)}
+        if cpu is not None and wl.fmt in ("int", "nvfp4", "int_sym"):
+            # mean score of the chosen candidate over that of min-max RTN at
+            # clip 1.0 with the standard dequantiser, on a sparse oracle sample
+            pairs = []
+            for m in mats[:per_step]:
+                oracle_rows(m, step * 8, diag_out=pairs)
+            err = np.concatenate([a for a, _ in pairs])
+            rtn = np.concatenate([b for _, b in pairs])
+            ok = rtn > 0
+            diag["mean_score_over_rtn"] = round(float(np.mean(err[ok] / rtn[ok])), 6)
+            diag["rtn_sample_groups"] = int(ok.sum())
+        line["diagnostics"] = diag
     print(json.dumps(line), flush=True)
     return 0
 
