@@ -3,6 +3,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <algorithm>
 #include <cmath>
 
 #include "quasar.h"
@@ -166,6 +167,75 @@ int quasar_absmax_batch(const quasar_desc* d, const quasar_matrix* mats, int n_m
 
 namespace {
 
+// The code of u under a clip with scale alpha, in the kernels' fp32 recipe:
+// clamp(rint(fma(u, alpha, 3.5)), 0, 7) (correctly rounded fma, ties to even).
+int rubin_code(float u, float alpha) {
+  const float x = rintf(fmaf(u, alpha, 3.5f));
+  return (int)fminf(fmaxf(x, 0.0f), 7.0f);
+}
+
+// fp32 values in increasing order <-> unsigned keys in increasing order
+uint32_t f32_order_key(float f) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+float f32_from_order_key(uint32_t k) {
+  const uint32_t u = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
+  float f;
+  memcpy(&f, &u, 4);
+  return f;
+}
+
+// Lay the sorted list out as an implicit binary search tree (node n's children
+// at 2n and 2n + 1) by an in-order walk.
+void eytzinger_fill(float* tree, const float* sorted, int& next, int node) {
+  if (node >= quasar::kRubinThresholds) return;
+  eytzinger_fill(tree, sorted, next, 2 * node);
+  tree[node] = sorted[next++];
+  eytzinger_fill(tree, sorted, next, 2 * node + 1);
+}
+
+// The Rubin kernel's code thresholds: the code is non-decreasing in u, so
+// T(k, b) = min{u : code_k(u) >= b + 1} is found by bisection over the
+// ordered fp32 values between -inf (code 0) and +inf (code 7).
+void rubin_thresholds(quasar::RubinParams& p, int K) {
+  float t[quasar::kRubinThresholds];
+  int n = 0;
+  for (int k = 0; k < K; k++) {
+    for (int b = 0; b < 7; b++) {
+      uint32_t lo = f32_order_key(-INFINITY), hi = f32_order_key(INFINITY);
+      while (hi - lo > 1) {
+        const uint32_t mid = lo + (hi - lo) / 2;
+        if (rubin_code(f32_from_order_key(mid), p.alpha[k]) >= b + 1)
+          hi = mid;
+        else
+          lo = mid;
+      }
+      t[n++] = f32_from_order_key(hi);
+    }
+  }
+  for (int k = 0; k < quasar::kMaxClips; k++) {
+    for (int b = 0; b < 9; b++) {
+      int cnt = 0;
+      if (k < K && b >= 1 && b <= 7) {
+        const float tb = t[7 * k + b - 1];
+        for (int i = 0; i < n; i++) cnt += t[i] <= tb;
+      } else if (k < K && b == 8) {
+        cnt = n + 1;
+      }
+      p.tpos[k][b] = (uint8_t)cnt;
+    }
+  }
+  std::sort(t, t + n);
+  // in-order walk of the complete tree with nodes 1 .. 127 = the sorted list
+  float sorted[quasar::kRubinThresholds - 1];
+  for (int i = 0; i < quasar::kRubinThresholds - 1; i++) sorted[i] = i < n ? t[i] : INFINITY;
+  int next = 0;
+  eytzinger_fill(p.thr, sorted, next, 1);
+  p.thr[0] = INFINITY;
+}
+
 // Launch the reconstruction (ema_mode 0-2) or the fused AdamW step plus
 // reconstruction (ema_mode 3-4) after the arguments were validated.
 int launch_path(const quasar_desc* d, const void* W, void* Wu, float* m, float* v, const void* g, int ema_mode,
@@ -233,6 +303,7 @@ int launch_path(const quasar_desc* d, const void* W, void* Wu, float* m, float* 
       p.clip[k] = f;
       p.alpha[k] = 7.0f / (2.0f * f);
     }
+    rubin_thresholds(p, K);
     if (batch) p.batch = *batch;
     e = quasar::launch_rubin(p, w_bf16, ema_mode, st);
   } else {

@@ -115,6 +115,9 @@ struct Nvfp4Params {
   BatchTable batch;
 };
 
+// Rubin INT3 LUT: room for the 7 code thresholds of every clip, sorted.
+constexpr int kRubinThresholds = 128;  // >= 7 * kMaxClips, a power of two
+
 // Per-call parameters of the Rubin INT3 LUT kernel (blocks of 8 rows x 64 columns).
 struct RubinParams {
   const void* W;
@@ -131,6 +134,13 @@ struct RubinParams {
   int weighting;
   float alpha[kMaxClips];  // 7 / (2 f_k)
   float clip[kMaxClips];
+  // T(k, b) = the least fp32 u with code >= b + 1 under clip k, for all k < K
+  // and b < 7: sorted, padded with +inf to 127 entries and stored as an
+  // implicit search tree (thr[1] the root, node n's children at 2n and 2n + 1;
+  // thr[0] unused); tpos[k][b] = the number of them at or below T(k, b - 1)
+  // (0 for b = 0, 7K + 1 for b = 8)
+  float thr[kRubinThresholds];
+  uint8_t tpos[kMaxClips][9];
   BatchTable batch;
 };
 

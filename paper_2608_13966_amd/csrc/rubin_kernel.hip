@@ -4,17 +4,36 @@
 // A block is 8 rows x 64 columns (512 weights) with 3-bit indices and an
 // 8-entry E4M3 codebook.  For every clip factor f the indices are the INT3
 // codes of the range [c - f rho, c + f rho] (the same fp32 recipe as the
-// affine kernel), each codebook entry is the saliency-weighted mean of the
-// weights with that index rounded to E4M3, and the candidate is scored with
-// Eq. fisher-obj; the lowest score is emitted.
+// affine kernel: u = fma(w, 1/rho, -c/rho), q = clamp(rint(fma(u, alpha_f, 3.5)))),
+// each codebook entry is the saliency-weighted mean of the weights with that
+// index rounded to E4M3, and the candidate is scored with Eq. fisher-obj; the
+// lowest score is emitted.
+//
+// Every code is a non-decreasing function of u, so the codes a weight gets
+// under all K clips are fixed by how many of the 7K per-clip thresholds
+// T(k, b) = min{u : q_k(u) >= b + 1} lie at or below u.  That count -- the
+// weight's cell, 0 .. 7K -- is what the kernel bins by, once per block: the
+// thresholds are exact fp32 values found on the host and passed as an implicit
+// binary search tree (node n's children at 2n and 2n + 1), and
+// for clip k the weights with code b are exactly the cells in a fixed range
+// [tpos(k, b), tpos(k, b + 1)).  The per-clip work then reads two prefix sums
+// per codebook entry instead of re-binning 512 weights.
+//
+// The cell sums of h and h w are kept exact, as integers: each value is
+// scaled by a power of two fixed per block (from the block's largest h and
+// |w|) and split into two integer limbs (its nearest integer below 2^51 and
+// the rounded remainder in units of 2^-50), and the limbs are added with
+// 64-bit LDS atomics.  Integer addition is exact and order-independent, so the
+// sums -- and everything computed from them -- are deterministic, and a
+// codebook entry's sums (differences of exact prefix sums) carry a single
+// rounding.  Only a saliency below 2^-101 of the block's largest is lost; a
+// codebook entry whose weights all have such a saliency is recomputed
+// directly in fp64 (it is detected from a per-cell flag of positive h).
 //
 // Work decomposition: one wavefront per block, lane l holding row l/8 of the
 // block and its 8 consecutive columns 8 (l % 8) .. 8 (l % 8) + 7.  The
-// per-index sums (sum h, sum h w) cannot be kept in registers (an element's
-// index selects one of 8 accumulators), so every lane accumulates into its own
-// 8 bins in LDS -- laid out [index][lane] so that a wavefront access touches
-// consecutive 16-byte slots -- and the wavefront then reduces the 64 lanes'
-// bins in two LDS stages.  No atomics: results are deterministic.
+// per-clip phase runs 8 clips at a time, lane (k, b) = (l / 8, l % 8) owning
+// codebook entry b of clip k.
 #include "device_common.h"
 #include "quasar_internal.h"
 
@@ -23,10 +42,11 @@ namespace {
 
 constexpr int NE = 8;          // weights per lane
 constexpr int kWaves = kThreads / 64;
+constexpr int kCells = kRubinThresholds;  // cell ids 0 .. 7K <= 112 < 128
+constexpr int kHiBits = 51;    // |scaled value| < 2^51: its nearest integer is the high limb
+constexpr int kLoBits = 50;    // the remainder, scaled by 2^50 and rounded, is the low limb
+constexpr double kMagic = 6755399441055744.0;  // 1.5 * 2^52: x + kMagic rounds x to an integer
 
-struct alignas(16) Bin {  // one 128-bit LDS access
-  double h, hw;
-};
 
 // E4M3 byte of x (nearest even, |x| clamped to 448 first: the conversion
 // gives NaN above 464), +0 for a zero result.
@@ -37,11 +57,37 @@ __device__ __forceinline__ uint32_t e4m3_byte(float x) {
 }
 __device__ __forceinline__ float e4m3_value(uint32_t e) { return __builtin_amdgcn_cvt_f32_fp8((int)e, 0); }
 
+// x (|x| < 2^51) as hi + lo 2^-50 with integer limbs: hi = rint(x), lo =
+// rint((x - hi) 2^50).  For |y| < 2^51, y + 1.5 2^52 lands where the fp64
+// spacing is 1, so its bit pattern minus that of 1.5 2^52 is rint(y) as a
+// two's-complement integer; x - hi and the scaling by 2^50 are exact.
+__device__ __forceinline__ void split_limbs(double x, int64_t& hi, int64_t& lo) {
+  const int64_t mb = __double_as_longlong(kMagic);
+  const double t = x + kMagic;
+  hi = __double_as_longlong(t) - mb;
+  const double r = __builtin_ldexp(x - (t - kMagic), kLoBits);
+  lo = __double_as_longlong(r + kMagic) - mb;
+}
+// hi + lo 2^-50 in fp64 (the limb sums stay below 2^60 in magnitude)
+__device__ __forceinline__ double join_limbs(int64_t hi, int64_t lo) {
+  return __builtin_ldexp((double)lo, -kLoBits) + (double)hi;
+}
+
+__device__ __forceinline__ int64_t shfl_up_i64(int64_t x, int d) {
+  return (int64_t)__shfl_up((long long)x, (unsigned)d, 64);
+}
+
 template <bool W_BF16, int EMA>
 __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams p) {
-  __shared__ Bin s_bins[kWaves][8][64];      // [wave][index][lane]
-  __shared__ Bin s_part[kWaves][8][8];       // [wave][lane group][index]
+  // per cell: h = hh + hl 2^-50 and h w = wh + wl 2^-50 in scaled units (one
+  // array per limb, so that lanes on different cells spread over the banks),
+  // then their exclusive prefix sums; a flag for an h > 0, then its prefix count
+  __shared__ int64_t s_limb[kWaves][4][kCells + 1];
+  __shared__ int s_flag[kWaves][kCells + 1];
+  __shared__ float s_thr[kCells];                 // thresholds in search-tree order
+  __shared__ uint8_t s_tpos[kMaxClips][9];        // cell range of code b under clip k
   __shared__ float s_lut[kWaves][8];
+  __shared__ uint32_t s_lutb[kWaves][8];
   __shared__ float s_alpha[kMaxClips], s_clip[kMaxClips];
 
   const int tid = threadIdx.x;
@@ -51,6 +97,8 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
     s_alpha[tid] = p.alpha[tid];
     s_clip[tid] = p.clip[tid];
   }
+  if (tid < kCells) s_thr[tid] = p.thr[tid];
+  if (tid < kMaxClips * 9) (&s_tpos[0][0])[tid] = (&p.tpos[0][0])[tid];
   __syncthreads();
 
   // this workgroup's matrix (see int_kernel.hip)
@@ -128,12 +176,13 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
     for (int i = 0; i < NE; i++) v[i] = weight_of(v[i], p.weighting);
   }
 
-  // ---- block range and clip-independent moments ------------------------------
-  float mn = w[0], mx = w[0];
+  // ---- block range, clip-independent moments, fixed-point scales --------------
+  float mn = w[0], mx = w[0], hm = v[0];
 #pragma unroll
   for (int i = 1; i < NE; i++) {
     mn = fminf(mn, w[i]);
     mx = fmaxf(mx, w[i]);
+    hm = fmaxf(hm, v[i]);
   }
   mn = run_min<16>(mn);
   mn = fminf(mn, __shfl_xor(mn, 16, 64));
@@ -146,7 +195,7 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
 #pragma unroll
   for (int i = 0; i < NE; i++) {
     H[i] = (double)v[i];
-    HW[i] = H[i] * (double)w[i];
+    HW[i] = H[i] * (double)w[i];  // exact: 24 x 24 significant bits
     sww = __builtin_fma(HW[i], (double)w[i], sww);
     sh += H[i];
   }
@@ -166,90 +215,167 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
 #pragma unroll
   for (int i = 0; i < NE; i++) u[i] = __builtin_fmaf(w[i], rrho, nc);
 
-  Bin(*bins)[64] = s_bins[wave];
-  Bin(*part)[8] = s_part[wave];
-  const int b8 = lane & 7;  // the index this lane reduces / owns in the codebook stage
-  double best_key = __longlong_as_double(0x7ff0000000000000ll);
-  uint32_t best_e = 0;  // lane b8's codebook byte of the best clip (lanes 0..7)
+  float* lutf = s_lut[wave];
+  uint32_t* lutb = s_lutb[wave];
+  double best_key = __longlong_as_double(0x7ff0000000000000ll);  // +inf
 
-  for (int k = 0; k < (constant ? 0 : K); k++) {
-    const float al = uniform_f32(s_alpha[k]);
-    // ---- this lane's per-index sums, in its private LDS bins -----------------
+  if (!constant) {  // uniform
+    // h < 2^eh and |h w| < 2^(eh + ew): the scaled values stay below 2^51,
+    // and the limb sums of 512 of them below 2^60
+    hm = run_max<16>(hm);
+    hm = fmaxf(hm, __shfl_xor(hm, 16, 64));
+    hm = fmaxf(hm, __shfl_xor(hm, 32, 64));
+    int eh, ew;
+    (void)__builtin_frexpf(hm, &eh);
+    (void)__builtin_frexpf(fmaxf(fabsf(mn), fabsf(mx)), &ew);
+    const int sh_exp = kHiBits - eh, sw_exp = kHiBits - eh - ew;
+
+    // ---- cells: clear, then add every weight's limbs into its cell ------------
+    int64_t(*limb)[kCells + 1] = s_limb[wave];
+    int* flag = s_flag[wave];
 #pragma unroll
-    for (int b = 0; b < 8; b++) bins[b][lane] = Bin{0.0, 0.0};
+    for (int t = 0; t < 2; t++) {
+#pragma unroll
+      for (int j = 0; j < 4; j++) limb[j][2 * lane + t] = 0;
+      flag[2 * lane + t] = 0;
+    }
+    wave_lds_fence();
 #pragma unroll
     for (int i = 0; i < NE; i++) {
-      const float x = __builtin_fmaf(u[i], al, 3.5f);
-      const int q = (int)__builtin_amdgcn_fmed3f(__builtin_rintf(x), 0.0f, 7.0f);
-      Bin t = bins[q][lane];
-      t.h += H[i];
-      t.hw += HW[i];
-      bins[q][lane] = t;
+      // cell = number of thresholds <= u: descend the implicit search tree
+      // (node n has children 2n, 2n + 1; the leaves 128 .. 255 are the counts)
+      int node = 1;
+#pragma unroll
+      for (int d = 0; d < 7; d++) node = 2 * node + (s_thr[node] <= u[i] ? 1 : 0);
+      const int pos = node - kCells;
+      int64_t x[4];
+      split_limbs(__builtin_ldexp(H[i], sh_exp), x[0], x[1]);
+      split_limbs(__builtin_ldexp(HW[i], sw_exp), x[2], x[3]);
+#pragma unroll
+      for (int j = 0; j < 4; j++)
+        atomicAdd(reinterpret_cast<unsigned long long*>(&limb[j][pos]), (unsigned long long)x[j]);
+      if (v[i] > 0.0f) flag[pos] = 1;
     }
     wave_lds_fence();
-    // ---- reduce over lanes: lane j sums index j/8 over the lanes congruent
-    // to j mod 8 (each group of 8 lanes reads 8 consecutive 16-byte slots:
-    // no bank conflicts) ----------------------------------------------------
+
+    // ---- exclusive prefix sums over the cells (lane l: cells 2l, 2l + 1) ------
     {
-      const int bi = lane >> 3, r0 = lane & 7;
-      double a = 0.0, bsum = 0.0;
+      int64_t a[4], x[4], t[4];
 #pragma unroll
-      for (int t = 0; t < 8; t++) {
-        const Bin x = bins[bi][r0 + 8 * t];
-        a += x.h;
-        bsum += x.hw;
+      for (int j = 0; j < 4; j++) {
+        a[j] = limb[j][2 * lane];
+        x[j] = t[j] = a[j] + limb[j][2 * lane + 1];
       }
-      part[r0][bi] = Bin{a, bsum};
+      const int fa = flag[2 * lane];
+      int xf = fa + flag[2 * lane + 1];
+      const int tf = xf;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {  // inclusive scan of the lane totals
+        int64_t y[4];
+#pragma unroll
+        for (int j = 0; j < 4; j++) y[j] = shfl_up_i64(x[j], d);
+        const int yf = __shfl_up(xf, (unsigned)d, 64);
+        if (lane >= d) {
+#pragma unroll
+          for (int j = 0; j < 4; j++) x[j] += y[j];
+          xf += yf;
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 4; j++) {
+        const int64_t e = x[j] - t[j];
+        limb[j][2 * lane] = e;
+        limb[j][2 * lane + 1] = e + a[j];
+        if (lane == 63) limb[j][kCells] = x[j];
+      }
+      const int ef = xf - tf;
+      flag[2 * lane] = ef;
+      flag[2 * lane + 1] = ef + fa;
+      if (lane == 63) flag[kCells] = xf;
     }
     wave_lds_fence();
-    // ---- lanes b = 0..7 (replicated in every group of 8): index b's totals ---
-    double hb = 0.0, hwb = 0.0;
+
+    // ---- clips, 8 at a time: lane (kk, b) owns codebook entry b of clip k0+kk --
+    const int kk = lane >> 3, b = lane & 7;
+    for (int k0 = 0; k0 < K; k0 += 8) {
+      const int k = k0 + kk;
+      const bool live = k < K;
+      const int kc = live ? k : 0;
+      const int t0 = s_tpos[kc][b], t1 = s_tpos[kc][b + 1];
+      const int cnt = flag[t1] - flag[t0];
+      double hb = __builtin_ldexp(join_limbs(limb[0][t1] - limb[0][t0], limb[1][t1] - limb[1][t0]), -sh_exp);
+      double hwb = __builtin_ldexp(join_limbs(limb[2][t1] - limb[2][t0], limb[3][t1] - limb[3][t0]), -sw_exp);
+      // entries whose saliency fell below the fixed-point range: exact fp64 sums
+      uint64_t need = __ballot(live && cnt > 0 && !(hb > 0.0));
+      while (need) {  // uniform; does not occur unless h spans over 2^101 in a block
+        const int L = __builtin_ctzll(need);
+        need &= need - 1;
+        const int kL = k0 + (L >> 3), bL = L & 7;
+        const float al = uniform_f32(s_alpha[kL]);
+        double sa = 0.0, sb = 0.0;
 #pragma unroll
-    for (int t = 0; t < 8; t++) {
-      const Bin x = part[t][b8];
-      hb += x.h;
-      hwb += x.hw;
+        for (int i = 0; i < NE; i++) {
+          const float q = __builtin_amdgcn_fmed3f(__builtin_rintf(__builtin_fmaf(u[i], al, 3.5f)), 0.0f, 7.0f);
+          if ((int)q == bL) {
+            sa += H[i];
+            sb += HW[i];
+          }
+        }
+        sa = run_sum<16>(sa);
+        sa += __shfl_xor(sa, 16, 64);
+        sa += __shfl_xor(sa, 32, 64);
+        sb = run_sum<16>(sb);
+        sb += __shfl_xor(sb, 16, 64);
+        sb += __shfl_xor(sb, 32, 64);
+        if (lane == L) {
+          hb = sa;
+          hwb = sb;
+        }
+      }
+      // Eq. rubin-fit: the loss-aware mean, in E4M3; an index with no saliency
+      // mass keeps the E4M3 value of its grid level
+      float meanf;
+      if (hb > 0.0) {
+        meanf = (float)div_f64(hwb, hb, rcp_f64(hb));
+      } else {
+        const float f = s_clip[kc];
+        const float fr = f * rho;
+        meanf = __builtin_fmaf((float)b, (2.0f * fr) / 7.0f, c - fr);
+      }
+      const uint32_t e = e4m3_byte(meanf);
+      const float cvf = e4m3_value(e);
+      const double cv = (double)cvf;
+      // score: sum_b (C_b^2 H_b - 2 C_b HW_b) + sum h w^2, over the 8 lanes of the clip
+      const double score = sww + run_sum<8>(cv * (cv * hb - 2.0 * hwb));
+      double key = live ? make_key(score, k) : __longlong_as_double(0x7ff0000000000000ll);
+      double kmin = run_min_f64<16>(key);
+      kmin = fmin(kmin, __shfl_xor(kmin, 16, 64));
+      kmin = fmin(kmin, __shfl_xor(kmin, 32, 64));
+      if (kmin < best_key) {  // uniform
+        best_key = kmin;
+        if (k == key_index(kmin)) {  // the 8 lanes of the winning clip
+          lutf[b] = cvf;
+          lutb[b] = e;
+        }
+      }
     }
-    wave_lds_fence();  // every lane has read part before the next clip writes it
-    // Eq. rubin-fit: the loss-aware mean, in E4M3; an index with no saliency
-    // mass keeps the E4M3 value of its grid level
-    float meanf;
-    if (hb > 0.0) {
-      meanf = (float)div_f64(hwb, hb, rcp_f64(hb));
-    } else {
-      const float f = uniform_f32(s_clip[k]);
-      const float fr = f * rho;
-      meanf = __builtin_fmaf((float)b8, (2.0f * fr) / 7.0f, c - fr);
-    }
-    const uint32_t e = e4m3_byte(meanf);
-    const double cv = (double)e4m3_value(e);
-    // score: sum_b (C_b^2 H_b - 2 C_b HW_b) + sum h w^2, summed over b = lane % 8
-    double term = cv * (cv * hb - 2.0 * hwb);
-    term = run_sum<8>(term);
-    const double score = sww + term;
-    const double key = make_key(score, k);
-    if (key < best_key) {  // uniform: every lane holds the same score
-      best_key = key;
-      best_e = e;
-    }
+  } else if (lane < 8) {  // constant block: every code 0, every entry E4M3(w)
+    const uint32_t e = e4m3_byte(mn);
+    lutf[lane] = e4m3_value(e);
+    lutb[lane] = e;
   }
+  wave_lds_fence();
 
   // ---- emit ------------------------------------------------------------------
-  const int kstar = key_index(best_key);
-  float* lut = s_lut[wave];
-  uint32_t lut_byte;
+  const int kstar = constant ? 0 : key_index(best_key);
   float err;
   if (constant) {
-    lut_byte = e4m3_byte(mn);
-    const double d = (double)e4m3_value(lut_byte) - (double)mn;
+    const double d = (double)lutf[0] - (double)mn;
     err = (float)(sh * d * d);
   } else {
-    lut_byte = best_e;
     err = (float)__longlong_as_double(__double_as_longlong(best_key) & ~15ll);
   }
-  if (lane < 8) lut[lane] = e4m3_value(lut_byte);
-  wave_lds_fence();
-  const float alpha = s_alpha[constant ? 0 : kstar];
+  const float alpha = s_alpha[kstar];
   uint32_t bits = 0;
   float r[NE];
 #pragma unroll
@@ -258,7 +384,7 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
     uint32_t q = (uint32_t)__builtin_amdgcn_fmed3f(__builtin_rintf(x), 0.0f, 7.0f);
     if (constant) q = 0;
     bits |= q << (3 * i);
-    r[i] = lut[q];
+    r[i] = lutf[q];
   }
   // 24 bits per lane at byte offset 3 lane of the block's 192-byte stream
   uint8_t* cp = mtx.codes + bid * 192 + lane * 3;
@@ -276,9 +402,9 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
       st128(rp + 4, make_uint4(as_u32(r[4]), as_u32(r[5]), as_u32(r[6]), as_u32(r[7])));
     }
   }
-  if (lane < 8) mtx.lut[bid * 8 + lane] = (uint8_t)lut_byte;
+  if (lane < 8) mtx.lut[bid * 8 + lane] = (uint8_t)lutb[lane];
   if (lane == 0) {
-    if (mtx.best_clip) mtx.best_clip[bid] = (uint8_t)(constant ? 0 : kstar);
+    if (mtx.best_clip) mtx.best_clip[bid] = (uint8_t)kstar;
     if (mtx.err) mtx.err[bid] = err;
   }
 }
