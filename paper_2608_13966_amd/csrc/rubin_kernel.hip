@@ -82,7 +82,7 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
   // per cell: h = hh + hl 2^-50 and h w = wh + wl 2^-50 in scaled units (one
   // array per limb, so that lanes on different cells spread over the banks),
   // then their exclusive prefix sums; a flag for an h > 0, then its prefix count
-  __shared__ int64_t s_limb[kWaves][4][kCells + 1];
+  __shared__ int64_t s_limb[kWaves][2][4][kCells + 1];
   __shared__ int s_flag[kWaves][kCells + 1];
   __shared__ float s_thr[kCells];                 // thresholds in search-tree order
   __shared__ uint8_t s_tpos[kMaxClips][9];        // cell range of code b under clip k
@@ -231,29 +231,39 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
     const int sh_exp = kHiBits - eh, sw_exp = kHiBits - eh - ew;
 
     // ---- cells: clear, then add every weight's limbs into its cell ------------
-    int64_t(*limb)[kCells + 1] = s_limb[wave];
+    // two copies of the cell sums (even / odd lanes) halve the atomics that
+    // meet on one address; the prefix sums go to copy 0
+    int64_t(*limb)[kCells + 1] = s_limb[wave][0];
+    int64_t(*limb1)[kCells + 1] = s_limb[wave][1];
+    int64_t(*mine)[kCells + 1] = s_limb[wave][lane & 1];
     int* flag = s_flag[wave];
 #pragma unroll
     for (int t = 0; t < 2; t++) {
 #pragma unroll
-      for (int j = 0; j < 4; j++) limb[j][2 * lane + t] = 0;
+      for (int j = 0; j < 4; j++) limb[j][2 * lane + t] = limb1[j][2 * lane + t] = 0;
       flag[2 * lane + t] = 0;
     }
     wave_lds_fence();
+    // cell = number of thresholds <= u: descend the implicit search tree
+    // (node n has children 2n, 2n + 1; the leaves 128 .. 255 are the counts),
+    // one level for all 8 weights at a time so that their reads overlap
+    int node[NE];
+#pragma unroll
+    for (int i = 0; i < NE; i++) node[i] = 1;
+#pragma unroll
+    for (int d = 0; d < 7; d++) {
+#pragma unroll
+      for (int i = 0; i < NE; i++) node[i] = 2 * node[i] + (s_thr[node[i]] <= u[i] ? 1 : 0);
+    }
 #pragma unroll
     for (int i = 0; i < NE; i++) {
-      // cell = number of thresholds <= u: descend the implicit search tree
-      // (node n has children 2n, 2n + 1; the leaves 128 .. 255 are the counts)
-      int node = 1;
-#pragma unroll
-      for (int d = 0; d < 7; d++) node = 2 * node + (s_thr[node] <= u[i] ? 1 : 0);
-      const int pos = node - kCells;
+      const int pos = node[i] - kCells;
       int64_t x[4];
       split_limbs(__builtin_ldexp(H[i], sh_exp), x[0], x[1]);
       split_limbs(__builtin_ldexp(HW[i], sw_exp), x[2], x[3]);
 #pragma unroll
       for (int j = 0; j < 4; j++)
-        atomicAdd(reinterpret_cast<unsigned long long*>(&limb[j][pos]), (unsigned long long)x[j]);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&mine[j][pos]), (unsigned long long)x[j]);
       if (v[i] > 0.0f) flag[pos] = 1;
     }
     wave_lds_fence();
@@ -263,8 +273,8 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
       int64_t a[4], x[4], t[4];
 #pragma unroll
       for (int j = 0; j < 4; j++) {
-        a[j] = limb[j][2 * lane];
-        x[j] = t[j] = a[j] + limb[j][2 * lane + 1];
+        a[j] = limb[j][2 * lane] + limb1[j][2 * lane];
+        x[j] = t[j] = a[j] + limb[j][2 * lane + 1] + limb1[j][2 * lane + 1];
       }
       const int fa = flag[2 * lane];
       int xf = fa + flag[2 * lane + 1];

@@ -136,3 +136,51 @@ def test_rubin_llama_gate_sampled():
     run_rubin("rubin.llama-gate", W, v, g, clips=clips, row_step_blocks=23)
     del W, v, g
     torch.cuda.empty_cache()
+
+
+def _f32_fma(a, b, c):
+    """fp32 fma on fp32 arrays: the fp64 product is exact and, at these
+    magnitudes, so is the fp64 sum, so one rounding to fp32 remains."""
+    return (a.astype(np.float64) * b.astype(np.float64) + c.astype(np.float64)).astype(np.float32)
+
+
+def _entries_below_range(W, v, clips):
+    """Number of (block, clip, index) whose weights all have a saliency below
+    2^-101 of their block's largest (and at least one such weight)."""
+    n = 0
+    for blk_w, blk_v in zip(_blocks(W, *W.shape), _blocks(v, *v.shape)):
+        mn, mx = blk_w.min(), blk_w.max()
+        c, rho = np.float32(0.5) * (mx + mn), np.float32(0.5) * (mx - mn)
+        rrho = np.float32(1.0) / rho
+        u = _f32_fma(blk_w, np.float32(rrho), np.float32(-(c * rrho)))
+        for f in clips:
+            al = np.float32(7.0) / (np.float32(2.0) * np.float32(f))
+            q = np.clip(np.rint(_f32_fma(u, al, np.float32(3.5))), 0, 7)
+            for b in range(8):
+                sel = blk_v[q == b]
+                n += int(sel.size > 0 and (sel.max() < blk_v.max() * 2.0 ** -101))
+    return n
+
+
+def test_rubin_saliency_beyond_fixed_point_range():
+    """Blocks whose saliency spans more than 2^101: the kernel's exact
+    fixed-point cell sums drop the smallest saliencies, and a codebook entry
+    made only of such weights is recomputed in fp64.  In every block one
+    weight has v = 1e20 and the weights above the block's 90th percentile of
+    w have v = 1e-15 (a ratio of 1e-35), so the top index of most clips holds
+    only those; codebook bytes, codes, r and scores must still match the
+    oracle's direct sums."""
+    torch.manual_seed(5)
+    W = (torch.randn(16, 128) * 0.02).float()
+    v = torch.rand(16, 128).float() + 0.5
+    for rb in range(2):
+        for cb in range(2):
+            blk = W[8 * rb:8 * rb + 8, 64 * cb:64 * cb + 64]
+            vb = v[8 * rb:8 * rb + 8, 64 * cb:64 * cb + 64]
+            top = blk >= torch.quantile(blk, 0.9)
+            vb[top] = 1e-15
+            vb[0, 0] = 1e20
+    clips = tuple(synth.clip_grid(1.0, 0.3, 15))
+    assert _entries_below_range(W.numpy(), v.numpy(), clips) > 0  # the case is exercised
+    run_rubin("rubin.saliency-range", W.cuda(), v.cuda(), clips=clips)
+    run_rubin("rubin.saliency-range.bf16", W.to(torch.bfloat16).cuda(), v.cuda(), clips=(1.0, 0.9, 0.75, 0.6))
