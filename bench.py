@@ -61,8 +61,13 @@ def algorithmic_valu_ops_per_weight(wl) -> float:
     if wl.fmt == "nvfp4":
         return 5.0 * K + 8.0 + pre
     if wl.fmt == "rubin":
-        # per clip: the code (3), the index address (2), two bin sums (2)
-        return 7.0 * K + 12.0 + pre
+        # per weight, once: its cell among the 7K code thresholds (7 levels of
+        # a search tree: compare and descend, 14), the exact fixed-point limbs
+        # of h and h w (10), range, h, h w, the clip-independent sums and the
+        # normalised position (8), the emitted code, codebook lookup and pack
+        # (5); per clip and block, each of the 8 codebook entries from two
+        # prefix sums (about 30 lane-ops per entry, 8 x 30 / 512 per weight)
+        return 37.0 + K * 8.0 * 30.0 / 512.0 + pre
     if wl.fmt == "int_sym":
         # per clip: the code (3), one product and two accumulations (3)
         return 6.0 * K + 9.0 + pre
