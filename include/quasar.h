@@ -278,6 +278,22 @@ int quasar_check(const quasar_desc* desc, const void* W, const float* v, const v
  * matrix; 0 for an invalid desc. */
 int64_t quasar_num_groups(const quasar_desc* desc);
 
+/* Which kernel serves INT and INT_SYM calls with this desc (host-only; the
+ * result depends on the clip grid, bits and group, not on the shape):
+ *  1  the binned kernel: each weight is placed once among the code thresholds
+ *     T(k, b) of every clip, and each candidate's moments for the fit of
+ *     Eq. ridgefit (Sec. 4.1.2) come from per-group suffix sums over those
+ *     cells;
+ *  0  the direct kernel: the moments are summed weight by weight for every
+ *     clip (grids with many thresholds per group lane, such as INT4 with 8
+ *     clips, where it is the faster one; or the environment variable
+ *     QUASAR_INT_PATH=direct).  QUASAR_INT_PATH=binned selects the binned
+ *     kernel for every grid whose thresholds fit its tables.
+ * Both give the same codes, chosen clip and r up to the rounding order of the
+ * fp64 moment sums.  A negative quasar_status for an invalid desc or another
+ * format. */
+int quasar_int_path(const quasar_desc* desc);
+
 /* Bytes of the packed code buffer; 0 for an invalid desc. */
 size_t quasar_codes_bytes(const quasar_desc* desc);
 

@@ -19,7 +19,7 @@ ROOT = os.path.dirname(HERE)
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libquasar.so")
-SOURCES = ["api.hip", "int_kernel.hip", "nvfp4_kernel.hip", "rubin_kernel.hip"]
+SOURCES = ["api.hip", "int_kernel.hip", "int_cells_kernel.hip", "nvfp4_kernel.hip", "rubin_kernel.hip"]
 ARCH = "gfx950"
 
 COMMON = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-ffp-contract=off",

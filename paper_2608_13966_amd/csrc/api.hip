@@ -1,6 +1,7 @@
 // api.hip -- the C ABI of libquasar.so (declared in include/quasar.h):
 // host-side argument validation, clip-table preparation and kernel dispatch.
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -167,6 +168,21 @@ int quasar_absmax_batch(const quasar_desc* d, const quasar_matrix* mats, int n_m
 
 namespace {
 
+// The clip tables of the INT kernels: f_k and the code scale alpha_k
+// (qmax / (2 f_k), symmetric Q / f_k, fp32 division); entries past K repeat
+// the last clip.
+void int_clip_tables(const quasar_desc* d, quasar::IntParams& p) {
+  const bool sym = d->format == QUASAR_INT_SYM;
+  const int K = d->n_clips;
+  const float qmax = (float)((1 << d->bits) - 1);
+  const float qsym = (float)((1 << (d->bits - 1)) - 1);
+  for (int k = 0; k < quasar::kMaxClips; k++) {
+    const float f = d->clip_ratios[k < K ? k : K - 1];
+    p.clip[k] = f;
+    p.alpha[k] = sym ? qsym / f : qmax / (2.0f * f);
+  }
+}
+
 // The code of u under a clip with scale alpha, in the kernels' fp32 recipe:
 // clamp(rint(fma(u, alpha, 3.5)), 0, 7) (correctly rounded fma, ties to even).
 int rubin_code(float u, float alpha) {
@@ -236,6 +252,104 @@ void rubin_thresholds(quasar::RubinParams& p, int K) {
   p.thr[0] = INFINITY;
 }
 
+// The code of u under clip k of an INT-b group, in the kernels' fp32 recipe:
+// asymmetric clamp(rint(fma(u, alpha, qmax/2)), 0, qmax), symmetric
+// clamp(rint(u * alpha), -Q, Q) (correctly rounded fma and product, ties to
+// even).
+int int_code(float u, float alpha, int qmax, bool sym) {
+  if (sym) {
+    const float x = rintf(u * alpha);
+    return (int)fminf(fmaxf(x, -(float)qmax), (float)qmax);
+  }
+  const float x = rintf(fmaf(u, alpha, 0.5f * (float)qmax));
+  return (int)fminf(fmaxf(x, 0.0f), (float)qmax);
+}
+
+// The bucket of u in the binned kernel, in its fp32 recipe.
+int cell_bucket(float u) {
+  const float h = 0.5f * (float)quasar::kCellBuckets;
+  return (int)fminf(fmaxf(fmaf(u, h, h), 0.0f), (float)(quasar::kCellBuckets - 1));
+}
+
+// The binned INT kernel's tables for this clip grid (int_cells_kernel.hip):
+// every threshold T(k, b) = the least fp32 u with code_k(u) >= q0 + b, found
+// by bisection over the ordered fp32 values between -inf (the lowest code)
+// and +inf (the highest).  Leaves n_cells = 0 -- the direct kernel runs --
+// when the cells do not fit the kernel's LDS budget, when a lane would scan
+// more than kCellsPerLaneAuto cells (the binned kernel's per-cell LDS work
+// then outweighs the per-clip work it saves: INT4 grids), or when
+// QUASAR_INT_PATH=direct is set.  QUASAR_INT_PATH=binned takes the binned
+// kernel wherever its tables fit.
+//
+// A bucket with more than three thresholds (every clip has one just below
+// u = 0, where the fp32 code rounding ties at qmax/2) takes the three at the
+// end that leaves the shorter stretch of the bucket to the exact search.
+void int_cells(quasar::IntParams& p, int K, int bits, bool sym, int group) {
+  memset(&p.cells, 0, sizeof(p.cells));
+  const char* force = getenv("QUASAR_INT_PATH");
+  if (force != nullptr && strcmp(force, "direct") == 0) return;
+  const bool any_fit = force != nullptr && strcmp(force, "binned") == 0;
+  const int qmax = sym ? (1 << (bits - 1)) - 1 : (1 << bits) - 1;
+  const int q0 = sym ? -qmax : 0;
+  const int nb = sym ? 2 * qmax : qmax;
+  float t[quasar::kMaxClips * quasar::kCellSteps];
+  int n = 0;
+  for (int k = 0; k < K; k++) {
+    for (int b = 1; b <= nb; b++) {
+      uint32_t lo = f32_order_key(-INFINITY), hi = f32_order_key(INFINITY);
+      while (hi - lo > 1) {
+        const uint32_t mid = lo + (hi - lo) / 2;
+        if (int_code(f32_from_order_key(mid), p.alpha[k], qmax, sym) >= q0 + b)
+          hi = mid;
+        else
+          lo = mid;
+      }
+      t[n++] = f32_from_order_key(hi);
+    }
+  }
+  float srt[quasar::kMaxClips * quasar::kCellSteps];
+  memcpy(srt, t, sizeof(float) * n);
+  std::sort(srt, srt + n);
+  const int m = (int)(std::unique(srt, srt + n) - srt);
+  const int L = group / 16;
+  const int cpl = (m + 1 + L - 1) / L;
+  if (cpl > quasar::kCellsPerLane || m + 3 > quasar::kCellThr || m > 127) return;
+  if (!any_fit && cpl > quasar::kCellsPerLaneAuto) return;
+  int cnt[quasar::kCellBuckets] = {0};
+  for (int i = 0; i < m; i++) cnt[cell_bucket(srt[i])]++;
+  int cmax = 1, below = 0, dense = 0;
+  const double width = 2.0 / quasar::kCellBuckets;
+  for (int b = 0; b < quasar::kCellBuckets; b++) {
+    int base = below, mode = 0;
+    if (cnt[b] > 3) {
+      // the stretch of the bucket each anchoring leaves to the search
+      const double b_lo = -1.0 + width * b, b_hi = b_lo + width;
+      const double up = b_hi - (double)srt[below + 2];          // mode 1: u >= t_base+2
+      const double down = (double)srt[below + cnt[b] - 3] - b_lo;  // mode 2: u < t_base
+      if (up <= down) {
+        mode = 1;
+      } else {
+        mode = 2;
+        base = below + cnt[b] - 3;
+      }
+      dense = 1;
+    }
+    p.cells.bucket[b] = (uint16_t)(base | (mode << 8));
+    below += cnt[b];
+    cmax = std::max(cmax, std::min(cnt[b], 3));
+  }
+  for (int k = 0; k < K; k++)
+    for (int b = 1; b <= nb; b++) {
+      const float tb = t[k * nb + b - 1];
+      p.cells.tp[k][b - 1] = (uint8_t)((std::lower_bound(srt, srt + m, tb) - srt) + 1);
+    }
+  for (int i = 0; i < quasar::kCellThr; i++) p.cells.thr[i] = i < m ? srt[i] : NAN;
+  p.cells.cpl = cpl;
+  p.cells.cmax = cmax;
+  p.cells.dense = dense;
+  p.cells.n_cells = m + 1;
+}
+
 // Launch the reconstruction (ema_mode 0-2) or the fused AdamW step plus
 // reconstruction (ema_mode 3-4) after the arguments were validated.
 int launch_path(const quasar_desc* d, const void* W, void* Wu, float* m, float* v, const void* g, int ema_mode,
@@ -267,18 +381,13 @@ int launch_path(const quasar_desc* d, const void* W, void* Wu, float* m, float* 
     p.weighting = d->weighting;
     p.param_dtype = d->param_dtype;
     p.symmetric = sym;
-    const float qmax = (float)((1 << d->bits) - 1);
-    const float qsym = (float)((1 << (d->bits - 1)) - 1);
-    for (int k = 0; k < quasar::kMaxClips; k++) {
-      const float f = d->clip_ratios[k < K ? k : K - 1];  // entries past K repeat the last clip
-      p.clip[k] = f;
-      p.alpha[k] = sym ? qsym / f : qmax / (2.0f * f);
-    }
+    int_clip_tables(d, p);
     p.Wu = Wu;
     p.m = m;
     if (adam) p.adam = *adam;
     p.r_bf16 = r_bf16;
     if (batch) p.batch = *batch;
+    int_cells(p, K, d->bits, sym, d->group);
     e = quasar::launch_int(p, d->bits, d->group, w_bf16, ema_mode, st);
   } else if (is_rubin(d)) {
     quasar::RubinParams p;
@@ -488,3 +597,14 @@ int quasar_adamw_reconstruct(const quasar_desc* d, const quasar_adamw* opt, void
 }
 
 }  // extern "C"
+
+extern "C" int quasar_int_path(const quasar_desc* d) {
+  const int s = check_desc(d);
+  if (s != QUASAR_OK) return s;
+  if (d->format != QUASAR_INT && d->format != QUASAR_INT_SYM) return QUASAR_ERR_FORMAT;
+  quasar::IntParams p;
+  memset(&p, 0, sizeof(p));
+  int_clip_tables(d, p);
+  int_cells(p, d->n_clips, d->bits, d->format == QUASAR_INT_SYM, d->group);
+  return p.cells.n_cells > 0 ? 1 : 0;
+}

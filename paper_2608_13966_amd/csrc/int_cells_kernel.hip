@@ -1,0 +1,324 @@
+// int_cells_kernel.hip -- QUASAR reconstruction for INT-b groups on gfx950,
+// the binned form: each weight is placed once among the code thresholds of
+// all candidates, and every candidate's moments come from per-group cell sums.
+//
+// Algorithm 1 (Sec. 4.1.2) needs, for every clip factor f_k, the weighted
+// moments sum h q, sum h q^2 and sum h q w of the RTN codes q = q_k(u)
+// (Eq. rtn) of the group's normalised positions u.  Each q_k is a
+// non-decreasing step function of u:
+//   q_k(u) = q0 + #{b in 1..NB : u >= T(k, b)},
+// with q0 = 0 and NB = qmax for asymmetric groups, q0 = -Q and NB = 2Q for
+// symmetric ones, and T(k, b) the least fp32 u whose code under clip k is at
+// least q0 + b.  The host finds every T(k, b) exactly, by bisection over the
+// ordered fp32 values with the kernels' own fp32 code recipe, and sorts the
+// distinct ones, t_0 < ... < t_{M-1}.  The cell of u is #{i : t_i <= u} in
+// [0, M]; all K codes of a weight are fixed by its cell.  With
+// P_b = sum of h over the weights with u >= T(k, b) (a suffix sum over cells)
+// and PW_b the same sum of h w, and n = q - q0:
+//   sum h n = sum_b P_b,   sum h n^2 = sum_b (2b - 1) P_b,   sum h n w = sum_b PW_b.
+// So the per-weight work no longer grows with the number of clips: one
+// bucket lookup and two LDS additions per weight replace K code evaluations
+// and 3K moment updates.
+//
+// Per weight: u; its bucket among 256 equal slices of [-1, 1] (the host table
+// gives the thresholds below the bucket and the next three thresholds), its
+// cell, then h and h w added into the group's cell as exact int64 values
+// (LDS atomics).  A group's lanes are spread over the wavefront (8 apart), so
+// members of one group that hit the same cell do not serialise the atomic.  Per group: suffix sums over the cells (each of the L lanes takes a
+// chunk; the chunk totals are combined across lanes), then each lane
+// assembles the moments of the clips it owns from NB suffix sums each and
+// solves and scores them exactly as the direct form does (int_common.h).
+// The emitted codes are recomputed from u with the fp32 recipe, so they are
+// bit-identical to the direct form's.
+#include "device_common.h"
+#include "int_common.h"
+#include "quasar_internal.h"
+
+namespace quasar {
+namespace {
+
+constexpr int N = kIntN;
+
+// Exclusive suffix sum over the members of a spread group (member j at lane
+// offset 8 j): member j gets the sum of the values of members j+1 .. L-1
+// (Hillis-Steele on the values shifted down by one member).
+template <int L>
+__device__ __forceinline__ double members_excl_suffix(double x, int j) {
+  double e = __shfl_down(x, 8);
+  if (j + 1 >= L) e = 0.0;
+#pragma unroll
+  for (int s = 1; s < L; s *= 2) {
+    const double y = __shfl_down(e, 8 * s);
+    if (j + s < L) e += y;
+  }
+  return e;
+}
+
+// An exact integer held as a double with |x| < 2^51, as int64: x + 1.5 2^52
+// lies in [2^52, 2^53), where the bit pattern is that of 1.5 2^52 plus x, and
+// the low word of 1.5 2^52 is zero.
+constexpr double kMagic = 6755399441055744.0;  // 1.5 * 2^52
+constexpr uint32_t kMagicHi = 0x43380000u;
+__device__ __forceinline__ uint64_t round_to_i64(double x) {
+  const uint64_t b = (uint64_t)__double_as_longlong(x + kMagic);  // rounds x to an integer (ties to even)
+  return b - ((uint64_t)kMagicHi << 32);
+}
+// ... and back (exact for |n| < 2^51)
+__device__ __forceinline__ double i64_to_double(uint64_t n) {
+  return __longlong_as_double((long long)(n + ((uint64_t)kMagicHi << 32))) - kMagic;
+}
+
+template <bool W_BF16, int EMA, int BITS, int G, bool SYM>
+__global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
+  constexpr int L = G / N;     // lanes per group
+  constexpr int GPW = 64 / L;  // groups per wavefront
+  constexpr int QMAX = SYM ? (1 << (BITS - 1)) - 1 : (1 << BITS) - 1;
+  constexpr int NB = SYM ? 2 * QMAX : QMAX;  // code steps per clip
+  constexpr int OWN = kMaxClips / L;         // clips a lane may own
+  constexpr int CPL = kCellsPerLane;         // most cells per lane
+  constexpr float kHalfBuckets = 0.5f * (float)kCellBuckets;
+  static_assert(kThreads == kCellBuckets && kThreads == kMaxClips * kCellSteps, "one table entry per thread");
+
+  extern __shared__ double s_hist[];  // [wave][group slot][cell][h, h w]
+  __shared__ uint4 s_bucket[kCellBuckets];
+  __shared__ float s_thr[128];
+  __shared__ uint8_t s_tp[kMaxClips * kCellSteps];
+  __shared__ float s_alpha[kMaxClips], s_clip[kMaxClips];
+  __shared__ float s_win[kThreads / 64][GPW][4];
+
+  using M = Members<L, true>;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int j = M::member(lane), slot = M::slot(lane);
+  const int K = p.n_clips;
+
+  {  // the tables, read from the kernel-argument segment with per-lane indices
+    const IntCells& cl = kernarg_params<IntParams>()->cells;
+    const uint32_t e = cl.bucket[tid];
+    const int c = (int)(e & 0xffu);
+    s_bucket[tid] = make_uint4(e, as_u32(cl.thr[c]), as_u32(cl.thr[c + 1]), as_u32(cl.thr[c + 2]));
+    s_tp[tid] = (&cl.tp[0][0])[tid];
+    if (tid < 128) s_thr[tid] = cl.thr[tid];
+  }
+  if (tid < kMaxClips) {
+    s_alpha[tid] = p.alpha[tid];
+    s_clip[tid] = p.clip[tid];
+  }
+  __syncthreads();
+
+  int64_t blk = blockIdx.x;
+  const IntMatrix mtx = int_matrix(p, blk);
+  int64_t gid = (blk * (kThreads / 64) + wave) * GPW + slot;
+  const bool active = gid < mtx.n_groups;
+  if (!active) gid = mtx.n_groups - 1;  // recompute the last group; nothing is stored
+  const int64_t e0 = gid * G + (int64_t)j * N;
+
+  WRegs<W_BF16> wr;
+  float v[N];
+  int_load<W_BF16, EMA>(p, mtx, e0, active, wr, v);
+  const IntRange rg = int_range<L, SYM, W_BF16, true>(wr);
+
+  // ---- this group's cells: lane j owns cells [j cpl, (j + 1) cpl) -----------
+  // Groups are int_cells_stride(cpl) cells apart, an odd number, so that the
+  // same cell of the wavefront's groups falls in different LDS banks.
+  const int cpl = p.cells.cpl;
+  double* hist = s_hist + (size_t)(wave * GPW + slot) * int_cells_stride<L>(cpl) * 2;
+  double* mine = hist + 2 * j * cpl;
+#pragma unroll
+  for (int i = 0; i < CPL; i++)
+    if (i < cpl) *reinterpret_cast<double2*>(mine + 2 * i) = make_double2(0.0, 0.0);
+  wave_lds_fence();
+
+  // ---- the cell of every weight (four bucket reads in flight at a time) -----
+  const int cmax = p.cells.cmax;
+  const bool dense = p.cells.dense != 0;
+  uint32_t cells[N / 4];  // four cells per register, one byte each
+#pragma unroll
+  for (int c4 = 0; c4 < N / 4; c4++) {
+    float u[4];
+    uint4 e[4];
+#pragma unroll
+    for (int t = 0; t < 4; t++) {
+      u[t] = int_u<SYM>(wr.get(4 * c4 + t), rg);
+      // bucket of u (monotone in u; a NaN u lands in bucket 0)
+      const float x =
+          fminf(fmaxf(__builtin_fmaf(u[t], kHalfBuckets, kHalfBuckets), 0.0f), (float)(kCellBuckets - 1));
+      e[t] = s_bucket[(int)x];
+    }
+    uint32_t packed = 0;
+#pragma unroll
+    for (int t = 0; t < 4; t++) {
+      // thresholds outside the bucket lie on the far side of u, and the
+      // table's padding is NaN, so the cell never passes the last threshold
+      int cell = (int)(e[t].x & 0xffu) + (u[t] >= as_f32(e[t].y) ? 1 : 0);
+      if (cmax > 1) cell += (u[t] >= as_f32(e[t].z) ? 1 : 0);
+      if (cmax > 2) cell += (u[t] >= as_f32(e[t].w) ? 1 : 0);
+      if (dense) {
+        // a bucket with more than three thresholds: outside the stretch its
+        // three compares cover, count every t_i <= u (t_127 is NaN)
+        const uint32_t mode = e[t].x >> 8;
+        if ((mode == 1 && u[t] >= as_f32(e[t].w)) || (mode == 2 && u[t] < as_f32(e[t].y))) {
+          int lo = 0;
+#pragma unroll
+          for (int step = 64; step >= 1; step >>= 1)
+            if (s_thr[lo + step - 1] <= u[t]) lo += step;
+          cell = lo;
+        }
+      }
+      packed |= (uint32_t)cell << (8 * t);
+    }
+    cells[c4] = packed;
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  // ---- h and h w of every weight into its cell, as exact integers --------------
+  // h and h w are scaled by powers of two that bring the group's largest |h|
+  // and |h| max|w| below 2^B, B = 51 - log2(G), rounded to integers and added
+  // as int64: every sum of at most G of them is exact and below 2^51, whatever
+  // the order of the atomics and of the scan, and stays exact in fp64.  Clips
+  // whose codes agree on the whole group get bit-identical moments, so their
+  // scores tie exactly and the lowest index wins, as in the exact definition.
+  // A term loses at most 2^-B of the largest one (about 6e-14).
+  constexpr int B = 51 - (G == 64 ? 6 : 7);
+  float hmax = 0.0f;
+#pragma unroll
+  for (int i = 0; i < N; i++) hmax = fmaxf(hmax, v[i]);
+  hmax = M::max(hmax);
+  const float wabs = SYM ? rg.mx : fmaxf(fabsf(rg.mn), fabsf(rg.mx));
+  // 2^eh > hmax and 2^ew > max |w| (frexp exponents)
+  const int eh = __builtin_amdgcn_frexp_expf(hmax), ew = __builtin_amdgcn_frexp_expf(wabs);
+  const double sh = __builtin_amdgcn_ldexp(1.0, B - eh), shw = __builtin_amdgcn_ldexp(1.0, B - eh - ew);
+  double Svww = 0.0;
+#pragma unroll
+  for (int i = 0; i < N; i++) {
+    const int cell = (int)((cells[i >> 2] >> (8 * (i & 3))) & 0xffu);
+    const double V = (double)v[i], Wd = (double)wr.get(i);
+    const double VW = V * Wd;
+    Svww = __builtin_fma(VW, Wd, Svww);
+    uint64_t* c64 = reinterpret_cast<uint64_t*>(hist + 2 * cell);
+    __hip_atomic_fetch_add(c64, round_to_i64(V * sh), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+    __hip_atomic_fetch_add(c64 + 1, round_to_i64(VW * shw), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+  }
+  wave_lds_fence();
+
+  // ---- suffix sums over the cells (exact integers, in fp64 from here on):
+  // the chunk totals first, then the members above this one, then a second
+  // pass that writes the suffix sums -------------------------------------------
+  {
+    double th = 0.0, tw = 0.0;
+#pragma unroll
+    for (int i = 0; i < CPL; i++) {
+      if (i < cpl) {
+        const ulonglong2 t = *reinterpret_cast<const ulonglong2*>(mine + 2 * i);
+        th += i64_to_double(t.x);
+        tw += i64_to_double(t.y);
+      }
+    }
+    double eh = members_excl_suffix<L>(th, j), ew = members_excl_suffix<L>(tw, j);
+#pragma unroll
+    for (int i = CPL - 1; i >= 0; i--) {
+      if (i < cpl) {
+        const ulonglong2 t = *reinterpret_cast<const ulonglong2*>(mine + 2 * i);
+        eh += i64_to_double(t.x);
+        ew += i64_to_double(t.y);
+        *reinterpret_cast<double2*>(mine + 2 * i) = make_double2(eh, ew);
+      }
+    }
+  }
+  wave_lds_fence();
+
+  // back from the integer scale (exact: powers of two)
+  const double rsh = __builtin_amdgcn_ldexp(1.0, eh - B), rshw = __builtin_amdgcn_ldexp(1.0, eh + ew - B);
+  IntMoments mo;
+  {
+    const double2 tot = *reinterpret_cast<const double2*>(hist);  // cell 0's suffix: the whole group
+    mo.Sv = tot.x * rsh;
+    mo.Svw = tot.y * rshw;
+  }
+  mo.Svww = M::sum(Svww);
+  mo.thr = 1e-12 * mo.Sv * mo.Sv * (double)QMAX * (double)QMAX;
+  mo.rSv = rcp_f64(mo.Sv);
+
+  // ---- the clips this lane owns: moments from NB suffix sums, fit, score ------
+  IntBest best = int_best_init();
+#pragma unroll 1
+  for (int t = 0; t < OWN; t++) {
+    const int k = j + L * t;
+    if (k < K) {
+      const uint4 tw4 = *reinterpret_cast<const uint4*>(s_tp + k * kCellSteps);
+      const uint32_t tw[4] = {tw4.x, tw4.y, tw4.z, tw4.w};
+      double A0 = 0.0, A1 = 0.0, A2 = 0.0;
+#pragma unroll
+      for (int b = 1; b <= NB; b++) {
+        const int c = (int)((tw[(b - 1) >> 2] >> (8 * ((b - 1) & 3))) & 0xffu);
+        const double2 s = *reinterpret_cast<const double2*>(hist + 2 * c);
+        A0 += s.x;
+        A1 = __builtin_fma((double)(2 * b - 1), s.x, A1);
+        A2 += s.y;
+      }
+      A0 *= rsh;
+      A1 *= rsh;
+      A2 *= rshw;
+      if constexpr (SYM) {  // q = n - Q
+        A1 = __builtin_fma((double)QMAX * (double)QMAX, mo.Sv, __builtin_fma(-2.0 * (double)QMAX, A0, A1));
+        A2 = __builtin_fma(-(double)QMAX, mo.Svw, A2);
+      }
+      int_fit_score<SYM, QMAX>(p, k, s_clip[k], rg, mo, A0, A1, A2, best);
+    }
+  }
+
+  int_finish<W_BF16, BITS, G, SYM, true>(p, mtx, wr, rg, mo.Sv, best, s_alpha, s_win[wave][slot], j, gid, e0,
+                                         active);
+}
+
+template <bool W_BF16, int EMA, int BITS, int G>
+hipError_t launch_g(const IntParams& p, hipStream_t s) {
+  constexpr int64_t groups_per_block = int_units_per_block(G);
+  const int64_t blocks =
+      p.batch.n > 1 ? p.batch.total_blocks : (p.n_groups + groups_per_block - 1) / groups_per_block;
+  const dim3 grid((unsigned)blocks), block(kThreads);
+  const size_t lds = int_cells_lds_bytes(G, p.cells.cpl);
+  if (p.symmetric) {
+    if constexpr (EMA <= 2) {
+      hipLaunchKernelGGL((int_cells_kernel<W_BF16, EMA, BITS, G, true>), grid, block, lds, s, p);
+      return hipGetLastError();
+    } else {
+      return hipErrorInvalidValue;
+    }
+  }
+  hipLaunchKernelGGL((int_cells_kernel<W_BF16, EMA, BITS, G, false>), grid, block, lds, s, p);
+  return hipGetLastError();
+}
+
+template <bool W_BF16, int EMA, int BITS>
+hipError_t launch_b(const IntParams& p, int group, hipStream_t s) {
+  return group == 64 ? launch_g<W_BF16, EMA, BITS, 64>(p, s) : launch_g<W_BF16, EMA, BITS, 128>(p, s);
+}
+
+template <bool W_BF16, int EMA>
+hipError_t launch_e(const IntParams& p, int bits, int group, hipStream_t s) {
+  switch (bits) {
+    case 2: return launch_b<W_BF16, EMA, 2>(p, group, s);
+    case 3: return launch_b<W_BF16, EMA, 3>(p, group, s);
+    default: return launch_b<W_BF16, EMA, 4>(p, group, s);
+  }
+}
+
+template <bool W_BF16>
+hipError_t launch_w(const IntParams& p, int bits, int group, int ema_mode, hipStream_t s) {
+  switch (ema_mode) {
+    case 1: return launch_e<W_BF16, 1>(p, bits, group, s);
+    case 2: return launch_e<W_BF16, 2>(p, bits, group, s);
+    case 3: return launch_e<W_BF16, 3>(p, bits, group, s);
+    case 4: return launch_e<W_BF16, 4>(p, bits, group, s);
+    default: return launch_e<W_BF16, 0>(p, bits, group, s);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_int_cells(const IntParams& p, int bits, int group, bool w_bf16, int ema_mode, hipStream_t s) {
+  return w_bf16 ? launch_w<true>(p, bits, group, ema_mode, s) : launch_w<false>(p, bits, group, ema_mode, s);
+}
+
+}  // namespace quasar

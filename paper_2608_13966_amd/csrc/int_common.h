@@ -1,0 +1,350 @@
+// int_common.h -- the parts of Algorithm 1 (Sec. 4.1.2) that both INT-b
+// reconstruction kernels share: the tile's matrix, the load with the optional
+// fused EMA / AdamW step, the group range, the closed-form fit and score of
+// one candidate, and the argmin + emit.  The kernels differ only in how they
+// obtain the per-candidate weighted moments (int_kernel.hip: direct sums per
+// clip; int_cells_kernel.hip: one binning by code threshold per weight).
+//
+// Work decomposition (both kernels): a group of G weights is owned by
+// L = G/16 consecutive lanes, each holding 16 consecutive weights in
+// registers; a wavefront processes 64/L groups.
+#pragma once
+
+#include "device_common.h"
+#include "quasar_internal.h"
+
+namespace quasar {
+
+constexpr int kIntN = 16;  // weights per lane
+
+// The L lanes that hold one group, and reductions over them.  Consecutive:
+// lanes L s .. L s + L - 1 (DPP inside a row of 16).  Spread: member j of
+// group s sits at lane s + 8 j (L = 8, s < 8) or (s & 7) + 8 j + 32 (s >> 3)
+// (L = 4, s < 16), so that no two members share an 8-lane block; LDS atomics
+// from members of one group that hit the same address then do not serialise.
+// Every pairing is symmetric and the operations commute, so all members end
+// with bit-identical results.
+template <int L, bool SPREAD>
+struct Members;
+
+template <int L>
+struct Members<L, false> {
+  static __device__ __forceinline__ int member(int lane) { return lane % L; }
+  static __device__ __forceinline__ int slot(int lane) { return lane / L; }
+  static __device__ __forceinline__ float min(float x) { return run_min<L>(x); }
+  static __device__ __forceinline__ float max(float x) { return run_max<L>(x); }
+  static __device__ __forceinline__ double sum(double x) { return run_sum<L>(x); }
+  static __device__ __forceinline__ double min_f64(double x) { return run_min_f64<L>(x); }
+};
+
+constexpr int kDppRor8 = 0x128;  // row_ror:8 -- lane i <-> i ^ 8 inside each 16
+
+template <int L>
+struct Members<L, true> {
+  static_assert(L == 4 || L == 8, "spread groups of 4 or 8 lanes");
+  static __device__ __forceinline__ int member(int lane) { return L == 8 ? lane >> 3 : (lane >> 3) & 3; }
+  static __device__ __forceinline__ int slot(int lane) { return L == 8 ? lane & 7 : (lane & 7) | ((lane >> 5) << 3); }
+  template <typename T, typename Op>
+  static __device__ __forceinline__ T reduce(T x, Op op) {
+    if constexpr (sizeof(T) == 8)
+      x = op(x, dpp_f64<kDppRor8>(x));
+    else
+      x = op(x, dpp_f32<kDppRor8>(x));
+    x = op(x, __shfl_xor(x, 16));
+    if constexpr (L == 8) x = op(x, __shfl_xor(x, 32));
+    return x;
+  }
+  static __device__ __forceinline__ float min(float x) { return reduce(x, [](float a, float b) { return fminf(a, b); }); }
+  static __device__ __forceinline__ float max(float x) { return reduce(x, [](float a, float b) { return fmaxf(a, b); }); }
+  static __device__ __forceinline__ double sum(double x) { return reduce(x, [](double a, double b) { return a + b; }); }
+  static __device__ __forceinline__ double min_f64(double x) {
+    return reduce(x, [](double a, double b) { return fmin(a, b); });
+  }
+};
+
+// The buffers of the matrix a workgroup works on: the call's own, or in a
+// batched launch the slot the workgroup falls in (uniform per workgroup).
+struct IntMatrix {
+  const void* W;
+  float* v;
+  const void* g;
+  uint8_t* codes;
+  float* scales;
+  float* zeros;
+  void* r;
+  uint8_t* best_clip;
+  float* err;
+  int64_t n_groups;
+};
+
+__device__ __forceinline__ IntMatrix int_matrix(const IntParams& p, int64_t& blk) {
+  IntMatrix m = {p.W, p.v, p.g, p.codes, p.scales, p.zeros, p.r, p.best_clip, p.err, p.n_groups};
+  if (p.batch.n > 1) {
+    const MatrixSlot& ms = batch_slot<IntParams>(blk);
+    m = {ms.W, ms.v, ms.g, ms.codes, static_cast<float*>(ms.scales), ms.zeros, ms.r, ms.best_clip, ms.err,
+         ms.n_units};
+  }
+  return m;
+}
+
+// Load the lane's 16 weights and saliencies (each byte of W, v, g once, with
+// 128-bit loads), run the fused EMA (EMA 1/2) or AdamW step (EMA 3/4) and
+// store their results, then apply the saliency weighting: h = v, v*v
+// (App. A.3) or 1 (Table 5).  W stays in its storage format in registers.
+template <bool W_BF16, int EMA>
+__device__ __forceinline__ void int_load(const IntParams& p, const IntMatrix& mtx, int64_t e0, bool active,
+                                         WRegs<W_BF16>& wr, float (&v)[kIntN]) {
+  wr.load(mtx.W, e0);
+  load16<false>(mtx.v, e0, v);
+  if constexpr (EMA == 1 || EMA == 2) {
+    float g[kIntN];
+    load16<EMA == 1>(mtx.g, e0, g);
+#pragma unroll
+    for (int i = 0; i < kIntN; i++) {
+      // v' = beta2 v + (1 - beta2) g^2 in the oracle's fp32 order
+      float t = g[i] * g[i];
+      float u = p.omb2 * t;
+      v[i] = __builtin_fmaf(p.beta2, v[i], u);
+    }
+    if (active) store16<false>(mtx.v, e0, v);
+  } else if constexpr (EMA >= 3) {
+    // one AdamW step first; the updated W is reconstructed and the updated
+    // second moment is the saliency
+    float g[kIntN], m[kIntN], w[kIntN];
+    load16<EMA == 3>(mtx.g, e0, g);
+    load16<false>(p.m, e0, m);
+#pragma unroll
+    for (int i = 0; i < kIntN; i++) w[i] = wr.get(i);
+    adamw16(w, m, v, g, p.adam, p.beta2, p.omb2);
+    wr.set(w);  // bf16 W: rounded here, and the rounded value is reconstructed
+    if (active) {
+      store16<false>(mtx.v, e0, v);
+      store16<false>(p.m, e0, m);
+      wr.store(p.Wu, e0);
+    }
+  }
+  if (p.weighting != 0) {
+#pragma unroll
+    for (int i = 0; i < kIntN; i++) v[i] = weight_of(v[i], p.weighting);
+  }
+}
+
+// The group's range (Alg. 1, first line).  Asymmetric: c = (mx + mn)/2,
+// rho = (mx - mn)/2, normalised position u = fmaf(w, 1/rho, -c/rho) in
+// [-1, 1].  Symmetric: m = max |w| (held in mx), u = w * (1/m).
+struct IntRange {
+  float mn, mx, c, rho, rrho, nc;
+  bool constant;  // asymmetric: mx == mn; symmetric: an all-zero group
+};
+
+template <int L, bool SYM, bool W_BF16, bool SPREAD = false>
+__device__ __forceinline__ IntRange int_range(const WRegs<W_BF16>& wr) {
+  using M = Members<L, SPREAD>;
+  IntRange g;
+  if constexpr (SYM) {
+    float mx = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kIntN; i++) mx = fmaxf(mx, fabsf(wr.get(i)));
+    mx = M::max(mx);
+    g.mn = 0.0f;
+    g.mx = mx;
+    g.constant = (mx == 0.0f);
+    g.c = 0.0f;
+    g.rho = mx;
+    g.rrho = 1.0f / mx;
+    g.nc = 0.0f;
+  } else {
+    float mn = wr.get(0), mx = wr.get(0);
+#pragma unroll
+    for (int i = 1; i < kIntN; i++) {
+      mn = fminf(mn, wr.get(i));
+      mx = fmaxf(mx, wr.get(i));
+    }
+    mn = M::min(mn);
+    mx = M::max(mx);
+    g.mn = mn;
+    g.mx = mx;
+    g.constant = (mx == mn);
+    g.c = 0.5f * (mx + mn);
+    g.rho = 0.5f * (mx - mn);
+    g.rrho = 1.0f / g.rho;
+    g.nc = -(g.c * g.rrho);
+  }
+  return g;
+}
+
+// The normalised position of w (the codes of clip k are then
+// clamp(rint(fmaf(u, alpha_k, qmax/2)), 0, qmax), symmetric
+// clamp(rint(u * alpha_k), -Q, Q)).
+template <bool SYM>
+__device__ __forceinline__ float int_u(float w, const IntRange& g) {
+  return SYM ? w * g.rrho : __builtin_fmaf(w, g.rrho, g.nc);
+}
+
+// Clip-independent moments of the group: sum h, sum h w, sum h w^2 (fp64).
+struct IntMoments {
+  double Sv, Svw, Svww;
+  double thr;  // rank-deficiency threshold 1e-12 (sum h)^2 qmax^2
+  double rSv;  // 1 / sum h
+};
+
+// Best candidate so far of one lane: the key (score with the clip index in
+// its low bits), the emitted (s, z) and the score as fp32.
+struct IntBest {
+  double key;
+  float a, b, err;
+};
+
+__device__ __forceinline__ IntBest int_best_init() {
+  IntBest b;
+  b.key = __longlong_as_double(0x7ff0000000000000ll);  // +inf
+  b.a = b.b = b.err = 0.0f;
+  return b;
+}
+
+// Fit (Eq. ridgefit) and score (Eq. fisher-obj) of clip k from its
+// clip-dependent moments A0 = sum h q, A1 = sum h q^2, A2 = sum h q w
+// (symmetric: A0 unused, scale-only fit); keeps the better candidate.
+template <bool SYM, int QMAX>
+__device__ __forceinline__ void int_fit_score(const IntParams& p, int k, float f, const IntRange& g,
+                                              const IntMoments& mo, double A0, double A1, double A2,
+                                              IntBest& best) {
+  constexpr float kQmax = (float)QMAX;
+  if constexpr (SYM) {
+    // scale-only fit: s* = sum h q w / sum h q^2 (the RTN scale f m / Q
+    // when sum h q^2 = 0); the score of r = s q is Svww + s (s A1 - 2 A2)
+    const double a = (A1 == 0.0) ? (double)((f * g.mx) / kQmax) : div_f64(A2, A1, rcp_f64(A1));
+    const float af = round_param((float)a, p.param_dtype);
+    const double ad = (double)af;
+    const double score = mo.Svww + ad * (ad * A1 - 2.0 * A2);
+    const double key = make_key(score, k);
+    if (key < best.key) {
+      best.key = key;
+      best.a = af;
+      best.b = 0.0f;
+      best.err = (float)fmax(score, 0.0);
+    }
+  } else {
+    const double Sv = mo.Sv, Svw = mo.Svw;
+    const double D = Sv * A1 - A0 * A0;
+    double a, b;
+    if (Sv == 0.0 || D <= mo.thr) {
+      // no saliency, or all of it on one code: the slope is undetermined
+      // and the RTN step of this range is kept
+      const float fr = f * g.rho;
+      const float s_rtn = (2.0f * fr) / kQmax;
+      a = (double)s_rtn;
+      b = (Sv == 0.0) ? (double)(g.c - fr) : div_f64(Svw - a * A0, Sv, mo.rSv);
+    } else {
+      // quotients from v_rcp_f64 + Newton: within a few ulp of the IEEE
+      // quotient, far below the fp32 rounding of (s, z) that follows
+      a = div_f64(Sv * A2 - A0 * Svw, D, rcp_f64(D));
+      b = div_f64(Svw - a * A0, Sv, mo.rSv);
+    }
+    // fp32, then the deployed precision: the candidate is scored with the
+    // dequantiser that is emitted
+    const float af = round_param((float)a, p.param_dtype), bf = round_param((float)b, p.param_dtype);
+    const double ad = (double)af, bd = (double)bf;
+    // Eq. fisher-obj of the emitted dequantiser, expanded in fp64
+    const double score = mo.Svww + ad * (ad * A1 + 2.0 * bd * A0 - 2.0 * A2) + bd * (bd * Sv - 2.0 * Svw);
+    const double key = make_key(score, k);
+    if (key < best.key) {
+      best.key = key;
+      best.a = af;
+      best.b = bf;
+      best.err = (float)fmax(score, 0.0);
+    }
+  }
+}
+
+// Argmin over the group's L lanes (ties to the lowest clip index), winner
+// broadcast through `win` (this group's 4 floats of LDS), then the emit:
+// codes of f*, r = fmaf(s, q, z) in W's dtype (or fp32 r), (s, z) and the
+// optional diagnostics.
+template <bool W_BF16, int BITS, int G, bool SYM, bool SPREAD = false>
+__device__ __forceinline__ void int_finish(const IntParams& p, const IntMatrix& mtx, const WRegs<W_BF16>& wr,
+                                           const IntRange& g, double Sv, const IntBest& best, const float* s_alpha,
+                                           float* win, int j, int64_t gid, int64_t e0, bool active) {
+  constexpr int L = G / kIntN;
+  constexpr int QMAX = SYM ? (1 << (BITS - 1)) - 1 : (1 << BITS) - 1;
+  constexpr float kQmax = (float)QMAX;
+  constexpr float kQmin = SYM ? -(float)QMAX : 0.0f;
+  constexpr float kBeta = 0.5f * (float)QMAX;
+
+  const double gkey = Members<L, SPREAD>::min_f64(best.key);
+  const int kstar = key_index(gkey);
+  if (best.key == gkey) {  // exactly one lane of the group owns clip kstar
+    win[0] = best.a;
+    win[1] = best.b;
+    win[2] = best.err;
+  }
+  wave_lds_fence();
+  float a = win[0], b = win[1], errv = win[2];
+  const float alpha = s_alpha[kstar];
+  int kout = kstar;
+  if (g.constant) {  // every code 0, z = w in the deployed precision (exact at fp32)
+    a = 0.0f;
+    b = SYM ? 0.0f : round_param(g.mn, p.param_dtype);  // symmetric: an all-zero group
+    const double d = (double)b - (double)g.mn;
+    errv = (float)(Sv * d * d);
+    kout = 0;
+  }
+
+  uint32_t qi[kIntN];
+  float r[kIntN];
+#pragma unroll
+  for (int i = 0; i < kIntN; i++) {
+    if constexpr (SYM) {
+      const float ui = wr.get(i) * g.rrho;
+      // + 0.0f turns a rounded -0 into +0, so a zero code gives r = s * (+0)
+      float q = __builtin_amdgcn_fmed3f(__builtin_rintf(ui * alpha), kQmin, kQmax) + 0.0f;
+      if (g.constant) q = 0.0f;
+      qi[i] = (uint32_t)(int)q & ((1u << BITS) - 1u);  // two's complement in BITS bits
+      r[i] = a * q;
+    } else {
+      const float ui = __builtin_fmaf(wr.get(i), g.rrho, g.nc);
+      float x = __builtin_fmaf(ui, alpha, kBeta);
+      float q = __builtin_amdgcn_fmed3f(__builtin_rintf(x), 0.0f, kQmax);
+      if (g.constant) q = 0.0f;
+      qi[i] = (uint32_t)q;
+      r[i] = __builtin_fmaf(a, q, b);
+    }
+  }
+  if (!active) return;
+  if (mtx.r) {
+    if (W_BF16 || p.r_bf16)
+      store16<true>(mtx.r, e0, r);
+    else
+      store16<false>(mtx.r, e0, r);
+  }
+  if constexpr (BITS == 4) {
+    uint32_t lo = 0, hi = 0;
+#pragma unroll
+    for (int i = 0; i < 8; i++) {
+      lo |= qi[i] << (4 * i);
+      hi |= qi[8 + i] << (4 * i);
+    }
+    *reinterpret_cast<uint2*>(mtx.codes + gid * (G / 2) + j * 8) = make_uint2(lo, hi);
+  } else if constexpr (BITS == 2) {
+    uint32_t x = 0;
+#pragma unroll
+    for (int i = 0; i < kIntN; i++) x |= qi[i] << (2 * i);
+    *reinterpret_cast<uint32_t*>(mtx.codes + gid * (G / 4) + j * 4) = x;
+  } else {  // BITS == 3: 48 bits per lane at byte offset 6 j of the group's stream
+    uint64_t x = 0;
+#pragma unroll
+    for (int i = 0; i < kIntN; i++) x |= (uint64_t)qi[i] << (3 * i);
+    uint16_t* dst = reinterpret_cast<uint16_t*>(mtx.codes + gid * (3 * G / 8) + j * 6);
+    dst[0] = (uint16_t)x;
+    dst[1] = (uint16_t)(x >> 16);
+    dst[2] = (uint16_t)(x >> 32);
+  }
+  if (j == 0) {
+    mtx.scales[gid] = a;
+    if (mtx.zeros) mtx.zeros[gid] = b;
+    if (mtx.best_clip) mtx.best_clip[gid] = (uint8_t)kout;
+    if (mtx.err) mtx.err[gid] = errv;
+  }
+}
+
+}  // namespace quasar

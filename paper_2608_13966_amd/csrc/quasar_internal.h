@@ -42,18 +42,23 @@ struct BatchTable {
   MatrixSlot s[kMaxBatch];
 };
 
-// The slot workgroup `blk` works on (n > 1), with blk made local to it.  The
-// table is read straight from the kernel-argument segment (the parameter
-// block is a kernel's first argument): indexing the by-value copy with a
-// run-time slot would force that copy into scratch memory.
+// The parameter block as it sits in the kernel-argument segment (it is a
+// kernel's first argument).  Tables inside it that are indexed with run-time
+// or per-lane values are read from there: indexing the by-value copy would
+// force that copy into scratch memory.
+template <typename Params>
+__device__ __forceinline__ const Params* kernarg_params() {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return reinterpret_cast<const Params*>(__builtin_amdgcn_kernarg_segment_ptr());
+#else
+  return nullptr;  // the host pass never runs device code
+#endif
+}
+
+// The slot workgroup `blk` works on (n > 1), with blk made local to it.
 template <typename Params>
 __device__ __forceinline__ const MatrixSlot& batch_slot(int64_t& blk) {
-#if defined(__HIP_DEVICE_COMPILE__)
-  const Params* kp = reinterpret_cast<const Params*>(__builtin_amdgcn_kernarg_segment_ptr());
-#else
-  const Params* kp = nullptr;  // the host pass never runs device code
-#endif
-  const BatchTable& b = kp->batch;
+  const BatchTable& b = kernarg_params<Params>()->batch;
   int mi = 0;
 #pragma unroll 1
   while (mi + 1 < b.n && blk >= b.s[mi + 1].block0) mi++;
@@ -61,7 +66,43 @@ __device__ __forceinline__ const MatrixSlot& batch_slot(int64_t& blk) {
   return b.s[mi];
 }
 
-// Per-call parameters of the INT-b kernel (passed by value as the kernel argument).
+// Code-threshold tables of the binned INT-b kernel (int_cells_kernel.hip),
+// built by the host for one clip grid.  T(k, b), b = 1 .. NB, is the least
+// fp32 u whose code under clip k is at least q0 + b; t_0 < ... < t_{M-1} are
+// the distinct T(k, b) of all clips, and the cell of u is #{i : t_i <= u}.
+constexpr int kCellBuckets = 256;  // equal slices of u in [-1, 1]
+constexpr int kCellSteps = 16;     // >= NB (15 at most), bytes per clip in tp
+constexpr int kCellsPerLane = 15;  // most cells a lane scans (LDS <= 60 KB)
+constexpr int kCellsPerLaneAuto = 10;  // most for which the binned kernel is the default
+constexpr int kCellThr = 136;      // >= 128 (the search range) and >= M + 3
+struct IntCells {
+  int n_cells;  // M + 1; 0 = use the direct kernel
+  int cpl;      // cells per lane: the group's L lanes scan L * cpl >= M + 1 cells
+  int cmax;     // compares per weight, 1 .. 3 (the most thresholds in a bucket, capped)
+  int dense;    // some bucket holds more than three thresholds
+  // per bucket: base | mode << 8.  The cell of u in the bucket is base plus
+  // the number of t_base, t_base+1, t_base+2 at or below u.  mode 0: exact
+  // (at most three thresholds in the bucket); mode 1: exact unless u >= t_base+2;
+  // mode 2: exact unless u < t_base; otherwise a search over all t_i decides.
+  uint16_t bucket[kCellBuckets];
+  uint8_t tp[kMaxClips][kCellSteps];  // [k][b - 1]: first cell with u >= T(k, b)
+  float thr[kCellThr];                // t_0 .. t_{M-1}, then NaN
+};
+
+// Cells between consecutive groups of the binned kernel: the L * cpl cells a
+// group scans, rounded up to an odd count so that the same cell of different
+// groups lands in different LDS banks (a cell is 16 bytes, four banks).
+template <int L>
+__host__ __device__ constexpr int int_cells_stride(int cpl) { return (L * cpl) | 1; }
+
+// LDS of one workgroup of the binned kernel: 64 / L groups per wavefront,
+// h and h w in fp64 per cell.
+constexpr size_t int_cells_lds_bytes(int group, int cpl) {
+  return (size_t)(kThreads / 64) * (size_t)(64 / (group / 16)) *
+         (size_t)(group == 64 ? int_cells_stride<4>(cpl) : int_cells_stride<8>(cpl)) * 16;
+}
+
+// Per-call parameters of the INT-b kernels (passed by value as the kernel argument).
 struct IntParams {
   const void* W;        // [rows, cols] fp32 or bf16
   float* v;             // [rows, cols] fp32 saliency (overwritten with the EMA when g != NULL)
@@ -87,7 +128,9 @@ struct IntParams {
   AdamWConsts adam;
   int r_bf16;
   BatchTable batch;
+  IntCells cells;
 };
+static_assert(sizeof(IntParams) <= 4096, "kernel arguments are limited to 4 KB");
 
 // Per-call parameters of the NVFP4 kernels.
 struct Nvfp4Params {
@@ -152,6 +195,7 @@ constexpr int64_t rubin_units_per_block() { return kThreads / 64; }
 // Launchers (return the hipGetLastError() of the launches).
 hipError_t launch_rubin(const RubinParams& p, bool w_bf16, int ema_mode, hipStream_t s);
 hipError_t launch_int(const IntParams& p, int bits, int group, bool w_bf16, int ema_mode, hipStream_t s);
+hipError_t launch_int_cells(const IntParams& p, int bits, int group, bool w_bf16, int ema_mode, hipStream_t s);
 hipError_t launch_nvfp4(const Nvfp4Params& p, bool w_bf16, int ema_mode, hipStream_t s);
 // Tensor absmax of up to kMaxBatch matrices in one launch: matrix i (W[i],
 // n_chunks[i] 16-byte chunks) is covered by workgroups [block0[i], block0[i+1])

@@ -6,7 +6,7 @@ kernels behind ``quasar_reconstruct``.  Tensors are torch tensors on the GPU
 and a missing library raises instead of falling back.
 
 The functions ``quasar_reconstruct``, ``quasar_absmax``, ``quasar_check``, ``quasar_num_groups``,
-``quasar_codes_bytes``, ``quasar_workspace_bytes``, ``quasar_status_string`` and
+``quasar_int_path``, ``quasar_codes_bytes``, ``quasar_workspace_bytes``, ``quasar_status_string`` and
 ``quasar_version`` mirror the C entry points one to one; ``reconstruct`` is a
 convenience wrapper that allocates the outputs and calls ``quasar_reconstruct``.
 """
@@ -31,7 +31,7 @@ MAX_CLIPS = 16
 
 EXPORTS = ("quasar_reconstruct", "quasar_absmax", "quasar_check", "quasar_adamw_reconstruct", "quasar_adamw_check",
            "quasar_reconstruct_batch", "quasar_batch_check", "quasar_absmax_batch", "quasar_absmax_batch_check",
-           "quasar_num_groups", "quasar_codes_bytes",
+           "quasar_num_groups", "quasar_int_path", "quasar_codes_bytes",
            "quasar_workspace_bytes", "quasar_status_string", "quasar_version")
 MAX_BATCH = 16
 
@@ -101,6 +101,8 @@ def lib():
             L.quasar_absmax_batch_check.restype = C.c_int
             L.quasar_num_groups.argtypes = [dp]
             L.quasar_num_groups.restype = C.c_int64
+            L.quasar_int_path.argtypes = [dp]
+            L.quasar_int_path.restype = C.c_int
             L.quasar_codes_bytes.argtypes = [dp]
             L.quasar_codes_bytes.restype = C.c_size_t
             L.quasar_workspace_bytes.argtypes = [dp, C.c_int]
@@ -212,6 +214,10 @@ def quasar_absmax_batch_check(d: Descriptor, mats, amax_out) -> int:
 
 def quasar_num_groups(d: Descriptor) -> int:
     return int(lib().quasar_num_groups(d.ref))
+
+
+def quasar_int_path(d: Descriptor) -> int:
+    return int(lib().quasar_int_path(d.ref))
 
 
 def quasar_codes_bytes(d: Descriptor) -> int:

@@ -236,3 +236,47 @@ def test_absmax_batch_validation():
     assert Q.quasar_absmax_batch_check(nv, [_mat(cols=24)], [A]) == Q.ERR_SHAPE  # not whole 16-blocks
     assert Q.quasar_absmax_batch_check(nv, [_mat(rows=0)], [A]) == Q.ERR_SHAPE
     assert Q.quasar_absmax_batch_check(_int_desc(), [_mat()], [A]) == Q.ERR_FORMAT
+
+
+def _with_path(value, fn):
+    old = os.environ.get("QUASAR_INT_PATH")
+    if value is None:
+        os.environ.pop("QUASAR_INT_PATH", None)
+    else:
+        os.environ["QUASAR_INT_PATH"] = value
+    try:
+        return fn()
+    finally:
+        if old is None:
+            os.environ.pop("QUASAR_INT_PATH", None)
+        else:
+            os.environ["QUASAR_INT_PATH"] = old
+
+
+def test_int_path_choice():
+    """Which INT kernel serves a clip grid (host-only).  By default the binned
+    kernel takes grids with few code thresholds per group lane (INT2, INT3 with
+    8 clips) and the direct kernel the rest (INT4 with 8 clips: about 110
+    thresholds); QUASAR_INT_PATH=binned takes the binned kernel wherever its
+    tables fit, QUASAR_INT_PATH=direct never."""
+    grid8 = tuple(np.linspace(1.0, 0.65, 8).astype(np.float32))
+    grid12 = tuple(np.linspace(1.0, 0.5, 12).astype(np.float32))
+    grid16 = tuple(np.linspace(1.0, 0.3, 16).astype(np.float32))
+    default_binned = [dict(bits=2, group=64, clips=grid12), dict(bits=3, group=128, clips=grid8),
+                      dict(bits=2, group=128, clips=grid16), dict(fmt="int_sym", bits=3, group=128, clips=grid8)]
+    fit_only = [dict(bits=4, group=128, clips=grid8), dict(fmt="int_sym", bits=4, group=128, clips=grid8),
+                dict(bits=3, group=64, clips=grid8)]
+    never = [dict(bits=4, group=64, clips=grid8), dict(bits=4, group=128, clips=grid16)]
+    for kw in default_binned:
+        assert Q.quasar_int_path(_int_desc(**kw)) == 1, kw
+    for kw in fit_only + never:
+        assert Q.quasar_int_path(_int_desc(**kw)) == 0, kw
+    for kw in default_binned + fit_only:
+        assert _with_path("binned", lambda: Q.quasar_int_path(_int_desc(**kw))) == 1, kw
+    for kw in never:
+        assert _with_path("binned", lambda: Q.quasar_int_path(_int_desc(**kw))) == 0, kw
+    for kw in default_binned:
+        assert _with_path("direct", lambda: Q.quasar_int_path(_int_desc(**kw))) == 0, kw
+    assert Q.quasar_int_path(_int_desc(fmt="nvfp4")) == Q.ERR_FORMAT
+    assert Q.quasar_int_path(_int_desc(bits=5)) == Q.ERR_FORMAT
+    assert Q.quasar_int_path(_int_desc(clips=(1.0, 1.5))) == Q.ERR_ARG

@@ -30,9 +30,36 @@ def host(t):
     return None if t is None else synth.to_host(t)
 
 
+class int_path:
+    """Run the INT kernels through one path: "auto" (the library's choice),
+    "direct" (the per-clip kernel) or "binned" (the threshold-cell kernel
+    wherever its tables fit), set with QUASAR_INT_PATH."""
+
+    def __init__(self, path):
+        self.path = path
+
+    def __enter__(self):
+        self.old = os.environ.get("QUASAR_INT_PATH")
+        if self.path == "auto":
+            os.environ.pop("QUASAR_INT_PATH", None)
+        else:
+            os.environ["QUASAR_INT_PATH"] = self.path
+
+    def __exit__(self, *exc):
+        if self.old is None:
+            os.environ.pop("QUASAR_INT_PATH", None)
+        else:
+            os.environ["QUASAR_INT_PATH"] = self.old
+
+
 def run_case(name, rows, cols, seed, *, fmt="int", bits=4, group=128, clips=(1.0, 0.9, 0.8), w_bf16=True,
              ema=False, g_fp32=False, row_step=1, supply_amax=False, want_r=True, W=None, v=None, g=None,
-             weighting="h", param_dtype="fp32"):
+             weighting="h", param_dtype="fp32", paths=None):
+    """GPU against the oracle on the same bytes.  INT formats run through
+    every kernel that can serve the grid (the library's own choice first, then
+    the direct and the binned kernel where they differ from it) unless `paths`
+    says otherwise; each run starts from the same v (the fused EMA overwrites
+    it), and the outputs of the first run are returned."""
     dev = "cuda"
     if W is None:
         W, v, g = synth.gen_matrix(rows, cols, seed, w_bf16=w_bf16, ema=ema, device=dev)
@@ -45,26 +72,12 @@ def run_case(name, rows, cols, seed, *, fmt="int", bits=4, group=128, clips=(1.0
         amax = oracle.absmax(Wh)
         if supply_amax:
             amax_t = torch.tensor([amax, 0, 0, 0], dtype=torch.float32, device=dev)
-    print(f"[case] {name} shape={tuple(W.shape)} fmt={fmt} bits={bits} group={group} K={len(clips)} "
-          f"w={'bf16' if w_bf16 else 'f32'} ema={ema}", flush=True)
-    out = Q.reconstruct(W, v, g, fmt=fmt, bits=bits, group=group, clips=clips, tensor_amax=amax_t, want_r=want_r,
-                        weighting=weighting, param_dtype=param_dtype)
-    torch.cuda.synchronize()
     G = 16 if fmt == "nvfp4" else group
     nb = 4 if fmt == "nvfp4" else bits
     R, Cc = W.shape
     rows_idx = np.arange(0, R, row_step)
     gpr = Cc // G
     gidx = (rows_idx[:, None] * gpr + np.arange(gpr)[None, :]).ravel()
-    codes = out["codes"].cpu().numpy().reshape(R, Cc * nb // 8)[rows_idx].ravel()
-    gpu = {"codes": codes, "scales": out["scales"].cpu().numpy()[gidx],
-           "best_clip": out["best_clip"].cpu().numpy()[gidx], "err": out["err"].cpu().numpy()[gidx],
-           "r": host(out["r"])[rows_idx] if want_r else None}
-    if fmt == "nvfp4":
-        gpu["tensor_scale"] = out["tensor_scale"].cpu().numpy()[0]
-    else:
-        gpu["zeros"] = out["zeros"].cpu().numpy()[gidx]
-    v_gpu = host(v)[rows_idx] if g is not None else None
     o = oracle.reconstruct(Wh[rows_idx], vh[rows_idx], fmt=fmt, bits=bits, group=group, clips=clips,
                            g=None if gh is None else gh[rows_idx], beta2=0.999, tensor_amax=amax,
                            want_scores=True, want_diag=True, n_threads=THREADS, weighting=weighting,
@@ -74,13 +87,48 @@ def run_case(name, rows, cols, seed, *, fmt="int", bits=4, group=128, clips=(1.0
         h = (h * h).astype(np.float32)
     elif weighting == "none":
         h = np.ones_like(h)
-    fails, st = _parity.compare(fmt=fmt, bits=bits, group=group, W=Wh[rows_idx], h=h, o=o, gpu=gpu,
-                                v_out_gpu=v_gpu)
-    record(name, st)
-    assert not fails, "\n".join(fails)
-    # exceptions are rare by construction
-    assert st["near_tie"] + st["near_e4m3"] <= max(2, 0.001 * st["groups"]), dict(st)
-    return out, o
+    if paths is None:
+        paths = ("auto",)
+        if fmt in ("int", "int_sym"):
+            d = Q.Descriptor(R, Cc, fmt=fmt, bits=bits, group=group, clips=clips)
+            kern = {}
+            for pth in ("auto", "direct", "binned"):
+                with int_path(pth):
+                    kern[pth] = Q.quasar_int_path(d)
+            paths = ("auto",) + tuple(pth for pth in ("direct", "binned") if kern[pth] != kern["auto"])
+    result = None
+    v0 = v.clone() if len(paths) > 1 else None
+    for path in paths:
+        vv = v if result is None else v0.clone()  # the first run updates the caller's v, as a single call does
+        with int_path(path):
+            used = ""
+            if fmt in ("int", "int_sym"):
+                d = Q.Descriptor(R, Cc, fmt=fmt, bits=bits, group=group, clips=clips,
+                                 w_dtype=Q.BF16 if W.dtype == torch.bfloat16 else Q.F32)
+                used = " kernel=" + ("binned" if Q.quasar_int_path(d) == 1 else "direct")
+            print(f"[case] {name} shape={tuple(W.shape)} fmt={fmt} bits={bits} group={group} K={len(clips)} "
+                  f"w={'bf16' if w_bf16 else 'f32'} ema={ema} path={path}{used}", flush=True)
+            out = Q.reconstruct(W, vv, g, fmt=fmt, bits=bits, group=group, clips=clips, tensor_amax=amax_t,
+                                want_r=want_r, weighting=weighting, param_dtype=param_dtype)
+            torch.cuda.synchronize()
+        codes = out["codes"].cpu().numpy().reshape(R, Cc * nb // 8)[rows_idx].ravel()
+        gpu = {"codes": codes, "scales": out["scales"].cpu().numpy()[gidx],
+               "best_clip": out["best_clip"].cpu().numpy()[gidx], "err": out["err"].cpu().numpy()[gidx],
+               "r": host(out["r"])[rows_idx] if want_r else None}
+        if fmt == "nvfp4":
+            gpu["tensor_scale"] = out["tensor_scale"].cpu().numpy()[0]
+        else:
+            gpu["zeros"] = out["zeros"].cpu().numpy()[gidx]
+        v_gpu = host(vv)[rows_idx] if g is not None else None
+        fails, st = _parity.compare(fmt=fmt, bits=bits, group=group, W=Wh[rows_idx], h=h, o=o, gpu=gpu,
+                                    v_out_gpu=v_gpu)
+        record(name if path == "auto" else f"{name}.{path}", st)
+        assert not fails, f"path {path}:\n" + "\n".join(fails)
+        # exceptions are rare by construction
+        assert st["near_tie"] + st["near_e4m3"] <= max(2, 0.001 * st["groups"]), dict(st)
+        if result is None:
+            result = (out, o)
+    return result
 
 
 # --------------------------------------------------------------------------- configs
