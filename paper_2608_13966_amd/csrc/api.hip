@@ -265,10 +265,12 @@ int int_code(float u, float alpha, int qmax, bool sym) {
   return (int)fminf(fmaxf(x, 0.0f), (float)qmax);
 }
 
-// The bucket of u in the binned kernel, in its fp32 recipe.
+// The bucket of a finite u in the binned kernel, in its fp32 recipe:
+// clamp(floor(u * 128), -128, 127) + 128 (u * 128 is exact), so a bucket
+// boundary falls exactly at u = 0.
 int cell_bucket(float u) {
   const float h = 0.5f * (float)quasar::kCellBuckets;
-  return (int)fminf(fmaxf(fmaf(u, h, h), 0.0f), (float)(quasar::kCellBuckets - 1));
+  return (int)fminf(fmaxf(floorf(u * h), -h), h - 1.0f) + quasar::kCellBuckets / 2;
 }
 
 // The binned INT kernel's tables for this clip grid (int_cells_kernel.hip):
@@ -277,13 +279,15 @@ int cell_bucket(float u) {
 // and +inf (the highest).  Leaves n_cells = 0 -- the direct kernel runs --
 // when the cells do not fit the kernel's LDS budget, when a lane would scan
 // more than kCellsPerLaneAuto cells (the binned kernel's per-cell LDS work
-// then outweighs the per-clip work it saves: INT4 grids), or when
-// QUASAR_INT_PATH=direct is set.  QUASAR_INT_PATH=binned takes the binned
-// kernel wherever its tables fit.
+// then outweighs the per-clip work it saves: INT4 grids), when a bucket
+// needs more than three compares, or when QUASAR_INT_PATH=direct is set.
+// QUASAR_INT_PATH=binned takes the binned kernel wherever its tables fit.
 //
-// A bucket with more than three thresholds (every clip has one just below
-// u = 0, where the fp32 code rounding ties at qmax/2) takes the three at the
-// end that leaves the shorter stretch of the bucket to the exact search.
+// With odd qmax every clip has a threshold just below u = 0, where the fp32
+// code rounding ties at qmax/2: T(k, (qmax+1)/2) lies in (-2^-20, 0).  These
+// tie thresholds are merged into one cell boundary at their least value;
+// a weight between the least and the greatest of them (the unsafe interval;
+// a few in ten million) makes the kernel sum its group's moments directly.
 void int_cells(quasar::IntParams& p, int K, int bits, bool sym, int group) {
   memset(&p.cells, 0, sizeof(p.cells));
   const char* force = getenv("QUASAR_INT_PATH");
@@ -292,8 +296,10 @@ void int_cells(quasar::IntParams& p, int K, int bits, bool sym, int group) {
   const int qmax = sym ? (1 << (bits - 1)) - 1 : (1 << bits) - 1;
   const int q0 = sym ? -qmax : 0;
   const int nb = sym ? 2 * qmax : qmax;
+  const int tie = sym ? 0 : (qmax + 1) / 2;  // step b whose thresholds are the tie cluster
   float t[quasar::kMaxClips * quasar::kCellSteps];
   int n = 0;
+  float ulo = INFINITY, uhi = -INFINITY;
   for (int k = 0; k < K; k++) {
     for (int b = 1; b <= nb; b++) {
       uint32_t lo = f32_order_key(-INFINITY), hi = f32_order_key(INFINITY);
@@ -305,48 +311,48 @@ void int_cells(quasar::IntParams& p, int K, int bits, bool sym, int group) {
           lo = mid;
       }
       t[n++] = f32_from_order_key(hi);
+      if (b == tie) {
+        ulo = fminf(ulo, t[n - 1]);
+        uhi = fmaxf(uhi, t[n - 1]);
+      }
     }
   }
+  const bool merge = tie > 0 && ulo < uhi;  // more than one distinct tie threshold
+  if (tie > 0 && !(ulo > -0x1p-20f && uhi < 0.0f)) return;
   float srt[quasar::kMaxClips * quasar::kCellSteps];
-  memcpy(srt, t, sizeof(float) * n);
-  std::sort(srt, srt + n);
-  const int m = (int)(std::unique(srt, srt + n) - srt);
+  int m = 0;
+  for (int i = 0; i < n; i++) srt[m++] = (merge && t[i] >= ulo && t[i] <= uhi) ? ulo : t[i];
+  std::sort(srt, srt + m);
+  m = (int)(std::unique(srt, srt + m) - srt);
+  if (merge) {
+    // no other threshold may fall inside the merged span
+    for (int i = 0; i < m; i++)
+      if (srt[i] > ulo && srt[i] <= uhi) return;
+  }
   const int L = group / 16;
   const int cpl = (m + 1 + L - 1) / L;
   if (cpl > quasar::kCellsPerLane || m + 3 > quasar::kCellThr || m > 127) return;
   if (!any_fit && cpl > quasar::kCellsPerLaneAuto) return;
   int cnt[quasar::kCellBuckets] = {0};
+  int cmax = 1, below = 0;
   for (int i = 0; i < m; i++) cnt[cell_bucket(srt[i])]++;
-  int cmax = 1, below = 0, dense = 0;
-  const double width = 2.0 / quasar::kCellBuckets;
   for (int b = 0; b < quasar::kCellBuckets; b++) {
-    int base = below, mode = 0;
-    if (cnt[b] > 3) {
-      // the stretch of the bucket each anchoring leaves to the search
-      const double b_lo = -1.0 + width * b, b_hi = b_lo + width;
-      const double up = b_hi - (double)srt[below + 2];          // mode 1: u >= t_base+2
-      const double down = (double)srt[below + cnt[b] - 3] - b_lo;  // mode 2: u < t_base
-      if (up <= down) {
-        mode = 1;
-      } else {
-        mode = 2;
-        base = below + cnt[b] - 3;
-      }
-      dense = 1;
-    }
-    p.cells.bucket[b] = (uint16_t)(base | (mode << 8));
+    cmax = std::max(cmax, cnt[b]);
+    p.cells.base[b] = (uint8_t)below;
     below += cnt[b];
-    cmax = std::max(cmax, std::min(cnt[b], 3));
   }
+  if (cmax > 3) return;
   for (int k = 0; k < K; k++)
     for (int b = 1; b <= nb; b++) {
-      const float tb = t[k * nb + b - 1];
+      float tb = t[k * nb + b - 1];
+      if (merge && tb >= ulo && tb <= uhi) tb = ulo;
       p.cells.tp[k][b - 1] = (uint8_t)((std::lower_bound(srt, srt + m, tb) - srt) + 1);
     }
   for (int i = 0; i < quasar::kCellThr; i++) p.cells.thr[i] = i < m ? srt[i] : NAN;
   p.cells.cpl = cpl;
   p.cells.cmax = cmax;
-  p.cells.dense = dense;
+  p.cells.unsafe_lo = merge ? ulo : INFINITY;
+  p.cells.unsafe_hi = merge ? uhi : INFINITY;
   p.cells.n_cells = m + 1;
 }
 

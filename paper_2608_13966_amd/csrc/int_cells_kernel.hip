@@ -30,6 +30,8 @@
 // solves and scores them exactly as the direct form does (int_common.h).
 // The emitted codes are recomputed from u with the fp32 recipe, so they are
 // bit-identical to the direct form's.
+#include <type_traits>
+
 #include "device_common.h"
 #include "int_common.h"
 #include "quasar_internal.h"
@@ -54,18 +56,28 @@ __device__ __forceinline__ double members_excl_suffix(double x, int j) {
   return e;
 }
 
-// An exact integer held as a double with |x| < 2^51, as int64: x + 1.5 2^52
-// lies in [2^52, 2^53), where the bit pattern is that of 1.5 2^52 plus x, and
-// the low word of 1.5 2^52 is zero.
+// x * scale rounded to an integer (ties to even), as int64, for
+// |x * scale| < 2^51: x * scale + 1.5 2^52 (one fma, one rounding) lies in
+// [2^52, 2^53), where its bit pattern is that of 1.5 2^52 plus the integer,
+// and the low word of 1.5 2^52 is zero.
 constexpr double kMagic = 6755399441055744.0;  // 1.5 * 2^52
 constexpr uint32_t kMagicHi = 0x43380000u;
-__device__ __forceinline__ uint64_t round_to_i64(double x) {
-  const uint64_t b = (uint64_t)__double_as_longlong(x + kMagic);  // rounds x to an integer (ties to even)
-  return b - ((uint64_t)kMagicHi << 32);
+__device__ __forceinline__ uint64_t scaled_to_i64(double x, double scale) {
+  const uint64_t b = (uint64_t)__double_as_longlong(__builtin_fma(x, scale, kMagic));
+  return ((uint64_t)((uint32_t)(b >> 32) - kMagicHi) << 32) | (uint32_t)b;
 }
 // ... and back (exact for |n| < 2^51)
 __device__ __forceinline__ double i64_to_double(uint64_t n) {
   return __longlong_as_double((long long)(n + ((uint64_t)kMagicHi << 32))) - kMagic;
+}
+
+// The bucket of u: clamp(floor(u * 128), -128, 127) + 128 (u * 128 is exact,
+// so a boundary falls exactly at u = 0); any u, NaN included, gives an index
+// in [0, 256).
+__device__ __forceinline__ int cell_bucket(float u) {
+  int f;
+  asm("v_cvt_flr_i32_f32 %0, %1" : "=v"(f) : "v"(u * (0.5f * (float)kCellBuckets)));
+  return min(max(f, -kCellBuckets / 2), kCellBuckets / 2 - 1) + kCellBuckets / 2;
 }
 
 template <bool W_BF16, int EMA, int BITS, int G, bool SYM>
@@ -76,12 +88,13 @@ __global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
   constexpr int NB = SYM ? 2 * QMAX : QMAX;  // code steps per clip
   constexpr int OWN = kMaxClips / L;         // clips a lane may own
   constexpr int CPL = kCellsPerLane;         // most cells per lane
-  constexpr float kHalfBuckets = 0.5f * (float)kCellBuckets;
+  constexpr float kQmax = (float)QMAX;
+  constexpr float kQmin = SYM ? -(float)QMAX : 0.0f;
+  constexpr float kBeta = 0.5f * (float)QMAX;
   static_assert(kThreads == kCellBuckets && kThreads == kMaxClips * kCellSteps, "one table entry per thread");
 
   extern __shared__ double s_hist[];  // [wave][group slot][cell][h, h w]
   __shared__ uint4 s_bucket[kCellBuckets];
-  __shared__ float s_thr[128];
   __shared__ uint8_t s_tp[kMaxClips * kCellSteps];
   __shared__ float s_alpha[kMaxClips], s_clip[kMaxClips];
   __shared__ float s_win[kThreads / 64][GPW][4];
@@ -94,11 +107,9 @@ __global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
 
   {  // the tables, read from the kernel-argument segment with per-lane indices
     const IntCells& cl = kernarg_params<IntParams>()->cells;
-    const uint32_t e = cl.bucket[tid];
-    const int c = (int)(e & 0xffu);
-    s_bucket[tid] = make_uint4(e, as_u32(cl.thr[c]), as_u32(cl.thr[c + 1]), as_u32(cl.thr[c + 2]));
+    const int c = cl.base[tid];
+    s_bucket[tid] = make_uint4((uint32_t)c, as_u32(cl.thr[c]), as_u32(cl.thr[c + 1]), as_u32(cl.thr[c + 2]));
     s_tp[tid] = (&cl.tp[0][0])[tid];
-    if (tid < 128) s_thr[tid] = cl.thr[tid];
   }
   if (tid < kMaxClips) {
     s_alpha[tid] = p.alpha[tid];
@@ -130,46 +141,42 @@ __global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
   wave_lds_fence();
 
   // ---- the cell of every weight (four bucket reads in flight at a time) -----
-  const int cmax = p.cells.cmax;
-  const bool dense = p.cells.dense != 0;
+  // Thresholds outside u's bucket lie on the far side of u and the table's
+  // padding is NaN, so cmax compares never pass the last threshold.
+  const float ulo = p.cells.unsafe_lo, uhi = p.cells.unsafe_hi;
+  bool unsafe = false;
   uint32_t cells[N / 4];  // four cells per register, one byte each
+  auto bin = [&](auto cmax_tag) {
+    constexpr int C = decltype(cmax_tag)::value;
 #pragma unroll
-  for (int c4 = 0; c4 < N / 4; c4++) {
-    float u[4];
-    uint4 e[4];
+    for (int c4 = 0; c4 < N / 4; c4++) {
+      float u[4];
+      uint4 e[4];
 #pragma unroll
-    for (int t = 0; t < 4; t++) {
-      u[t] = int_u<SYM>(wr.get(4 * c4 + t), rg);
-      // bucket of u (monotone in u; a NaN u lands in bucket 0)
-      const float x =
-          fminf(fmaxf(__builtin_fmaf(u[t], kHalfBuckets, kHalfBuckets), 0.0f), (float)(kCellBuckets - 1));
-      e[t] = s_bucket[(int)x];
-    }
-    uint32_t packed = 0;
-#pragma unroll
-    for (int t = 0; t < 4; t++) {
-      // thresholds outside the bucket lie on the far side of u, and the
-      // table's padding is NaN, so the cell never passes the last threshold
-      int cell = (int)(e[t].x & 0xffu) + (u[t] >= as_f32(e[t].y) ? 1 : 0);
-      if (cmax > 1) cell += (u[t] >= as_f32(e[t].z) ? 1 : 0);
-      if (cmax > 2) cell += (u[t] >= as_f32(e[t].w) ? 1 : 0);
-      if (dense) {
-        // a bucket with more than three thresholds: outside the stretch its
-        // three compares cover, count every t_i <= u (t_127 is NaN)
-        const uint32_t mode = e[t].x >> 8;
-        if ((mode == 1 && u[t] >= as_f32(e[t].w)) || (mode == 2 && u[t] < as_f32(e[t].y))) {
-          int lo = 0;
-#pragma unroll
-          for (int step = 64; step >= 1; step >>= 1)
-            if (s_thr[lo + step - 1] <= u[t]) lo += step;
-          cell = lo;
-        }
+      for (int t = 0; t < 4; t++) {
+        u[t] = int_u<SYM>(wr.get(4 * c4 + t), rg);
+        e[t] = s_bucket[cell_bucket(u[t])];
       }
-      packed |= (uint32_t)cell << (8 * t);
+      uint32_t packed = 0;
+#pragma unroll
+      for (int t = 0; t < 4; t++) {
+        uint32_t cell = e[t].x + (u[t] >= as_f32(e[t].y) ? 1u : 0u);
+        if constexpr (C > 1) cell += (u[t] >= as_f32(e[t].z) ? 1u : 0u);
+        if constexpr (C > 2) cell += (u[t] >= as_f32(e[t].w) ? 1u : 0u);
+        packed |= cell << (8 * t);
+        unsafe |= (u[t] >= ulo) & (u[t] <= uhi);
+      }
+      cells[c4] = packed;
+      __builtin_amdgcn_sched_barrier(0);
     }
-    cells[c4] = packed;
-    __builtin_amdgcn_sched_barrier(0);
-  }
+  };
+  const int cmax = p.cells.cmax;
+  if (cmax == 1)
+    bin(std::integral_constant<int, 1>{});
+  else if (cmax == 2)
+    bin(std::integral_constant<int, 2>{});
+  else
+    bin(std::integral_constant<int, 3>{});
 
   // ---- h and h w of every weight into its cell, as exact integers --------------
   // h and h w are scaled by powers of two that bring the group's largest |h|
@@ -196,8 +203,8 @@ __global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
     const double VW = V * Wd;
     Svww = __builtin_fma(VW, Wd, Svww);
     uint64_t* c64 = reinterpret_cast<uint64_t*>(hist + 2 * cell);
-    __hip_atomic_fetch_add(c64, round_to_i64(V * sh), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
-    __hip_atomic_fetch_add(c64 + 1, round_to_i64(VW * shw), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+    __hip_atomic_fetch_add(c64, scaled_to_i64(V, sh), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+    __hip_atomic_fetch_add(c64 + 1, scaled_to_i64(VW, shw), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
   }
   wave_lds_fence();
 
@@ -214,14 +221,14 @@ __global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
         tw += i64_to_double(t.y);
       }
     }
-    double eh = members_excl_suffix<L>(th, j), ew = members_excl_suffix<L>(tw, j);
+    double eh2 = members_excl_suffix<L>(th, j), ew2 = members_excl_suffix<L>(tw, j);
 #pragma unroll
     for (int i = CPL - 1; i >= 0; i--) {
       if (i < cpl) {
         const ulonglong2 t = *reinterpret_cast<const ulonglong2*>(mine + 2 * i);
-        eh += i64_to_double(t.x);
-        ew += i64_to_double(t.y);
-        *reinterpret_cast<double2*>(mine + 2 * i) = make_double2(eh, ew);
+        eh2 += i64_to_double(t.x);
+        ew2 += i64_to_double(t.y);
+        *reinterpret_cast<double2*>(mine + 2 * i) = make_double2(eh2, ew2);
       }
     }
   }
@@ -239,29 +246,78 @@ __global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
   mo.thr = 1e-12 * mo.Sv * mo.Sv * (double)QMAX * (double)QMAX;
   mo.rSv = rcp_f64(mo.Sv);
 
+  // ---- a weight among merged thresholds (rare): its group's moments are summed
+  // directly for every clip and left in the group's cells, 3 per clip ---------
+  const bool group_unsafe = M::max(unsafe ? 1.0f : 0.0f) > 0.0f;
+  if (group_unsafe) {
+    // the saliencies again (v' when this kernel stored it: the fence makes
+    // this lane's own stores visible to its loads; an inactive lane's group
+    // is recomputed but never stored)
+    __threadfence();
+    float hv[N];
+    load16<false>(mtx.v, e0, hv);
+    if (p.weighting != 0) {
+#pragma unroll
+      for (int i = 0; i < N; i++) hv[i] = weight_of(hv[i], p.weighting);
+    }
+    wave_lds_fence();
+#pragma unroll 1
+    for (int k = 0; k < K; k++) {
+      const float al = s_alpha[k];
+      double a0 = 0.0, a1 = 0.0, a2 = 0.0;
+#pragma unroll
+      for (int i = 0; i < N; i++) {
+        const float w = wr.get(i);
+        const float u = int_u<SYM>(w, rg);
+        const float x = SYM ? u * al : __builtin_fmaf(u, al, kBeta);
+        const double Q = (double)__builtin_amdgcn_fmed3f(__builtin_rintf(x), kQmin, kQmax);
+        const double V = (double)hv[i];
+        const double VQ = V * Q;
+        a0 += VQ;
+        a1 = __builtin_fma(VQ, Q, a1);
+        a2 = __builtin_fma(V * (double)w, Q, a2);
+      }
+      a0 = M::sum(a0);
+      a1 = M::sum(a1);
+      a2 = M::sum(a2);
+      if (j == 0) {
+        hist[3 * k] = a0;
+        hist[3 * k + 1] = a1;
+        hist[3 * k + 2] = a2;
+      }
+    }
+    wave_lds_fence();
+  }
+
   // ---- the clips this lane owns: moments from NB suffix sums, fit, score ------
   IntBest best = int_best_init();
 #pragma unroll 1
   for (int t = 0; t < OWN; t++) {
     const int k = j + L * t;
     if (k < K) {
-      const uint4 tw4 = *reinterpret_cast<const uint4*>(s_tp + k * kCellSteps);
-      const uint32_t tw[4] = {tw4.x, tw4.y, tw4.z, tw4.w};
       double A0 = 0.0, A1 = 0.0, A2 = 0.0;
+      if (group_unsafe) {
+        A0 = hist[3 * k];
+        A1 = hist[3 * k + 1];
+        A2 = hist[3 * k + 2];
+      } else {
+        const uint4 tw4 = *reinterpret_cast<const uint4*>(s_tp + k * kCellSteps);
+        const uint32_t tw[4] = {tw4.x, tw4.y, tw4.z, tw4.w};
 #pragma unroll
-      for (int b = 1; b <= NB; b++) {
-        const int c = (int)((tw[(b - 1) >> 2] >> (8 * ((b - 1) & 3))) & 0xffu);
-        const double2 s = *reinterpret_cast<const double2*>(hist + 2 * c);
-        A0 += s.x;
-        A1 = __builtin_fma((double)(2 * b - 1), s.x, A1);
-        A2 += s.y;
-      }
-      A0 *= rsh;
-      A1 *= rsh;
-      A2 *= rshw;
-      if constexpr (SYM) {  // q = n - Q
-        A1 = __builtin_fma((double)QMAX * (double)QMAX, mo.Sv, __builtin_fma(-2.0 * (double)QMAX, A0, A1));
-        A2 = __builtin_fma(-(double)QMAX, mo.Svw, A2);
+        for (int b = 1; b <= NB; b++) {
+          const int c = (int)((tw[(b - 1) >> 2] >> (8 * ((b - 1) & 3))) & 0xffu);
+          const double2 s = *reinterpret_cast<const double2*>(hist + 2 * c);
+          A0 += s.x;
+          A1 = __builtin_fma((double)(2 * b - 1), s.x, A1);
+          A2 += s.y;
+        }
+        A0 *= rsh;
+        A1 *= rsh;
+        A2 *= rshw;
+        if constexpr (SYM) {  // q = n - Q
+          A1 = __builtin_fma((double)QMAX * (double)QMAX, mo.Sv, __builtin_fma(-2.0 * (double)QMAX, A0, A1));
+          A2 = __builtin_fma(-(double)QMAX, mo.Svw, A2);
+        }
       }
       int_fit_score<SYM, QMAX>(p, k, s_clip[k], rg, mo, A0, A1, A2, best);
     }
@@ -276,8 +332,8 @@ hipError_t launch_g(const IntParams& p, hipStream_t s) {
   constexpr int64_t groups_per_block = int_units_per_block(G);
   const int64_t blocks =
       p.batch.n > 1 ? p.batch.total_blocks : (p.n_groups + groups_per_block - 1) / groups_per_block;
-  const dim3 grid((unsigned)blocks), block(kThreads);
   const size_t lds = int_cells_lds_bytes(G, p.cells.cpl);
+  const dim3 grid((unsigned)blocks), block(kThreads);
   if (p.symmetric) {
     if constexpr (EMA <= 2) {
       hipLaunchKernelGGL((int_cells_kernel<W_BF16, EMA, BITS, G, true>), grid, block, lds, s, p);

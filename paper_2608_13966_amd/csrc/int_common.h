@@ -290,54 +290,55 @@ __device__ __forceinline__ void int_finish(const IntParams& p, const IntMatrix& 
     kout = 0;
   }
 
-  uint32_t qi[kIntN];
-  float r[kIntN];
+  // two chunks of 8 weights: codes and r of a chunk are formed and its r
+  // stored before the next chunk, which keeps few values live at once
+  uint64_t bits = 0;  // this lane's 16 codes, code i at bits [BITS i, BITS i + BITS)
 #pragma unroll
-  for (int i = 0; i < kIntN; i++) {
-    if constexpr (SYM) {
-      const float ui = wr.get(i) * g.rrho;
-      // + 0.0f turns a rounded -0 into +0, so a zero code gives r = s * (+0)
-      float q = __builtin_amdgcn_fmed3f(__builtin_rintf(ui * alpha), kQmin, kQmax) + 0.0f;
-      if (g.constant) q = 0.0f;
-      qi[i] = (uint32_t)(int)q & ((1u << BITS) - 1u);  // two's complement in BITS bits
-      r[i] = a * q;
-    } else {
-      const float ui = __builtin_fmaf(wr.get(i), g.rrho, g.nc);
-      float x = __builtin_fmaf(ui, alpha, kBeta);
-      float q = __builtin_amdgcn_fmed3f(__builtin_rintf(x), 0.0f, kQmax);
-      if (g.constant) q = 0.0f;
-      qi[i] = (uint32_t)q;
-      r[i] = __builtin_fmaf(a, q, b);
+  for (int h = 0; h < 2; h++) {
+    float r[8];
+#pragma unroll
+    for (int t = 0; t < 8; t++) {
+      const int i = 8 * h + t;
+      uint32_t qi;
+      if constexpr (SYM) {
+        const float ui = wr.get(i) * g.rrho;
+        // + 0.0f turns a rounded -0 into +0, so a zero code gives r = s * (+0)
+        float q = __builtin_amdgcn_fmed3f(__builtin_rintf(ui * alpha), kQmin, kQmax) + 0.0f;
+        if (g.constant) q = 0.0f;
+        qi = (uint32_t)(int)q & ((1u << BITS) - 1u);  // two's complement in BITS bits
+        r[t] = a * q;
+      } else {
+        const float ui = __builtin_fmaf(wr.get(i), g.rrho, g.nc);
+        float x = __builtin_fmaf(ui, alpha, kBeta);
+        float q = __builtin_amdgcn_fmed3f(__builtin_rintf(x), 0.0f, kQmax);
+        if (g.constant) q = 0.0f;
+        qi = (uint32_t)q;
+        r[t] = __builtin_fmaf(a, q, b);
+      }
+      bits |= (uint64_t)qi << (BITS * i);
+    }
+    if (active && mtx.r) {
+      if (W_BF16 || p.r_bf16) {
+        uint16_t* pr = reinterpret_cast<uint16_t*>(mtx.r) + e0 + 8 * h;
+        st128(pr, make_uint4(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]), pack_bf16x2(r[4], r[5]),
+                             pack_bf16x2(r[6], r[7])));
+      } else {
+        float* pr = reinterpret_cast<float*>(mtx.r) + e0 + 8 * h;
+        st128(pr, make_uint4(as_u32(r[0]), as_u32(r[1]), as_u32(r[2]), as_u32(r[3])));
+        st128(pr + 4, make_uint4(as_u32(r[4]), as_u32(r[5]), as_u32(r[6]), as_u32(r[7])));
+      }
     }
   }
   if (!active) return;
-  if (mtx.r) {
-    if (W_BF16 || p.r_bf16)
-      store16<true>(mtx.r, e0, r);
-    else
-      store16<false>(mtx.r, e0, r);
-  }
   if constexpr (BITS == 4) {
-    uint32_t lo = 0, hi = 0;
-#pragma unroll
-    for (int i = 0; i < 8; i++) {
-      lo |= qi[i] << (4 * i);
-      hi |= qi[8 + i] << (4 * i);
-    }
-    *reinterpret_cast<uint2*>(mtx.codes + gid * (G / 2) + j * 8) = make_uint2(lo, hi);
+    *reinterpret_cast<uint2*>(mtx.codes + gid * (G / 2) + j * 8) = make_uint2((uint32_t)bits, (uint32_t)(bits >> 32));
   } else if constexpr (BITS == 2) {
-    uint32_t x = 0;
-#pragma unroll
-    for (int i = 0; i < kIntN; i++) x |= qi[i] << (2 * i);
-    *reinterpret_cast<uint32_t*>(mtx.codes + gid * (G / 4) + j * 4) = x;
+    *reinterpret_cast<uint32_t*>(mtx.codes + gid * (G / 4) + j * 4) = (uint32_t)bits;
   } else {  // BITS == 3: 48 bits per lane at byte offset 6 j of the group's stream
-    uint64_t x = 0;
-#pragma unroll
-    for (int i = 0; i < kIntN; i++) x |= (uint64_t)qi[i] << (3 * i);
     uint16_t* dst = reinterpret_cast<uint16_t*>(mtx.codes + gid * (3 * G / 8) + j * 6);
-    dst[0] = (uint16_t)x;
-    dst[1] = (uint16_t)(x >> 16);
-    dst[2] = (uint16_t)(x >> 32);
+    dst[0] = (uint16_t)bits;
+    dst[1] = (uint16_t)(bits >> 16);
+    dst[2] = (uint16_t)(bits >> 32);
   }
   if (j == 0) {
     mtx.scales[gid] = a;

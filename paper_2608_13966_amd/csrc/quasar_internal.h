@@ -78,13 +78,15 @@ constexpr int kCellThr = 136;      // >= 128 (the search range) and >= M + 3
 struct IntCells {
   int n_cells;  // M + 1; 0 = use the direct kernel
   int cpl;      // cells per lane: the group's L lanes scan L * cpl >= M + 1 cells
-  int cmax;     // compares per weight, 1 .. 3 (the most thresholds in a bucket, capped)
-  int dense;    // some bucket holds more than three thresholds
-  // per bucket: base | mode << 8.  The cell of u in the bucket is base plus
-  // the number of t_base, t_base+1, t_base+2 at or below u.  mode 0: exact
-  // (at most three thresholds in the bucket); mode 1: exact unless u >= t_base+2;
-  // mode 2: exact unless u < t_base; otherwise a search over all t_i decides.
-  uint16_t bucket[kCellBuckets];
+  int cmax;     // compares per weight, 1 .. 3
+  // u in [unsafe_lo, unsafe_hi] (closed) lies among merged thresholds, where
+  // the cell does not fix every clip's code; a group with such a weight has
+  // its moments summed directly (empty interval: +inf, +inf)
+  float unsafe_lo, unsafe_hi;
+  // per bucket b = clamp(floor(128 u), -128, 127) + 128: for u in the
+  // bucket the cell is base plus the number of t_base .. t_base+cmax-1 at
+  // or below u
+  uint8_t base[kCellBuckets];
   uint8_t tp[kMaxClips][kCellSteps];  // [k][b - 1]: first cell with u >= T(k, b)
   float thr[kCellThr];                // t_0 .. t_{M-1}, then NaN
 };

@@ -294,6 +294,34 @@ def test_degenerate_groups():
              v=torch.ones(2, 64, device="cuda"), w_bf16=False)
 
 
+def test_weights_among_tie_thresholds():
+    """For odd qmax every clip has a code threshold just below u = 0 (where
+    the fp32 rounding of the code ties at qmax/2), all within about 3e-8 of
+    each other.  The binned kernel merges them into one cell boundary and sums
+    a group directly when one of its weights lies between them.  Here groups
+    with c = 0 and rho = 1 (so u = w) hold weights spread over and around that
+    span, next to ordinary groups in the same wavefronts, with the fused EMA.
+    The GPU must match the oracle in both kernels."""
+    torch.manual_seed(11)
+    rows, cols = 24, 384
+    W = (torch.randn(rows, cols) * 0.3).float()
+    v = torch.rand(rows, cols).float() + 0.01
+    tie = -torch.linspace(3.2e-8, 1.7e-8, 62)
+    for r in range(0, rows, 3):
+        c0 = 64 * (r % 6)
+        W[r, c0] = -1.0
+        W[r, c0 + 1] = 1.0
+        W[r, c0 + 2:c0 + 64] = tie[torch.randperm(62)]
+    g = (torch.randn(rows, cols) * 1e-3).to(torch.bfloat16)
+    clips = tuple(synth.clip_grid(1.0, 0.5, 12))
+    for bits in (2, 3):
+        Wg, vg = _place(W, v)
+        run_case(f"tie-cluster.int{bits}.f32", 0, 0, 0, bits=bits, group=64, clips=clips, W=Wg, v=vg.clone(),
+                 g=g.cuda(), w_bf16=False, ema=True)
+    Wb = W.to(torch.bfloat16).cuda()
+    run_case("tie-cluster.int2.bf16", 0, 0, 0, bits=2, group=64, clips=clips, W=Wb, v=v.cuda(), w_bf16=True)
+
+
 def test_tiny_shapes():
     for rows, cols, bits, group in [(1, 64, 2, 64), (1, 128, 4, 128), (2, 64, 3, 64), (3, 16, 4, 16)]:
         fmt = "nvfp4" if group == 16 else "int"
