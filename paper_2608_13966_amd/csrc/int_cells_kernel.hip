@@ -41,16 +41,22 @@ namespace {
 
 constexpr int N = kIntN;
 
-// Exclusive suffix sum over the members of a spread group (member j at lane
-// offset 8 j): member j gets the sum of the values of members j+1 .. L-1
-// (Hillis-Steele on the values shifted down by one member).
+// Lanes of one group: spread over the wavefront (member j of a group 8 lanes
+// from member j - 1), so that LDS atomics from members of one group that hit
+// the same address do not serialise.
+constexpr bool kSpread = true;
+constexpr int kMemberStride = kSpread ? 8 : 1;
+
+// Exclusive suffix sum over the members of a group: member j gets the sum of
+// the values of members j+1 .. L-1 (Hillis-Steele on the values shifted down
+// by one member).
 template <int L>
 __device__ __forceinline__ double members_excl_suffix(double x, int j) {
-  double e = __shfl_down(x, 8);
+  double e = __shfl_down(x, kMemberStride);
   if (j + 1 >= L) e = 0.0;
 #pragma unroll
   for (int s = 1; s < L; s *= 2) {
-    const double y = __shfl_down(e, 8 * s);
+    const double y = __shfl_down(e, kMemberStride * s);
     if (j + s < L) e += y;
   }
   return e;
@@ -99,7 +105,7 @@ __global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
   __shared__ float s_alpha[kMaxClips], s_clip[kMaxClips];
   __shared__ float s_win[kThreads / 64][GPW][4];
 
-  using M = Members<L, true>;
+  using M = Members<L, kSpread>;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int j = M::member(lane), slot = M::slot(lane);
@@ -127,7 +133,7 @@ __global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
   WRegs<W_BF16> wr;
   float v[N];
   int_load<W_BF16, EMA>(p, mtx, e0, active, wr, v);
-  const IntRange rg = int_range<L, SYM, W_BF16, true>(wr);
+  const IntRange rg = int_range<L, SYM, W_BF16, kSpread>(wr);
 
   // ---- this group's cells: lane j owns cells [j cpl, (j + 1) cpl) -----------
   // Groups are int_cells_stride(cpl) cells apart, an odd number, so that the
@@ -289,41 +295,88 @@ __global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
     wave_lds_fence();
   }
 
-  // ---- the clips this lane owns: moments from NB suffix sums, fit, score ------
-  IntBest best = int_best_init();
-#pragma unroll 1
-  for (int t = 0; t < OWN; t++) {
-    const int k = j + L * t;
-    if (k < K) {
-      double A0 = 0.0, A1 = 0.0, A2 = 0.0;
-      if (group_unsafe) {
-        A0 = hist[3 * k];
-        A1 = hist[3 * k + 1];
-        A2 = hist[3 * k + 2];
-      } else {
-        const uint4 tw4 = *reinterpret_cast<const uint4*>(s_tp + k * kCellSteps);
-        const uint32_t tw[4] = {tw4.x, tw4.y, tw4.z, tw4.w};
+  // ---- the clips this lane owns: moments from NB suffix sums ------------------
+  auto moments = [&](int k, double& A0, double& A1, double& A2) {
+    A0 = A1 = A2 = 0.0;
+    if (group_unsafe) {
+      A0 = hist[3 * k];
+      A1 = hist[3 * k + 1];
+      A2 = hist[3 * k + 2];
+      return;
+    }
+    const uint4 tw4 = *reinterpret_cast<const uint4*>(s_tp + k * kCellSteps);
+    const uint32_t tw[4] = {tw4.x, tw4.y, tw4.z, tw4.w};
 #pragma unroll
-        for (int b = 1; b <= NB; b++) {
-          const int c = (int)((tw[(b - 1) >> 2] >> (8 * ((b - 1) & 3))) & 0xffu);
-          const double2 s = *reinterpret_cast<const double2*>(hist + 2 * c);
-          A0 += s.x;
-          A1 = __builtin_fma((double)(2 * b - 1), s.x, A1);
-          A2 += s.y;
-        }
-        A0 *= rsh;
-        A1 *= rsh;
-        A2 *= rshw;
-        if constexpr (SYM) {  // q = n - Q
-          A1 = __builtin_fma((double)QMAX * (double)QMAX, mo.Sv, __builtin_fma(-2.0 * (double)QMAX, A0, A1));
-          A2 = __builtin_fma(-(double)QMAX, mo.Svw, A2);
+    for (int b = 1; b <= NB; b++) {
+      const int c = (int)((tw[(b - 1) >> 2] >> (8 * ((b - 1) & 3))) & 0xffu);
+      const double2 s = *reinterpret_cast<const double2*>(hist + 2 * c);
+      A0 += s.x;
+      A1 = __builtin_fma((double)(2 * b - 1), s.x, A1);
+      A2 += s.y;
+    }
+    A0 *= rsh;
+    A1 *= rsh;
+    A2 *= rshw;
+    if constexpr (SYM) {  // q = n - Q
+      A1 = __builtin_fma((double)QMAX * (double)QMAX, mo.Sv, __builtin_fma(-2.0 * (double)QMAX, A0, A1));
+      A2 = __builtin_fma(-(double)QMAX, mo.Svw, A2);
+    }
+  };
+
+  // Selection.  With fp32 (s, z) the candidate's score is that of its exact
+  // fit up to the fp32 rounding of (s, z), a relative 1e-12 or so; the exact
+  // fit's score is C - num^2 / (Sv D) (asymmetric: num = Sv A2 - A0 Svw,
+  // D = Sv A1 - A0^2; symmetric: C - A2^2 / A1), with C the same for every
+  // clip.  So each lane ranks its clips by num^2 / D (cross-multiplied, ties
+  // to the lowest index), fits and scores only its best one, and the group's
+  // argmin runs over keys made from D / num^2.  Groups with a clip whose fit
+  // degenerates (no saliency, all of it on one code), and deployed
+  // precisions other than fp32, score every clip (int_fit_score).
+  IntBest best = int_best_init();
+  bool full = p.param_dtype != 0;
+  int bk = -1;
+  double bn = 0.0, bd = 1.0, b0 = 0.0, b1 = 0.0, b2 = 0.0;
+  if (!full) {
+#pragma unroll 1
+    for (int t = 0; t < OWN; t++) {
+      const int k = j + L * t;
+      if (k < K) {
+        double A0, A1, A2;
+        moments(k, A0, A1, A2);
+        const double D = SYM ? A1 : mo.Sv * A1 - A0 * A0;
+        const double num = SYM ? A2 : mo.Sv * A2 - A0 * mo.Svw;
+        const bool degenerate = SYM ? (A1 == 0.0) : (mo.Sv == 0.0 || D <= mo.thr);
+        const double n2 = num * num;
+        if (degenerate) {
+          full = true;
+        } else if (bk < 0 || n2 * bd > bn * D) {
+          bk = k;
+          bn = n2;
+          bd = D;
+          b0 = A0;
+          b1 = A1;
+          b2 = A2;
         }
       }
-      int_fit_score<SYM, QMAX>(p, k, s_clip[k], rg, mo, A0, A1, A2, best);
     }
   }
+  if (M::max(full ? 1.0f : 0.0f) > 0.0f) {
+#pragma unroll 1
+    for (int t = 0; t < OWN; t++) {
+      const int k = j + L * t;
+      if (k < K) {
+        double A0, A1, A2;
+        moments(k, A0, A1, A2);
+        int_fit_score<SYM, QMAX>(p, k, s_clip[k], rg, mo, A0, A1, A2, best);
+      }
+    }
+  } else if (bk >= 0) {
+    int_fit_score<SYM, QMAX>(p, bk, s_clip[bk], rg, mo, b0, b1, b2, best);
+    // rank by D / num^2 (num = 0: the worst fit, kept finite)
+    best.key = make_key(fmin(bd * rcp_f64(bn), 1e300), bk);
+  }
 
-  int_finish<W_BF16, BITS, G, SYM, true>(p, mtx, wr, rg, mo.Sv, best, s_alpha, s_win[wave][slot], j, gid, e0,
+  int_finish<W_BF16, BITS, G, SYM, kSpread>(p, mtx, wr, rg, mo.Sv, best, s_alpha, s_win[wave][slot], j, gid, e0,
                                          active);
 }
 
