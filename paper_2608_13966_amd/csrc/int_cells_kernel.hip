@@ -218,16 +218,16 @@ __global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
   // the chunk totals first, then the members above this one, then a second
   // pass that writes the suffix sums -------------------------------------------
   {
-    double th = 0.0, tw = 0.0;
+    uint64_t ih = 0, iw = 0;  // exact integer chunk totals
 #pragma unroll
     for (int i = 0; i < CPL; i++) {
       if (i < cpl) {
         const ulonglong2 t = *reinterpret_cast<const ulonglong2*>(mine + 2 * i);
-        th += i64_to_double(t.x);
-        tw += i64_to_double(t.y);
+        ih += t.x;
+        iw += t.y;
       }
     }
-    double eh2 = members_excl_suffix<L>(th, j), ew2 = members_excl_suffix<L>(tw, j);
+    double eh2 = members_excl_suffix<L>(i64_to_double(ih), j), ew2 = members_excl_suffix<L>(i64_to_double(iw), j);
 #pragma unroll
     for (int i = CPL - 1; i >= 0; i--) {
       if (i < cpl) {
@@ -335,7 +335,7 @@ __global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
   IntBest best = int_best_init();
   bool full = p.param_dtype != 0;
   int bk = -1;
-  double bn = 0.0, bd = 1.0, b0 = 0.0, b1 = 0.0, b2 = 0.0;
+  double bn = 0.0, bd = 1.0;
   if (!full) {
 #pragma unroll 1
     for (int t = 0; t < OWN; t++) {
@@ -353,9 +353,6 @@ __global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
           bk = k;
           bn = n2;
           bd = D;
-          b0 = A0;
-          b1 = A1;
-          b2 = A2;
         }
       }
     }
@@ -371,6 +368,8 @@ __global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
       }
     }
   } else if (bk >= 0) {
+    double b0, b1, b2;
+    moments(bk, b0, b1, b2);
     int_fit_score<SYM, QMAX>(p, bk, s_clip[bk], rg, mo, b0, b1, b2, best);
     // rank by D / num^2 (num = 0: the worst fit, kept finite)
     best.key = make_key(fmin(bd * rcp_f64(bn), 1e300), bk);
