@@ -48,6 +48,52 @@ def source_fingerprint() -> str:
     return h.hexdigest()[:16]
 
 
+def binned_valu_ops_per_weight(wl, n_cells: int) -> float:
+    """VALU lane-operations per weight of the binned INT kernel (the clips'
+    moments from per-group threshold-cell sums): per weight, the range (2),
+    the position u (1), its bucket (4) and cell (one compare and add: 2),
+    the packed cell (1), h and h w as exact integers (conversions, product,
+    sum h w^2, two scaled roundings with their high-word corrections, cell
+    address: 10), the emitted code, r and pack (5), and the EMA (3); per
+    group of G weights, the suffix scan (about 12 per cell), each clip's
+    moments from its NB suffix sums and its ratio test (3 NB + 11 per clip)
+    and one fit and score per 16 weights (about 45)."""
+    K = len(wl.clips)
+    qmax = (1 << (wl.bits - 1)) - 1 if wl.fmt == "int_sym" else (1 << wl.bits) - 1
+    nb = 2 * qmax if wl.fmt == "int_sym" else qmax
+    pre = 10.0 if wl.adamw else (3.0 if wl.ema else 0.0)
+    per_group = 12.0 * n_cells + (3.0 * nb + 11.0) * K + 45.0 * (wl.group / 16)
+    return 25.0 + pre + per_group / wl.group
+
+
+def int_kernel_choice(wl):
+    """(kernel name, cells) of the INT kernel the library takes for this
+    workload's clip grid (quasar_int_path; host-only)."""
+    from paper_2608_13966_amd import quasar as Q
+    d = Q.Descriptor(8, wl.group, fmt=wl.fmt, bits=wl.bits, group=wl.group, clips=wl.clips,
+                     w_dtype=Q.BF16 if wl.w_bf16 else Q.F32)
+    if Q.quasar_int_path(d) == 1:
+        return "int_cells_kernel", int_cells_count(wl)
+    return "int_reconstruct_kernel", 0
+
+
+def int_cells_count(wl) -> int:
+    """Cells per group of the binned kernel: the distinct code thresholds of
+    all clips plus one, with the clips' tie thresholds below u = 0 (odd
+    qmax) counted once -- in exact arithmetic T(k, b) = (b - qmax/2 - 1/2)
+    (2 f_k / qmax) for asymmetric groups and (b - Q - 1/2) (f_k / Q) for
+    symmetric ones."""
+    import numpy as np
+    sym = wl.fmt == "int_sym"
+    qmax = (1 << (wl.bits - 1)) - 1 if sym else (1 << wl.bits) - 1
+    ts = set()
+    for f in wl.clips:
+        for b in range(1, (2 * qmax if sym else qmax) + 1):
+            t = (b - qmax - 0.5) * f / qmax if sym else (b - qmax / 2 - 0.5) * 2 * f / qmax
+            ts.add(round(t, 9))
+    return len(ts) + 1
+
+
 def algorithmic_valu_ops_per_weight(wl) -> float:
     """VALU lane-operations per weight that the method needs as computed here:
     per clip, the code (scale-shift, round, clamp; NVFP4: scale, E2M1 round)
@@ -68,6 +114,10 @@ def algorithmic_valu_ops_per_weight(wl) -> float:
         # (5); per clip and block, each of the 8 codebook entries from two
         # prefix sums (about 30 lane-ops per entry, 8 x 30 / 512 per weight)
         return 37.0 + K * 8.0 * 30.0 / 512.0 + pre
+    if wl.fmt in ("int", "int_sym"):
+        kname, cells = int_kernel_choice(wl)
+        if kname == "int_cells_kernel":
+            return binned_valu_ops_per_weight(wl, cells)
     if wl.fmt == "int_sym":
         # per clip: the code (3), one product and two accumulations (3)
         return 6.0 * K + 9.0 + pre
@@ -430,7 +480,10 @@ def main(argv=None):
             traffic_ratio = round(ent["bytes_per_weight"] / kbpw, 4)
     except (OSError, ValueError, KeyError):
         pass
-    kname = {"nvfp4": "nvfp4_reconstruct", "rubin": "rubin_reconstruct"}.get(wl.fmt, "int_reconstruct")
+    if wl.fmt in ("int", "int_sym"):
+        kname = int_kernel_choice(wl)[0]
+    else:
+        kname = {"nvfp4": "nvfp4_reconstruct_kernel", "rubin": "rubin_reconstruct_kernel"}[wl.fmt]
     if t_alu > t_hbm:
         achieved = ops_w * k_wps / 1e12
         roofline = {"bound": "alu", "achieved": round(achieved, 2), "peak": round(PEAK_VALU_TOPS, 2),

@@ -297,12 +297,33 @@ void int_cells(quasar::IntParams& p, int K, int bits, bool sym, int group) {
   const int q0 = sym ? -qmax : 0;
   const int nb = sym ? 2 * qmax : qmax;
   const int tie = sym ? 0 : (qmax + 1) / 2;  // step b whose thresholds are the tie cluster
+  const int L = group / 16;
+  {
+    // at most K nb thresholds (the tie ones count once): when even that many
+    // fit, or when they cannot fit at all, this is decided before any search
+    const int m_upper = K * nb - (tie > 0 ? K - 1 : 0);
+    const int limit = any_fit ? quasar::kCellsPerLane : quasar::kCellsPerLaneAuto;
+    if ((m_upper + 1 + L - 1) / L > limit) return;
+  }
   float t[quasar::kMaxClips * quasar::kCellSteps];
   int n = 0;
   float ulo = INFINITY, uhi = -INFINITY;
   for (int k = 0; k < K; k++) {
     for (int b = 1; b <= nb; b++) {
+      // bracket: around the threshold of exact arithmetic, (b - q0 - qmax/2 - 1/2) / alpha
+      // (symmetric: (b - Q - 1/2) / alpha), widened until it holds
+      const double center = sym ? (b - qmax - 0.5) / (double)p.alpha[k]
+                                : (b - 0.5 * qmax - 0.5) / (double)p.alpha[k];
       uint32_t lo = f32_order_key(-INFINITY), hi = f32_order_key(INFINITY);
+      for (double half = 1e-6; half < 4.0; half *= 16.0) {
+        const uint32_t a = f32_order_key((float)(center - half)), z = f32_order_key((float)(center + half));
+        if (int_code(f32_from_order_key(a), p.alpha[k], qmax, sym) < q0 + b &&
+            int_code(f32_from_order_key(z), p.alpha[k], qmax, sym) >= q0 + b) {
+          lo = a;
+          hi = z;
+          break;
+        }
+      }
       while (hi - lo > 1) {
         const uint32_t mid = lo + (hi - lo) / 2;
         if (int_code(f32_from_order_key(mid), p.alpha[k], qmax, sym) >= q0 + b)
@@ -329,7 +350,6 @@ void int_cells(quasar::IntParams& p, int K, int bits, bool sym, int group) {
     for (int i = 0; i < m; i++)
       if (srt[i] > ulo && srt[i] <= uhi) return;
   }
-  const int L = group / 16;
   const int cpl = (m + 1 + L - 1) / L;
   if (cpl > quasar::kCellsPerLane || m + 3 > quasar::kCellThr || m > 127) return;
   if (!any_fit && cpl > quasar::kCellsPerLaneAuto) return;
