@@ -27,9 +27,52 @@ namespace {
 constexpr int N = 16;
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
+// E2M1 codes of (a, b) into byte `sel` of `old` (the other bytes kept), and
+// the two values of byte `sel` back; sel must fold to a constant
+__device__ __forceinline__ uint32_t fp4_put(uint32_t old, float a, float b, int sel) {
+  switch (sel) {
+    case 0: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, a, b, 1.0f, 0);
+    case 1: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, a, b, 1.0f, 1);
+    case 2: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, a, b, 1.0f, 2);
+    default: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, a, b, 1.0f, 3);
+  }
+}
+__device__ __forceinline__ f32x2 fp4_get(uint32_t pk, int sel) {
+  switch (sel) {
+    case 0: return __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(pk, 1.0f, 0);
+    case 1: return __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(pk, 1.0f, 1);
+    case 2: return __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(pk, 1.0f, 2);
+    default: return __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(pk, 1.0f, 3);
+  }
+}
+
+// E4M3 bytes of (a, b) into word `hi` of `old` (the other word kept), and the
+// value of byte `sel`; hi and sel must fold to constants
+__device__ __forceinline__ uint32_t fp8_put(uint32_t old, float a, float b, int hi) {
+  return (uint32_t)(hi ? __builtin_amdgcn_cvt_pk_fp8_f32(a, b, (int)old, true)
+                       : __builtin_amdgcn_cvt_pk_fp8_f32(a, b, (int)old, false));
+}
+__device__ __forceinline__ float fp8_get(uint32_t d, int sel) {
+  switch (sel) {
+    case 0: return __builtin_amdgcn_cvt_f32_fp8((int)d, 0);
+    case 1: return __builtin_amdgcn_cvt_f32_fp8((int)d, 1);
+    case 2: return __builtin_amdgcn_cvt_f32_fp8((int)d, 2);
+    default: return __builtin_amdgcn_cvt_f32_fp8((int)d, 3);
+  }
+}
+
+// minimum of two non-negative, non-NaN doubles (v_min_f64 without the
+// quieting of its inputs that fmin() adds)
+__device__ __forceinline__ double min_f64(double a, double b) {
+  double r;
+  asm("v_min_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
 template <bool W_BF16, int EMA, int KC, bool MULTI>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu((KC > 8 || MULTI) ? 3 : 4)))
 void nvfp4_reconstruct_kernel(Nvfp4Params p) {
+  static_assert(KC % 4 == 0, "clips are converted four at a time");
   __shared__ float s_c6[kMaxClips], s_clip[kMaxClips];
   const int tid = threadIdx.x;
   const int K = p.n_clips;
@@ -110,7 +153,9 @@ void nvfp4_reconstruct_kernel(Nvfp4Params p) {
   for (int i = 0; i < N; i++) u[i] = wr.get(i) * rm;
 
   double Sww = 0.0;  // sum h w^2, accumulated in the first pass
-  const float rst = 1.0f / st;
+  // x of the search scale, used when no weight with saliency gets a non-zero
+  // code: f * (m / 6) / S_t (like every x, it only picks an E4M3 neighbour)
+  const float mx = m * (1.0f / 6.0f) * __builtin_amdgcn_rcpf(st);
 
   double best_key = __longlong_as_double(0x7ff0000000000000ll);
   uint32_t best_e = 0;
@@ -129,6 +174,9 @@ void nvfp4_reconstruct_kernel(Nvfp4Params p) {
     double acc[KC][2];
 #pragma unroll
     for (int kk = 0; kk < KC; kk++) acc[kk][0] = acc[kk][1] = 0.0;
+    // Clips kk .. kk+3 put their two codes in bytes 0..3 of pk, and all four
+    // are read back from the finished dword (no zeroing, one live copy).
+    uint32_t pk = 0u;
 #pragma unroll
     for (int i = 0; i < N; i += 2) {
       float v0 = v[i], v1 = v[i + 1], w0 = wr.get(i), w1 = wr.get(i + 1);
@@ -140,45 +188,67 @@ void nvfp4_reconstruct_kernel(Nvfp4Params p) {
         Sww = __builtin_fma(H1 * W1, W1, Sww);
       }
 #pragma unroll
-      for (int kk = 0; kk < KC; kk++) {
+      for (int k4 = 0; k4 < KC; k4 += 4) {
         // E2M1 round-to-nearest-even with saturation at 6 for two weights
         // (v_cvt_scalef32_pk_fp4_f32) and back to fp32
-        const uint32_t pk = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, u[i] * cs[kk], u[i + 1] * cs[kk], 1.0f, 0);
-        const f32x2 qq = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(pk, 1.0f, 0);
-        const double Q0 = (double)qq[0], Q1 = (double)qq[1];
-        const double HQ0 = H0 * Q0, HQ1 = H1 * Q1;
-        acc[kk][0] = __builtin_fma(HQ0, Q0, acc[kk][0]);
-        acc[kk][1] = __builtin_fma(HQ0, W0, acc[kk][1]);
-        acc[kk][0] = __builtin_fma(HQ1, Q1, acc[kk][0]);
-        acc[kk][1] = __builtin_fma(HQ1, W1, acc[kk][1]);
+#pragma unroll
+        for (int kk = k4; kk < k4 + 4; kk++) pk = fp4_put(pk, u[i] * cs[kk], u[i + 1] * cs[kk], kk & 3);
+#pragma unroll
+        for (int kk = k4; kk < k4 + 4; kk++) {
+          const f32x2 qq = fp4_get(pk, kk & 3);
+          const double Q0 = (double)qq[0], Q1 = (double)qq[1];
+          const double HQ0 = H0 * Q0, HQ1 = H1 * Q1;
+          acc[kk][0] = __builtin_fma(HQ0, Q0, acc[kk][0]);
+          acc[kk][1] = __builtin_fma(HQ0, W0, acc[kk][1]);
+          acc[kk][0] = __builtin_fma(HQ1, Q1, acc[kk][0]);
+          acc[kk][1] = __builtin_fma(HQ1, W1, acc[kk][1]);
+        }
       }
       __builtin_amdgcn_sched_barrier(0);
     }
+    __builtin_amdgcn_sched_barrier(0);
     // Branch-free on purpose: a clip-dependent branch here would let the
     // compiler sink each clip's moment accumulation into its own block and
     // serialise the clips (one 16-deep fp64 chain at a time).
+    // The E4M3 bytes of clips kk, kk+1 are converted together and kept, four
+    // to a dword, in eb[kk / 4].
+    uint32_t eb[KC / 4];
 #pragma unroll
-    for (int kk = 0; kk < KC; kk++) {
-      const int k = k0 + kk;
-      const double Sqq = acc[kk][0], Sqw = acc[kk][1];
-      // x = s*/S_t with s* = Sqw / Sqq (the search scale f m / 6 when no
-      // weight with saliency has a non-zero code).  fp32 is enough: x only
-      // picks an E4M3 neighbour, and its error (a few 1e-7 relative) can flip
-      // that choice only next to a rounding midpoint.
-      const float xr = (float)Sqw * __builtin_amdgcn_rcpf((float)Sqq * st);
-      const float xz = (fs[kk] * m) * (1.0f / 6.0f) * rst;
-      const float x = (Sqq == 0.0) ? xz : xr;
-      // nearest E4M3FN (RNE; the hardware conversion returns NaN above 464,
-      // hence the clamp to 448, which is also the saturated value)
-      const uint32_t e = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(fminf(x, 448.0f), 0.0f, 0, false) & 0xffu;
-      const float sblk = st * __builtin_amdgcn_cvt_f32_fp8((int)e, 0);
-      const double sb = (double)sblk;
-      const double score = sb * (sb * Sqq - 2.0 * Sqw) + Sww;
-      double key = make_key(score, k);
-      key = (k < K) ? key : __longlong_as_double(0x7ff0000000000000ll);  // padding clips never win
-      const bool better = key < best_key;
-      best_key = better ? key : best_key;
-      best_e = better ? e : best_e;
+    for (int kk = 0; kk < KC; kk += 2) {
+      float xc[2];
+#pragma unroll
+      for (int t = 0; t < 2; t++) {
+        const double Sqq = acc[kk + t][0], Sqw = acc[kk + t][1];
+        // x = s*/S_t with s* = Sqw / Sqq (the search scale f m / 6 when no
+        // weight with saliency has a non-zero code).  fp32 is enough: x only
+        // picks an E4M3 neighbour, and its error (a few 1e-7 relative) can
+        // flip that choice only next to a rounding midpoint.  x >= 0 (q has
+        // the sign of w); the clamp to 448, the saturated value, keeps it
+        // below 464, above which the conversion returns NaN.
+        const float xr = (float)Sqw * __builtin_amdgcn_rcpf((float)Sqq * st);
+        xc[t] = __builtin_amdgcn_fmed3f((Sqq == 0.0) ? fs[kk + t] * mx : xr, 0.0f, 448.0f);
+      }
+      // nearest E4M3FN (RNE) of both
+      eb[kk / 4] = fp8_put(kk % 4 == 0 ? __float_as_uint(xc[0]) : eb[kk / 4], xc[0], xc[1], (kk / 2) & 1);
+#pragma unroll
+      for (int t = 0; t < 2; t++) {
+        const int k = k0 + kk + t;
+        const double Sqq = acc[kk + t][0], Sqw = acc[kk + t][1];
+        const double sb = (double)(st * fp8_get(eb[kk / 4], (kk + t) & 3));
+        // sum h (sb q - w)^2 expanded: Sww + sb (sb Sqq - 2 Sqw)
+        const double score = __builtin_fma(sb, __builtin_fma(sb, Sqq, -2.0 * Sqw), Sww);
+        // keys order like the scores and keep the lowest index among equal
+        // ones; padding clips repeat clip K-1 with a larger index
+        best_key = min_f64(best_key, make_key(score, k));
+      }
+    }
+    // the winner's E4M3 byte, if it is a clip of this pass
+    const int kb = key_index(best_key) - k0;
+    if (kb >= 0 && kb < KC) {
+      uint32_t d = eb[0];
+#pragma unroll
+      for (int t = 1; t < KC / 4; t++) d = (kb >= 4 * t) ? eb[t] : d;
+      best_e = (d >> (8 * (kb & 3))) & 0xffu;
     }
   }
 
