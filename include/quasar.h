@@ -290,8 +290,15 @@ int64_t quasar_num_groups(const quasar_desc* desc);
  *     QUASAR_INT_PATH=direct).  QUASAR_INT_PATH=binned selects the binned
  *     kernel for every grid whose thresholds fit its tables.
  * Both give the same codes, chosen clip and r up to the rounding order of the
- * fp64 moment sums.  A negative quasar_status for an invalid desc or another
- * format. */
+ * fp64 moment sums.
+ * For RUBIN_INT3 (whose per-clip sums of Eq. rubin-fit, App. B, always come
+ * from such cells) it tells how a weight finds its cell:
+ *  1  a table of 256 equal slices of the normalised range and at most three
+ *     compares (clip grids whose thresholds are spread enough);
+ *  0  a binary search over all thresholds (any grid, or the environment
+ *     variable QUASAR_RUBIN_PATH=tree).
+ * Both give identical results.  A negative quasar_status for an invalid desc
+ * or the NVFP4 format. */
 int quasar_int_path(const quasar_desc* desc);
 
 /* Bytes of the packed code buffer; 0 for an invalid desc. */

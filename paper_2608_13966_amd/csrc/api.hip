@@ -183,6 +183,17 @@ void int_clip_tables(const quasar_desc* d, quasar::IntParams& p) {
   }
 }
 
+// The clip tables of the Rubin kernel: f_k and alpha_k = 7 / (2 f_k) (fp32
+// division); entries past K repeat the last clip.
+void rubin_clip_tables(const quasar_desc* d, quasar::RubinParams& p) {
+  const int K = d->n_clips;
+  for (int k = 0; k < quasar::kMaxClips; k++) {
+    const float f = d->clip_ratios[k < K ? k : K - 1];
+    p.clip[k] = f;
+    p.alpha[k] = 7.0f / (2.0f * f);
+  }
+}
+
 // The code of u under a clip with scale alpha, in the kernels' fp32 recipe:
 // clamp(rint(fma(u, alpha, 3.5)), 0, 7) (correctly rounded fma, ties to even).
 int rubin_code(float u, float alpha) {
@@ -210,6 +221,65 @@ void eytzinger_fill(float* tree, const float* sorted, int& next, int node) {
   eytzinger_fill(tree, sorted, next, 2 * node);
   tree[node] = sorted[next++];
   eytzinger_fill(tree, sorted, next, 2 * node + 1);
+}
+
+int cell_bucket(float u);
+
+// The bucket form of the Rubin kernel's cells from the thresholds t[7 k + b]
+// = T(k, b) (see RubinParams): the tie-cluster thresholds T(k, 3) are merged
+// into one at their least value, and every other bucket may hold at most
+// three thresholds.  Returns false (the tree form is used) when the grid does
+// not allow it or QUASAR_RUBIN_PATH=tree is set.
+bool rubin_buckets(quasar::RubinParams& p, const float* t, int K) {
+  const char* force = getenv("QUASAR_RUBIN_PATH");
+  if (force != nullptr && strcmp(force, "tree") == 0) return false;
+  const int n = 7 * K;
+  float ulo = INFINITY, uhi = -INFINITY;
+  for (int k = 0; k < K; k++) {
+    ulo = fminf(ulo, t[7 * k + 3]);
+    uhi = fmaxf(uhi, t[7 * k + 3]);
+  }
+  if (!(ulo > -0x1p-20f && uhi < 0.0f)) return false;
+  const bool merge = ulo < uhi;
+  float srt[quasar::kRubinThresholds];
+  int m = 0;
+  for (int i = 0; i < n; i++) srt[m++] = (merge && t[i] >= ulo && t[i] <= uhi) ? ulo : t[i];
+  std::sort(srt, srt + m);
+  m = (int)(std::unique(srt, srt + m) - srt);
+  if (merge) {  // no other threshold may fall inside the merged span
+    for (int i = 0; i < m; i++)
+      if (srt[i] > ulo && srt[i] <= uhi) return false;
+  }
+  int cnt[quasar::kCellBuckets] = {0};
+  int cmax = 1, below = 0;
+  for (int i = 0; i < m; i++) cnt[cell_bucket(srt[i])]++;
+  uint8_t base[quasar::kCellBuckets];
+  for (int b = 0; b < quasar::kCellBuckets; b++) {
+    cmax = std::max(cmax, cnt[b]);
+    base[b] = (uint8_t)below;
+    below += cnt[b];
+  }
+  if (cmax > 3) return false;
+  for (int k = 0; k < quasar::kMaxClips; k++) {
+    for (int b = 0; b < 9; b++) {
+      int c = 0;
+      if (k < K && b >= 1 && b <= 7) {
+        float tb = t[7 * k + b - 1];
+        if (merge && tb >= ulo && tb <= uhi) tb = ulo;
+        c = (int)(std::lower_bound(srt, srt + m, tb) - srt) + 1;
+      } else if (k < K && b == 8) {
+        c = m + 1;
+      }
+      p.tpos[k][b] = (uint8_t)c;
+    }
+  }
+  for (int i = 0; i < quasar::kRubinThresholds; i++) p.thr[i] = i < m ? srt[i] : NAN;
+  memcpy(p.base, base, sizeof(base));
+  p.buckets = 1;
+  p.cmax = cmax;
+  p.unsafe_lo = merge ? ulo : INFINITY;
+  p.unsafe_hi = merge ? uhi : INFINITY;
+  return true;
 }
 
 // The Rubin kernel's code thresholds: the code is non-decreasing in u, so
@@ -243,6 +313,7 @@ void rubin_thresholds(quasar::RubinParams& p, int K) {
       p.tpos[k][b] = (uint8_t)cnt;
     }
   }
+  if (rubin_buckets(p, t, K)) return;
   std::sort(t, t + n);
   // in-order walk of the complete tree with nodes 1 .. 127 = the sorted list
   float sorted[quasar::kRubinThresholds - 1];
@@ -433,11 +504,7 @@ int launch_path(const quasar_desc* d, const void* W, void* Wu, float* m, float* 
     p.omb2 = omb2;
     p.n_clips = K;
     p.weighting = d->weighting;
-    for (int k = 0; k < quasar::kMaxClips; k++) {
-      const float f = d->clip_ratios[k < K ? k : K - 1];
-      p.clip[k] = f;
-      p.alpha[k] = 7.0f / (2.0f * f);
-    }
+    rubin_clip_tables(d, p);
     rubin_thresholds(p, K);
     if (batch) p.batch = *batch;
     e = quasar::launch_rubin(p, w_bf16, ema_mode, st);
@@ -627,6 +694,13 @@ int quasar_adamw_reconstruct(const quasar_desc* d, const quasar_adamw* opt, void
 extern "C" int quasar_int_path(const quasar_desc* d) {
   const int s = check_desc(d);
   if (s != QUASAR_OK) return s;
+  if (is_rubin(d)) {
+    quasar::RubinParams p;
+    memset(&p, 0, sizeof(p));
+    rubin_clip_tables(d, p);
+    rubin_thresholds(p, d->n_clips);
+    return p.buckets;
+  }
   if (d->format != QUASAR_INT && d->format != QUASAR_INT_SYM) return QUASAR_ERR_FORMAT;
   quasar::IntParams p;
   memset(&p, 0, sizeof(p));

@@ -17,6 +17,15 @@ __device__ __forceinline__ float uniform_f32(float x) {
   return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(x)));
 }
 
+// The bucket of u among 256 equal slices of [-1, 1]: clamp(floor(u * 128),
+// -128, 127) + 128 (u * 128 is exact, so a boundary falls exactly at u = 0);
+// any u, NaN included, gives an index in [0, 256).
+__device__ __forceinline__ int cell_bucket(float u) {
+  int f;
+  asm("v_cvt_flr_i32_f32 %0, %1" : "=v"(f) : "v"(u * 128.0f));
+  return min(max(f, -128), 127) + 128;
+}
+
 // ---- bf16 ------------------------------------------------------------------
 // Two fp32 values -> packed bf16 (round to nearest even) in one gfx950
 // instruction (v_cvt_pk_bf16_f32); the low half holds `a`.
@@ -231,6 +240,49 @@ __device__ __forceinline__ double run_min_f64(double x) {
   if constexpr (L >= 8) x = fmin(x, dpp_f64<kDppHalfMirror>(x));
   if constexpr (L >= 16) x = fmin(x, dpp_f64<kDppMirror>(x));
   return x;
+}
+
+// Combine values that are uniform within each row of 16 over the wavefront's
+// four rows, without LDS: row_bcast:15 brings row 0's value into row 1 and
+// row 2's into row 3, row_bcast:31 brings lane 31's into rows 2 and 3 (rows
+// outside the mask take `id`, the operation's identity), and lane 63, which
+// then holds op(op(r3, r2), op(r1, r0)), is read into every lane.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp_rows(uint32_t id, uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)id, (int)x, CTRL, ROW_MASK, 0xF, false);
+}
+__device__ __forceinline__ float rows_min(float x) {
+  x = fminf(x, as_f32(dpp_rows<0x142, 0xA>(as_u32(INFINITY), as_u32(x))));
+  x = fminf(x, as_f32(dpp_rows<0x143, 0xC>(as_u32(INFINITY), as_u32(x))));
+  return as_f32((uint32_t)__builtin_amdgcn_readlane((int)as_u32(x), 63));
+}
+__device__ __forceinline__ float rows_max(float x) {
+  x = fmaxf(x, as_f32(dpp_rows<0x142, 0xA>(as_u32(-INFINITY), as_u32(x))));
+  x = fmaxf(x, as_f32(dpp_rows<0x143, 0xC>(as_u32(-INFINITY), as_u32(x))));
+  return as_f32((uint32_t)__builtin_amdgcn_readlane((int)as_u32(x), 63));
+}
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ double dpp_rows_f64(double id, double x) {
+  const uint64_t i = (uint64_t)__double_as_longlong(id), u = (uint64_t)__double_as_longlong(x);
+  const uint32_t lo = dpp_rows<CTRL, ROW_MASK>((uint32_t)i, (uint32_t)u);
+  const uint32_t hi = dpp_rows<CTRL, ROW_MASK>((uint32_t)(i >> 32), (uint32_t)(u >> 32));
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+__device__ __forceinline__ double lane63_f64(double x) {
+  const uint64_t u = (uint64_t)__double_as_longlong(x);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, 63);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), 63);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+__device__ __forceinline__ double rows_sum(double x) {
+  x = x + dpp_rows_f64<0x142, 0xA>(0.0, x);
+  x = x + dpp_rows_f64<0x143, 0xC>(0.0, x);
+  return lane63_f64(x);
+}
+__device__ __forceinline__ double rows_min_f64(double x) {
+  x = fmin(x, dpp_rows_f64<0x142, 0xA>(INFINITY, x));
+  x = fmin(x, dpp_rows_f64<0x143, 0xC>(INFINITY, x));
+  return lane63_f64(x);
 }
 
 // A non-negative score with the candidate index in its 4 low mantissa bits:

@@ -77,15 +77,6 @@ __device__ __forceinline__ double i64_to_double(uint64_t n) {
   return __longlong_as_double((long long)(n + ((uint64_t)kMagicHi << 32))) - kMagic;
 }
 
-// The bucket of u: clamp(floor(u * 128), -128, 127) + 128 (u * 128 is exact,
-// so a boundary falls exactly at u = 0); any u, NaN included, gives an index
-// in [0, 256).
-__device__ __forceinline__ int cell_bucket(float u) {
-  int f;
-  asm("v_cvt_flr_i32_f32 %0, %1" : "=v"(f) : "v"(u * (0.5f * (float)kCellBuckets)));
-  return min(max(f, -kCellBuckets / 2), kCellBuckets / 2 - 1) + kCellBuckets / 2;
-}
-
 template <bool W_BF16, int EMA, int BITS, int G, bool SYM>
 __global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
   constexpr int L = G / N;     // lanes per group

@@ -70,7 +70,7 @@ __device__ __forceinline__ const MatrixSlot& batch_slot(int64_t& blk) {
 // built by the host for one clip grid.  T(k, b), b = 1 .. NB, is the least
 // fp32 u whose code under clip k is at least q0 + b; t_0 < ... < t_{M-1} are
 // the distinct T(k, b) of all clips, and the cell of u is #{i : t_i <= u}.
-constexpr int kCellBuckets = 256;  // equal slices of u in [-1, 1]
+constexpr int kCellBuckets = 256;  // equal slices of u in [-1, 1] (cell_bucket in device_common.h)
 constexpr int kCellSteps = 16;     // >= NB (15 at most), bytes per clip in tp
 constexpr int kCellsPerLane = 15;  // most cells a lane scans (LDS <= 60 KB)
 constexpr int kCellsPerLaneAuto = 10;  // most for which the binned kernel is the default
@@ -186,8 +186,21 @@ struct RubinParams {
   // (0 for b = 0, 7K + 1 for b = 8)
   float thr[kRubinThresholds];
   uint8_t tpos[kMaxClips][9];
+  // Bucket form (buckets = 1), taken when the clip grid allows it: the
+  // tie-cluster thresholds T(k, 3) (all in (-2^-20, 0), where the fp32 code
+  // rounding ties at 3.5) are merged into one at their least value, thr holds
+  // the m distinct merged thresholds sorted (NaN padding) and tpos indexes
+  // them (tpos[k][8] = m + 1); base[bkt] = the number of them below bucket bkt
+  // of the binned INT kernel's bucketing, each bucket holding at most cmax.
+  // A weight in [unsafe_lo, unsafe_hi] (between tie thresholds) makes the
+  // kernel sum its block's code-3 and code-4 entries directly.
+  int buckets;
+  int cmax;
+  float unsafe_lo, unsafe_hi;
+  uint8_t base[kCellBuckets];
   BatchTable batch;
 };
+static_assert(sizeof(RubinParams) <= 4096, "kernel arguments are limited to 4 KB");
 
 // Work units (groups / blocks) one workgroup of each kernel covers.
 constexpr int64_t int_units_per_block(int group) { return kThreads / (group / 16); }

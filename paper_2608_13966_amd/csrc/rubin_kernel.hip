@@ -34,6 +34,8 @@
 // block and its 8 consecutive columns 8 (l % 8) .. 8 (l % 8) + 7.  The
 // per-clip phase runs 8 clips at a time, lane (k, b) = (l / 8, l % 8) owning
 // codebook entry b of clip k.
+#include <type_traits>
+
 #include "device_common.h"
 #include "quasar_internal.h"
 
@@ -73,18 +75,39 @@ __device__ __forceinline__ double join_limbs(int64_t hi, int64_t lo) {
   return __builtin_ldexp((double)lo, -kLoBits) + (double)hi;
 }
 
-__device__ __forceinline__ int64_t shfl_up_i64(int64_t x, int d) {
-  return (int64_t)__shfl_up((long long)x, (unsigned)d, 64);
+typedef long long ll2 __attribute__((ext_vector_type(2)));
+
+// cells 2 l and 2 l + 1 of a cell row as one 16-byte LDS access
+__device__ __forceinline__ ll2* cell_pair(int64_t* row, int l) { return reinterpret_cast<ll2*>(row + 2 * l); }
+
+// One step of a wavefront-wide inclusive scan of four int64 and one int:
+// every lane adds the values DPP control CTRL brings it (lanes of rows outside
+// ROW_MASK, and lanes without a source, add 0).  Integer addition: exact.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ void scan_step(int64_t (&x)[4], int& xf) {
+#pragma unroll
+  for (int j = 0; j < 4; j++) {
+    const uint64_t u = (uint64_t)x[j];
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)u, CTRL, ROW_MASK, 0xf, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(u >> 32), CTRL, ROW_MASK, 0xf, false);
+    x[j] += (int64_t)(((uint64_t)hi << 32) | lo);
+  }
+  xf += __builtin_amdgcn_update_dpp(0, xf, CTRL, ROW_MASK, 0xf, false);
 }
 
-template <bool W_BF16, int EMA>
+// BK: the bucket form of the cells (RubinParams::buckets), else the tree form.
+template <bool W_BF16, int EMA, bool BK>
 __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams p) {
+  static_assert(kThreads == kCellBuckets, "one bucket entry per thread");
   // per cell: h = hh + hl 2^-50 and h w = wh + wl 2^-50 in scaled units (one
   // array per limb, so that lanes on different cells spread over the banks),
   // then their exclusive prefix sums; a flag for an h > 0, then its prefix count
-  __shared__ int64_t s_limb[kWaves][2][4][kCells + 1];
-  __shared__ int s_flag[kWaves][kCells + 1];
-  __shared__ float s_thr[kCells];                 // thresholds in search-tree order
+  // rows of kCells + 2 entries keep every row 16-byte aligned for the
+  // two-cell (128-bit) accesses of the scan
+  __shared__ int64_t s_limb[kWaves][2][4][kCells + 2];
+  __shared__ int s_flag[kWaves][kCells + 2];
+  __shared__ float s_thr[BK ? 1 : kCells];        // tree form: thresholds in search-tree order
+  __shared__ uint4 s_bucket[BK ? kCellBuckets : 1];  // bucket form: first cell, next three thresholds
   __shared__ uint8_t s_tpos[kMaxClips][9];        // cell range of code b under clip k
   __shared__ float s_lut[kWaves][8];
   __shared__ uint32_t s_lutb[kWaves][8];
@@ -97,7 +120,13 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
     s_alpha[tid] = p.alpha[tid];
     s_clip[tid] = p.clip[tid];
   }
-  if (tid < kCells) s_thr[tid] = p.thr[tid];
+  if constexpr (BK) {  // read from the kernel-argument segment with per-lane indices
+    const RubinParams* kp = kernarg_params<RubinParams>();
+    const int c = kp->base[tid];
+    s_bucket[tid] = make_uint4((uint32_t)c, as_u32(kp->thr[c]), as_u32(kp->thr[c + 1]), as_u32(kp->thr[c + 2]));
+  } else {
+    if (tid < kCells) s_thr[tid] = p.thr[tid];
+  }
   if (tid < kMaxClips * 9) (&s_tpos[0][0])[tid] = (&p.tpos[0][0])[tid];
   __syncthreads();
 
@@ -184,12 +213,8 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
     mx = fmaxf(mx, w[i]);
     hm = fmaxf(hm, v[i]);
   }
-  mn = run_min<16>(mn);
-  mn = fminf(mn, __shfl_xor(mn, 16, 64));
-  mn = fminf(mn, __shfl_xor(mn, 32, 64));
-  mx = run_max<16>(mx);
-  mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  mn = rows_min(run_min<16>(mn));
+  mx = rows_max(run_max<16>(mx));
   double H[NE], HW[NE];
   double sww = 0.0, sh = 0.0;
 #pragma unroll
@@ -199,12 +224,8 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
     sww = __builtin_fma(HW[i], (double)w[i], sww);
     sh += H[i];
   }
-  sww = run_sum<16>(sww);
-  sww += __shfl_xor(sww, 16, 64);
-  sww += __shfl_xor(sww, 32, 64);
-  sh = run_sum<16>(sh);
-  sh += __shfl_xor(sh, 16, 64);
-  sh += __shfl_xor(sh, 32, 64);
+  sww = rows_sum(run_sum<16>(sww));
+  sh = rows_sum(run_sum<16>(sh));
 
   const bool constant = (mx == mn);
   const float c = 0.5f * (mx + mn);
@@ -222,9 +243,7 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
   if (!constant) {  // uniform
     // h < 2^eh and |h w| < 2^(eh + ew): the scaled values stay below 2^51,
     // and the limb sums of 512 of them below 2^60
-    hm = run_max<16>(hm);
-    hm = fmaxf(hm, __shfl_xor(hm, 16, 64));
-    hm = fmaxf(hm, __shfl_xor(hm, 32, 64));
+    hm = rows_max(run_max<16>(hm));
     int eh, ew;
     (void)__builtin_frexpf(hm, &eh);
     (void)__builtin_frexpf(fmaxf(fabsf(mn), fabsf(mx)), &ew);
@@ -233,38 +252,73 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
     // ---- cells: clear, then add every weight's limbs into its cell ------------
     // two copies of the cell sums (even / odd lanes) halve the atomics that
     // meet on one address; the prefix sums go to copy 0
-    int64_t(*limb)[kCells + 1] = s_limb[wave][0];
-    int64_t(*limb1)[kCells + 1] = s_limb[wave][1];
-    int64_t(*mine)[kCells + 1] = s_limb[wave][lane & 1];
+    int64_t(*limb)[kCells + 2] = s_limb[wave][0];
+    int64_t(*limb1)[kCells + 2] = s_limb[wave][1];
+    int64_t(*mine)[kCells + 2] = s_limb[wave][lane & 1];
     int* flag = s_flag[wave];
 #pragma unroll
-    for (int t = 0; t < 2; t++) {
-#pragma unroll
-      for (int j = 0; j < 4; j++) limb[j][2 * lane + t] = limb1[j][2 * lane + t] = 0;
-      flag[2 * lane + t] = 0;
-    }
+    for (int j = 0; j < 4; j++) *cell_pair(limb[j], lane) = *cell_pair(limb1[j], lane) = ll2{0, 0};
+    *reinterpret_cast<int2*>(flag + 2 * lane) = make_int2(0, 0);
     wave_lds_fence();
-    // cell = number of thresholds <= u: descend the implicit search tree
-    // (node n has children 2n, 2n + 1; the leaves 128 .. 255 are the counts),
-    // one level for all 8 weights at a time so that their reads overlap
-    int node[NE];
+    // the cell of every weight: the number of thresholds <= u
+    int pos[NE];
+    bool unsafe = false;
+    if constexpr (BK) {
+      // the bucket's first cell plus cmax compares (thresholds outside u's
+      // bucket lie on the far side of u; the padding is NaN), four bucket
+      // reads in flight at a time
+      const float ulo = p.unsafe_lo, uhi = p.unsafe_hi;
+      auto bin = [&](auto cmax_tag) {
+        constexpr int C = decltype(cmax_tag)::value;
 #pragma unroll
-    for (int i = 0; i < NE; i++) node[i] = 1;
+        for (int i0 = 0; i0 < NE; i0 += 4) {
+          uint4 e[4];
 #pragma unroll
-    for (int d = 0; d < 7; d++) {
+          for (int t = 0; t < 4; t++) e[t] = s_bucket[cell_bucket(u[i0 + t])];
 #pragma unroll
-      for (int i = 0; i < NE; i++) node[i] = 2 * node[i] + (s_thr[node[i]] <= u[i] ? 1 : 0);
+          for (int t = 0; t < 4; t++) {
+            const float x = u[i0 + t];
+            int c = (int)e[t].x + (x >= as_f32(e[t].y) ? 1 : 0);
+            if constexpr (C > 1) c += (x >= as_f32(e[t].z) ? 1 : 0);
+            if constexpr (C > 2) c += (x >= as_f32(e[t].w) ? 1 : 0);
+            pos[i0 + t] = c;
+            unsafe |= (x >= ulo) & (x <= uhi);
+          }
+        }
+      };
+      if (p.cmax == 1)
+        bin(std::integral_constant<int, 1>{});
+      else if (p.cmax == 2)
+        bin(std::integral_constant<int, 2>{});
+      else
+        bin(std::integral_constant<int, 3>{});
+    } else {
+      // descend the implicit search tree (node n has children 2n, 2n + 1; the
+      // leaves 128 .. 255 are the counts), one level for all 8 weights at a
+      // time so that their reads overlap
+      int node[NE];
+#pragma unroll
+      for (int i = 0; i < NE; i++) node[i] = 1;
+#pragma unroll
+      for (int d = 0; d < 7; d++) {
+#pragma unroll
+        for (int i = 0; i < NE; i++) node[i] = 2 * node[i] + (s_thr[node[i]] <= u[i] ? 1 : 0);
+      }
+#pragma unroll
+      for (int i = 0; i < NE; i++) pos[i] = node[i] - kCells;
     }
+    // a weight between tie thresholds: the block's code-3 and code-4 entries
+    // are summed directly below
+    const bool block_unsafe = __ballot(unsafe) != 0;  // uniform
 #pragma unroll
     for (int i = 0; i < NE; i++) {
-      const int pos = node[i] - kCells;
       int64_t x[4];
       split_limbs(__builtin_ldexp(H[i], sh_exp), x[0], x[1]);
       split_limbs(__builtin_ldexp(HW[i], sw_exp), x[2], x[3]);
 #pragma unroll
       for (int j = 0; j < 4; j++)
-        atomicAdd(reinterpret_cast<unsigned long long*>(&mine[j][pos]), (unsigned long long)x[j]);
-      if (v[i] > 0.0f) flag[pos] = 1;
+        atomicAdd(reinterpret_cast<unsigned long long*>(&mine[j][pos[i]]), (unsigned long long)x[j]);
+      if (v[i] > 0.0f) flag[pos[i]] = 1;
     }
     wave_lds_fence();
 
@@ -273,34 +327,29 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
       int64_t a[4], x[4], t[4];
 #pragma unroll
       for (int j = 0; j < 4; j++) {
-        a[j] = limb[j][2 * lane] + limb1[j][2 * lane];
-        x[j] = t[j] = a[j] + limb[j][2 * lane + 1] + limb1[j][2 * lane + 1];
+        const ll2 c0 = *cell_pair(limb[j], lane), c1 = *cell_pair(limb1[j], lane);
+        a[j] = c0.x + c1.x;
+        x[j] = t[j] = a[j] + c0.y + c1.y;
       }
-      const int fa = flag[2 * lane];
-      int xf = fa + flag[2 * lane + 1];
+      const int2 fl = *reinterpret_cast<const int2*>(flag + 2 * lane);
+      const int fa = fl.x;
+      int xf = fa + fl.y;
       const int tf = xf;
-#pragma unroll
-      for (int d = 1; d < 64; d <<= 1) {  // inclusive scan of the lane totals
-        int64_t y[4];
-#pragma unroll
-        for (int j = 0; j < 4; j++) y[j] = shfl_up_i64(x[j], d);
-        const int yf = __shfl_up(xf, (unsigned)d, 64);
-        if (lane >= d) {
-#pragma unroll
-          for (int j = 0; j < 4; j++) x[j] += y[j];
-          xf += yf;
-        }
-      }
+      // inclusive scan of the lane totals over the wavefront
+      scan_step<0x111, 0xf>(x, xf);  // row_shr:1
+      scan_step<0x112, 0xf>(x, xf);  // row_shr:2
+      scan_step<0x114, 0xf>(x, xf);  // row_shr:4
+      scan_step<0x118, 0xf>(x, xf);  // row_shr:8: each row of 16 is scanned
+      scan_step<0x142, 0xa>(x, xf);  // row_bcast:15 into rows 1 and 3
+      scan_step<0x143, 0xc>(x, xf);  // row_bcast:31 into rows 2 and 3
 #pragma unroll
       for (int j = 0; j < 4; j++) {
         const int64_t e = x[j] - t[j];
-        limb[j][2 * lane] = e;
-        limb[j][2 * lane + 1] = e + a[j];
+        *cell_pair(limb[j], lane) = ll2{e, e + a[j]};
         if (lane == 63) limb[j][kCells] = x[j];
       }
       const int ef = xf - tf;
-      flag[2 * lane] = ef;
-      flag[2 * lane + 1] = ef + fa;
+      *reinterpret_cast<int2*>(flag + 2 * lane) = make_int2(ef, ef + fa);
       if (lane == 63) flag[kCells] = xf;
     }
     wave_lds_fence();
@@ -315,9 +364,11 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
       const int cnt = flag[t1] - flag[t0];
       double hb = __builtin_ldexp(join_limbs(limb[0][t1] - limb[0][t0], limb[1][t1] - limb[1][t0]), -sh_exp);
       double hwb = __builtin_ldexp(join_limbs(limb[2][t1] - limb[2][t0], limb[3][t1] - limb[3][t0]), -sw_exp);
-      // entries whose saliency fell below the fixed-point range: exact fp64 sums
-      uint64_t need = __ballot(live && cnt > 0 && !(hb > 0.0));
-      while (need) {  // uniform; does not occur unless h spans over 2^101 in a block
+      // entries whose saliency fell below the fixed-point range, and in a
+      // block with weights between tie thresholds the entries of codes 3 and 4:
+      // exact fp64 sums
+      uint64_t need = __ballot(live && ((cnt > 0 && !(hb > 0.0)) || (block_unsafe && (b == 3 || b == 4))));
+      while (need) {  // uniform; rare (h spanning over 2^101 in a block, or a weight at the tie)
         const int L = __builtin_ctzll(need);
         need &= need - 1;
         const int kL = k0 + (L >> 3), bL = L & 7;
@@ -331,12 +382,8 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
             sb += HW[i];
           }
         }
-        sa = run_sum<16>(sa);
-        sa += __shfl_xor(sa, 16, 64);
-        sa += __shfl_xor(sa, 32, 64);
-        sb = run_sum<16>(sb);
-        sb += __shfl_xor(sb, 16, 64);
-        sb += __shfl_xor(sb, 32, 64);
+        sa = rows_sum(run_sum<16>(sa));
+        sb = rows_sum(run_sum<16>(sb));
         if (lane == L) {
           hb = sa;
           hwb = sb;
@@ -358,9 +405,7 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
       // score: sum_b (C_b^2 H_b - 2 C_b HW_b) + sum h w^2, over the 8 lanes of the clip
       const double score = sww + run_sum<8>(cv * (cv * hb - 2.0 * hwb));
       double key = live ? make_key(score, k) : __longlong_as_double(0x7ff0000000000000ll);
-      double kmin = run_min_f64<16>(key);
-      kmin = fmin(kmin, __shfl_xor(kmin, 16, 64));
-      kmin = fmin(kmin, __shfl_xor(kmin, 32, 64));
+      const double kmin = rows_min_f64(run_min_f64<16>(key));
       if (kmin < best_key) {  // uniform
         best_key = kmin;
         if (k == key_index(kmin)) {  // the 8 lanes of the winning clip
@@ -419,16 +464,21 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
   }
 }
 
-template <bool W_BF16>
-hipError_t launch_e(const RubinParams& p, int ema_mode, hipStream_t s) {
+template <bool W_BF16, bool BK>
+hipError_t launch_b(const RubinParams& p, int ema_mode, hipStream_t s) {
   const int64_t blocks = p.batch.n > 1 ? p.batch.total_blocks : (p.n_blocks + kWaves - 1) / kWaves;
   const dim3 grid((unsigned)blocks), block(kThreads);
   switch (ema_mode) {
-    case 1: hipLaunchKernelGGL((rubin_reconstruct_kernel<W_BF16, 1>), grid, block, 0, s, p); break;
-    case 2: hipLaunchKernelGGL((rubin_reconstruct_kernel<W_BF16, 2>), grid, block, 0, s, p); break;
-    default: hipLaunchKernelGGL((rubin_reconstruct_kernel<W_BF16, 0>), grid, block, 0, s, p); break;
+    case 1: hipLaunchKernelGGL((rubin_reconstruct_kernel<W_BF16, 1, BK>), grid, block, 0, s, p); break;
+    case 2: hipLaunchKernelGGL((rubin_reconstruct_kernel<W_BF16, 2, BK>), grid, block, 0, s, p); break;
+    default: hipLaunchKernelGGL((rubin_reconstruct_kernel<W_BF16, 0, BK>), grid, block, 0, s, p); break;
   }
   return hipGetLastError();
+}
+
+template <bool W_BF16>
+hipError_t launch_e(const RubinParams& p, int ema_mode, hipStream_t s) {
+  return p.buckets ? launch_b<W_BF16, true>(p, ema_mode, s) : launch_b<W_BF16, false>(p, ema_mode, s);
 }
 
 }  // namespace

@@ -253,6 +253,29 @@ def _with_path(value, fn):
             os.environ["QUASAR_INT_PATH"] = old
 
 
+def test_rubin_cell_search_choice():
+    """How the Rubin kernel finds a weight's cell (host-only): the bucket table
+    for the paper's 15-factor grid and other spread grids, the tree search for
+    a grid too dense for three compares per bucket or with
+    QUASAR_RUBIN_PATH=tree."""
+    paper = tuple(np.float32(x) for x in np.round(np.arange(1.0, 0.29, -0.05), 2))
+    spread = [paper, (1.0,), tuple(np.linspace(1.0, 0.3, 8).astype(np.float32)),
+              tuple(np.linspace(1.0, 0.3, 16).astype(np.float32))]
+    dense = tuple(np.linspace(1.0, 0.9, 16).astype(np.float32))
+    for clips in spread:
+        assert Q.quasar_int_path(_int_desc(fmt="rubin", clips=clips)) == 1, clips
+    assert Q.quasar_int_path(_int_desc(fmt="rubin", clips=dense)) == 0
+    old = os.environ.get("QUASAR_RUBIN_PATH")
+    os.environ["QUASAR_RUBIN_PATH"] = "tree"
+    try:
+        assert Q.quasar_int_path(_int_desc(fmt="rubin", clips=paper)) == 0
+    finally:
+        if old is None:
+            os.environ.pop("QUASAR_RUBIN_PATH", None)
+        else:
+            os.environ["QUASAR_RUBIN_PATH"] = old
+
+
 def test_int_path_choice():
     """Which INT kernel serves a clip grid (host-only).  By default the binned
     kernel takes grids with few code thresholds per group lane (INT2, INT3 with

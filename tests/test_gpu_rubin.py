@@ -7,6 +7,7 @@ score's rounding floor), and a codebook byte whose oracle mean lies within
 1e-6 of an E4M3 rounding midpoint (the GPU rounds the mean through fp32);
 r of that index then follows the GPU's entry."""
 import itertools
+import os
 
 import numpy as np
 import pytest
@@ -32,21 +33,59 @@ def _f32(a):
     return (a.astype(np.uint32) << 16).view(np.float32) if a.dtype == np.uint16 else a
 
 
+class rubin_path:
+    """Run the Rubin kernel with the cells found one way: "auto" (the
+    library's choice) or "tree" (the binary search for every grid), set with
+    QUASAR_RUBIN_PATH."""
+
+    def __init__(self, path):
+        self.path = path
+
+    def __enter__(self):
+        self.old = os.environ.get("QUASAR_RUBIN_PATH")
+        if self.path == "auto":
+            os.environ.pop("QUASAR_RUBIN_PATH", None)
+        else:
+            os.environ["QUASAR_RUBIN_PATH"] = self.path
+
+    def __exit__(self, *exc):
+        if self.old is None:
+            os.environ.pop("QUASAR_RUBIN_PATH", None)
+        else:
+            os.environ["QUASAR_RUBIN_PATH"] = self.old
+
+
 def run_rubin(name, W, v, g=None, *, clips, weighting="h", row_step_blocks=1):
+    """Both ways of finding the cells (when the library's choice is the bucket
+    table, the tree search too), each from the same v, against one oracle run;
+    the first run updates the caller's v, as a single call does."""
     R, C = W.shape
     Wh, vh, gh = host(W), host(v), host(g)
-    print(f"[case] {name} shape={(R, C)} K={len(clips)} ema={g is not None} w={weighting}", flush=True)
-    out = Q.reconstruct(W, v, g, fmt="rubin", clips=clips, weighting=weighting)
-    torch.cuda.synchronize()
     brows = np.arange(0, R // 8, row_step_blocks)
     rows = (brows[:, None] * 8 + np.arange(8)[None, :]).ravel()
     bpr = C // 64
     bidx = (brows[:, None] * bpr + np.arange(bpr)[None, :]).ravel()
     o = oracle.rubin_reconstruct(Wh[rows], vh[rows], clips=clips, g=None if gh is None else gh[rows], beta2=0.999,
                                  weighting=weighting, want_scores=True, n_threads=THREADS)
+    d = Q.Descriptor(R, C, fmt="rubin", clips=clips)
+    paths = ("auto", "tree") if Q.quasar_int_path(d) == 1 else ("auto",)
+    v0 = v.clone() if len(paths) > 1 else None
+    for i, path in enumerate(paths):
+        vv = v if i == 0 else v0.clone()
+        with rubin_path(path):
+            form = "buckets" if Q.quasar_int_path(d) == 1 else "tree"
+            print(f"[case] {name} shape={(R, C)} K={len(clips)} ema={g is not None} w={weighting} path={path} "
+                  f"cells={form}", flush=True)
+            out = Q.reconstruct(W, vv, g, fmt="rubin", clips=clips, weighting=weighting)
+            torch.cuda.synchronize()
+        _check_rubin(name if path == "auto" else f"{name}.{path}", out, o, Wh, vv, g, rows, bidx, C, weighting)
+
+
+def _check_rubin(name, out, o, Wh, v, g, rows, bidx, C, weighting):
     fails, st = [], {"groups": len(bidx), "near_tie": 0, "near_e4m3": 0}
+    vh = host(v)
     if g is not None:
-        bad = np.count_nonzero(o["v_out"].view(np.uint32) != host(v)[rows].view(np.uint32))
+        bad = np.count_nonzero(o["v_out"].view(np.uint32) != vh[rows].view(np.uint32))
         if bad:
             fails.append(f"EMA v' differs in {bad} elements")
     h = o["v_out"] if g is not None else vh[rows]
@@ -184,3 +223,31 @@ def test_rubin_saliency_beyond_fixed_point_range():
     assert _entries_below_range(W.numpy(), v.numpy(), clips) > 0  # the case is exercised
     run_rubin("rubin.saliency-range", W.cuda(), v.cuda(), clips=clips)
     run_rubin("rubin.saliency-range.bf16", W.to(torch.bfloat16).cuda(), v.cuda(), clips=(1.0, 0.9, 0.75, 0.6))
+
+
+def test_rubin_weights_among_tie_thresholds():
+    """Weights whose normalised position lies between the clips' tie
+    thresholds T(k, 3) (just below u = 0, where the fp32 code rounding ties at
+    3.5), which the bucket table merges into one cell boundary: their blocks'
+    code-3 and code-4 entries are summed directly.  Every block has c = 0 and
+    rho = 1, so u = w, and 40 weights spread over the span."""
+    torch.manual_seed(11)
+    W = (torch.randn(16, 128) * 0.3).clamp(-0.9, 0.9).float()
+    v = torch.rand(16, 128).float() + 0.1
+    for rb in range(2):
+        for cb in range(2):
+            blk = W[8 * rb:8 * rb + 8, 64 * cb:64 * cb + 64]
+            blk[0, 0], blk[0, 1] = -1.0, 1.0
+            blk[1:6, 2:10] = -torch.linspace(3.3e-8, 1.0e-8, 40).reshape(5, 8)
+    clips = tuple(synth.clip_grid(1.0, 0.3, 15))
+    run_rubin("rubin.tie-span", W.cuda(), v.cuda(), clips=clips)
+    run_rubin("rubin.tie-span.bf16", W.to(torch.bfloat16).cuda(), v.cuda(), clips=clips)
+
+
+def test_rubin_dense_grid_takes_tree():
+    """A clip grid too dense for the bucket table (16 factors in [0.9, 1]):
+    the tree search serves it."""
+    clips = tuple(synth.clip_grid(1.0, 0.9, 16))
+    assert Q.quasar_int_path(Q.Descriptor(16, 128, fmt="rubin", clips=clips)) == 0
+    W, v, g = synth.gen_matrix(16, 128, 861, w_bf16=True, ema=True, device="cuda")
+    run_rubin("rubin.dense-grid", W, v, g, clips=clips)
