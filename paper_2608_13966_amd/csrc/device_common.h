@@ -242,6 +242,39 @@ __device__ __forceinline__ double run_min_f64(double x) {
   return x;
 }
 
+// op(x, x of lane l ^ 16) (ROWS = 16) or op(x, x of lane l ^ 32) (ROWS = 32)
+// without LDS: v_permlane16_swap / v_permlane32_swap of x with itself leave
+// the two rows (halves) of each pair in two registers, at the same positions
+// in both, so op of the two is the same value in every lane of the pair (for
+// a commutative op).
+template <int ROWS>
+__device__ __forceinline__ void swap_rows(uint32_t x, uint32_t& a, uint32_t& b) {
+  if constexpr (ROWS == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    a = r[0];
+    b = r[1];
+  } else {
+    const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+    a = r[0];
+    b = r[1];
+  }
+}
+template <int ROWS, typename Op>
+__device__ __forceinline__ float pair_rows(float x, Op op) {
+  uint32_t a, b;
+  swap_rows<ROWS>(as_u32(x), a, b);
+  return op(as_f32(a), as_f32(b));
+}
+template <int ROWS, typename Op>
+__device__ __forceinline__ double pair_rows(double x, Op op) {
+  const uint64_t u = (uint64_t)__double_as_longlong(x);
+  uint32_t alo, blo, ahi, bhi;
+  swap_rows<ROWS>((uint32_t)u, alo, blo);
+  swap_rows<ROWS>((uint32_t)(u >> 32), ahi, bhi);
+  return op(__longlong_as_double((long long)(((uint64_t)ahi << 32) | alo)),
+            __longlong_as_double((long long)(((uint64_t)bhi << 32) | blo)));
+}
+
 // Combine values that are uniform within each row of 16 over the wavefront's
 // four rows, without LDS: row_bcast:15 brings row 0's value into row 1 and
 // row 2's into row 3, row_bcast:31 brings lane 31's into rows 2 and 3 (rows

@@ -47,17 +47,38 @@ constexpr int N = kIntN;
 constexpr bool kSpread = true;
 constexpr int kMemberStride = kSpread ? 8 : 1;
 
+// The value x of the lane in the paired row (ROWS = 16: rows 0 <-> 1, 2 <-> 3)
+// or half (ROWS = 32), at the same position, for a lane in an even row (the
+// lower half) when `low` is set: the swap leaves the even rows' values in its
+// first result and the odd rows' in its second.
+template <int ROWS>
+__device__ __forceinline__ double paired(double x, bool low) {
+  const uint64_t u = (uint64_t)__double_as_longlong(x);
+  uint32_t alo, blo, ahi, bhi;
+  swap_rows<ROWS>((uint32_t)u, alo, blo);
+  swap_rows<ROWS>((uint32_t)(u >> 32), ahi, bhi);
+  return low ? __longlong_as_double((long long)(((uint64_t)bhi << 32) | blo))
+             : __longlong_as_double((long long)(((uint64_t)ahi << 32) | alo));
+}
+
 // Exclusive suffix sum over the members of a group: member j gets the sum of
-// the values of members j+1 .. L-1 (Hillis-Steele on the values shifted down
-// by one member).
+// the values of members j+1 .. L-1.  Members 2i and 2i+1 share a row of 16
+// (8 lanes apart), so member j's suffix is its row partner's value (j even)
+// plus the totals of the later rows, exchanged between rows and halves
+// without LDS.  The values are integers below 2^51: every sum is exact.
 template <int L>
 __device__ __forceinline__ double members_excl_suffix(double x, int j) {
-  double e = __shfl_down(x, kMemberStride);
-  if (j + 1 >= L) e = 0.0;
-#pragma unroll
-  for (int s = 1; s < L; s *= 2) {
-    const double y = __shfl_down(e, kMemberStride * s);
-    if (j + s < L) e += y;
+  static_assert(kSpread, "members 8 lanes apart");
+  const double nb = dpp_f64<kDppRor8>(x);  // member j ^ 1
+  double e = (j & 1) ? 0.0 : nb;
+  const double r = x + nb;                 // this row's two members
+  const int row = j >> 1;                  // the group's rows in order
+  const double t = paired<16>(r, (row & 1) == 0);
+  if constexpr (L == 4) {
+    if (row == 0) e += t;
+  } else {
+    const double o = paired<32>(r + t, row < 2);  // the other half's four members
+    e += ((row & 1) ? 0.0 : t) + (row < 2 ? o : 0.0);
   }
   return e;
 }

@@ -50,8 +50,8 @@ struct Members<L, true> {
       x = op(x, dpp_f64<kDppRor8>(x));
     else
       x = op(x, dpp_f32<kDppRor8>(x));
-    x = op(x, __shfl_xor(x, 16));
-    if constexpr (L == 8) x = op(x, __shfl_xor(x, 32));
+    x = pair_rows<16>(x, op);
+    if constexpr (L == 8) x = pair_rows<32>(x, op);
     return x;
   }
   static __device__ __forceinline__ float min(float x) { return reduce(x, [](float a, float b) { return fminf(a, b); }); }
