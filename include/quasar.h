@@ -199,7 +199,8 @@ typedef struct {
  *               taken from (e.g. last step's amax_out); the updated tensor's
  *               own absmax is not known before the pass.  INT: NULL.
  *  amax_out     NVFP4: optional device fp32, receives max |W'| for the next
- *               step (cleared and filled by the call).  INT: NULL.
+ *               step (cleared and filled by the call); not the tensor_amax
+ *               buffer (QUASAR_ERR_ARG).  INT: NULL.
  * No workspace is needed.  Returns a quasar_status; on error nothing is
  * launched and W, m, v are untouched.
  */

@@ -654,6 +654,8 @@ int quasar_adamw_check(const quasar_desc* d, const quasar_adamw* opt, const void
                        d->format == QUASAR_NVFP4 ? tensor_amax : nullptr, nullptr, 0);
   if (s != QUASAR_OK) return s;
   if (d->format == QUASAR_INT && (tensor_amax != nullptr || amax_out != nullptr)) return QUASAR_ERR_ARG;
+  // amax_out is cleared before the pass that reads tensor_amax
+  if (amax_out != nullptr && amax_out == tensor_amax) return QUASAR_ERR_ARG;
   if (!aligned16(m) || !aligned16(amax_out)) return QUASAR_ERR_ALIGN;
   if (r_dtype != QUASAR_F32 && r_dtype != QUASAR_BF16) return QUASAR_ERR_FORMAT;
   if (d->w_dtype == QUASAR_BF16 && r_dtype != QUASAR_BF16) return QUASAR_ERR_FORMAT;

@@ -149,11 +149,12 @@ def test_adamw_entry_point_validation():
     assert _adam_check(f32, r_dtype=Q.F16) == Q.ERR_FORMAT
     nv = _int_desc(fmt="nvfp4", w_dtype=Q.F32)
     assert _adam_check(nv) == Q.OK
-    assert _adam_check(nv, amax_out=A) == Q.OK
+    assert _adam_check(nv, amax_out=A + 16) == Q.OK
+    assert _adam_check(nv, amax_out=A) == Q.ERR_ARG            # the same buffer as tensor_amax
     assert _adam_check(nv, tensor_amax=None) == Q.ERR_ARG      # the tensor scale needs an amax
     assert _adam_check(f32, tensor_amax=A) == Q.ERR_ARG
     assert _adam_check(f32, amax_out=A) == Q.ERR_ARG
-    assert _adam_check(nv, amax_out=A + 4) == Q.ERR_ALIGN
+    assert _adam_check(nv, amax_out=A + 20) == Q.ERR_ALIGN
     for name in ("m", "g", "W", "v", "codes", "scales"):
         assert _adam_check(f32, **{name: None}) == Q.ERR_ARG, name
     assert _adam_check(f32, m=A + 8) == Q.ERR_ALIGN
