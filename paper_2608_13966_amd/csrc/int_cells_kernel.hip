@@ -24,10 +24,12 @@
 // gives the thresholds below the bucket and the next three thresholds), its
 // cell, then h and h w added into the group's cell as exact int64 values
 // (LDS atomics).  A group's lanes are spread over the wavefront (8 apart), so
-// members of one group that hit the same cell do not serialise the atomic.  Per group: suffix sums over the cells (each of the L lanes takes a
-// chunk; the chunk totals are combined across lanes), then each lane
-// assembles the moments of the clips it owns from NB suffix sums each and
-// solves and scores them exactly as the direct form does (int_common.h).
+// members of one group that hit the same cell do not serialise the atomic.
+// Per group: suffix sums over the cells (each of the L lanes takes a chunk;
+// the chunk totals are combined across lanes with DPP and permlane swaps),
+// then each lane assembles the moments of the clips it owns from NB suffix
+// sums each and solves and scores them exactly as the direct form does
+// (int_common.h).
 // The emitted codes are recomputed from u with the fp32 recipe, so they are
 // bit-identical to the direct form's.
 #include <type_traits>

@@ -12,12 +12,16 @@
 // Every code is a non-decreasing function of u, so the codes a weight gets
 // under all K clips are fixed by how many of the 7K per-clip thresholds
 // T(k, b) = min{u : q_k(u) >= b + 1} lie at or below u.  That count -- the
-// weight's cell, 0 .. 7K -- is what the kernel bins by, once per block: the
-// thresholds are exact fp32 values found on the host and passed as an implicit
-// binary search tree (node n's children at 2n and 2n + 1), and
+// weight's cell, 0 .. 7K -- is what the kernel bins by, once per block, and
 // for clip k the weights with code b are exactly the cells in a fixed range
 // [tpos(k, b), tpos(k, b + 1)).  The per-clip work then reads two prefix sums
-// per codebook entry instead of re-binning 512 weights.
+// per codebook entry instead of re-binning 512 weights.  The thresholds are
+// exact fp32 values found on the host.  A weight finds its cell either from
+// a table over 256 equal slices of u plus at most three compares (BK, the
+// bucket form, with the clips' tie thresholds just below u = 0 merged into
+// one; a block with a weight between them sums its code-3 and code-4 entries
+// directly) or by descending an implicit binary search tree over all of them
+// (node n's children at 2n and 2n + 1; any clip grid).
 //
 // The cell sums of h and h w are kept exact, as integers: each value is
 // scaled by a power of two fixed per block (from the block's largest h and
@@ -44,7 +48,7 @@ namespace {
 
 constexpr int NE = 8;          // weights per lane
 constexpr int kWaves = kThreads / 64;
-constexpr int kCells = kRubinThresholds;  // cell ids 0 .. 7K <= 112 < 128
+constexpr int kCells = kRubinThresholds;  // cell ids 0 .. 7K <= 112 < 128 (fewer in the bucket form)
 constexpr int kHiBits = 51;    // |scaled value| < 2^51: its nearest integer is the high limb
 constexpr int kLoBits = 50;    // the remainder, scaled by 2^50 and rounded, is the low limb
 constexpr double kMagic = 6755399441055744.0;  // 1.5 * 2^52: x + kMagic rounds x to an integer
