@@ -178,8 +178,8 @@ def main(argv=None):
     args = ap.parse_args(argv)
 
     if args.gpus != 1:
-        print(f"bench.py: this build runs on exactly one GPU (asked for {args.gpus}); the reconstruction "
-              "shards by rows or whole matrices with no communication, but no multi-GPU path is built.",
+        print(f"bench.py: runs on exactly one GPU (asked for {args.gpus}); the reconstruction would shard "
+              "by rows or whole matrices with no communication, but no multi-GPU path exists.",
               file=sys.stderr)
         return 2
 
