@@ -290,7 +290,19 @@ void rubin_thresholds(quasar::RubinParams& p, int K) {
   int n = 0;
   for (int k = 0; k < K; k++) {
     for (int b = 0; b < 7; b++) {
+      // bracket: around the threshold of exact arithmetic, (b - 3) / alpha,
+      // widened until it holds (else the whole range)
+      const double center = (b - 3.0) / (double)p.alpha[k];
       uint32_t lo = f32_order_key(-INFINITY), hi = f32_order_key(INFINITY);
+      for (double half = 1e-6; half < 4.0; half *= 16.0) {
+        const uint32_t a = f32_order_key((float)(center - half)), z = f32_order_key((float)(center + half));
+        if (rubin_code(f32_from_order_key(a), p.alpha[k]) < b + 1 &&
+            rubin_code(f32_from_order_key(z), p.alpha[k]) >= b + 1) {
+          lo = a;
+          hi = z;
+          break;
+        }
+      }
       while (hi - lo > 1) {
         const uint32_t mid = lo + (hi - lo) / 2;
         if (rubin_code(f32_from_order_key(mid), p.alpha[k]) >= b + 1)
