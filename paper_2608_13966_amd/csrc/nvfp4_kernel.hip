@@ -344,8 +344,9 @@ __device__ __forceinline__ float chunk_absmax(uint4 t) {
 
 // One workgroup per span of kAbsChunks 16-byte chunks of one matrix: lane t
 // loads chunks t, t + 256, ... (each load instruction reads 1 KB contiguous per
-// wavefront), all kAbsSpan loads in flight at once; then a DPP / LDS maximum
-// and one atomicMax on the fp32 bit pattern per workgroup.
+// wavefront), kAbsBatch loads in flight at a time; then a DPP / LDS maximum
+// and one atomicMax on the fp32 bit pattern per workgroup (a larger span means
+// fewer workgroups meeting on one address).
 constexpr int64_t kAbsChunks = (int64_t)kThreads * kAbsSpan;
 
 template <bool W_BF16>
@@ -365,18 +366,20 @@ __global__ __launch_bounds__(kThreads) void absmax_kernel(AbsmaxTable t) {
   const uint4* src = reinterpret_cast<const uint4*>(kt->W[mi]);
   const int64_t n_chunks = kt->n_chunks[mi];
   const int64_t c0 = blk * kAbsChunks + threadIdx.x;
-  uint4 buf[kAbsSpan];
-#pragma unroll
-  for (int u = 0; u < kAbsSpan; u++) {
-    const int64_t c = c0 + (int64_t)u * kThreads;
-    buf[u] = c < n_chunks ? src[c] : make_uint4(0u, 0u, 0u, 0u);
-  }
+  // batches of kAbsBatch loads in flight at a time
   float m = 0.0f;
+#pragma unroll 1
+  for (int b0 = 0; b0 < kAbsSpan; b0 += kAbsBatch) {
+    uint4 buf[kAbsBatch];
 #pragma unroll
-  for (int u = 0; u < kAbsSpan; u++) m = fmaxf(m, chunk_absmax<W_BF16>(buf[u]));
-  m = run_max<16>(m);
-  m = fmaxf(m, __shfl_xor(m, 16, 64));
-  m = fmaxf(m, __shfl_xor(m, 32, 64));
+    for (int u = 0; u < kAbsBatch; u++) {
+      const int64_t c = c0 + (int64_t)(b0 + u) * kThreads;
+      buf[u] = c < n_chunks ? src[c] : make_uint4(0u, 0u, 0u, 0u);
+    }
+#pragma unroll
+    for (int u = 0; u < kAbsBatch; u++) m = fmaxf(m, chunk_absmax<W_BF16>(buf[u]));
+  }
+  m = rows_max(run_max<16>(m));
   if ((threadIdx.x & 63) == 0) s_m[threadIdx.x >> 6] = m;
   __syncthreads();
   if (threadIdx.x == 0) {
