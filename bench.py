@@ -268,7 +268,7 @@ def main(argv=None):
 
     # ---- launch plan: per matrix, or batched runs of up to MAX_BATCH matrices ----
     nv = wl.fmt == "nvfp4" and not wl.adamw   # the plain NVFP4 path runs its absmax pass every step
-    batched = args.launch == "batch" and not wl.adamw
+    batched = args.launch == "batch"
     plans = []
     for ci in range(copies):
         ms = mats[ci * per_step:(ci + 1) * per_step]
@@ -276,7 +276,7 @@ def main(argv=None):
         plan = []
         for grp in grps:
             arr = None
-            if len(grp) > 1:
+            if len(grp) > 1 and not wl.adamw:  # the fused step's arrays are built per step (see launch_group)
                 arr = (Q.Matrix * len(grp))(*[Q.matrix(m["W"], m["v"], m["g"], m["out"], m["out"]["amax"])
                                               for m in grp])
                 if nv:  # the group's absmax passes in one launch as well
@@ -294,6 +294,23 @@ def main(argv=None):
             raise Q.QuasarError(s, "quasar_absmax_batch")
 
     def launch_group(grp, arr):
+        if wl.adamw and len(grp) > 1:
+            # one batched optimiser step + reconstruction; NVFP4 takes this
+            # step's tensor scale from the previous step's max |W'| by-products
+            opt = Q.AdamW(1e-5, 0.9, wl.beta2, 1e-8, 0.01, step_no[0] + 1)
+            am = [Q.AdamWMatrix(m["W"].shape[0], m["W"].shape[1], Q._p(m["W"]), Q._p(m["m"]), Q._p(m["v"]),
+                                Q._p(m["g"]), Q._p(m["out"]["codes"]), Q._p(m["out"]["scales"]),
+                                Q._p(m["out"]["zeros"]), Q._p(m["out"]["r"]), None, None,
+                                Q._p(m["out"]["tensor_scale"]), Q._p(m["out"]["amax"]), Q._p(m["out"]["amax2"]))
+                  for m in grp]
+            s = Q.quasar_adamw_reconstruct_batch(grp[0]["d"], opt, am, Q.BF16, stream.cuda_stream)
+            if s != Q.OK:
+                raise Q.QuasarError(s, "quasar_adamw_reconstruct_batch")
+            for m in grp:
+                o = m["out"]
+                if o["amax"] is not None:
+                    o["amax"], o["amax2"] = o["amax2"], o["amax"]
+            return
         if arr is None:
             launch(grp[0])
             return

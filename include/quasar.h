@@ -253,6 +253,41 @@ int quasar_reconstruct_batch(const quasar_desc* desc, const quasar_matrix* mats,
 int quasar_batch_check(const quasar_desc* desc, const quasar_matrix* mats, int n_mats);
 
 /*
+ * The fused AdamW step and reconstruction of quasar_adamw_reconstruct over
+ * several matrices in one launch (e.g. the seven projections of a transformer
+ * layer), with the same results as one call per matrix.  desc, opt and r_dtype
+ * are shared (desc's rows/cols and beta2 are ignored); each
+ * quasar_adamw_matrix gives a matrix's shape and buffers with the meaning and
+ * requirements of the same-named quasar_adamw_reconstruct arguments (W is
+ * updated in place).  Every amax_out given is cleared before the pass, so none
+ * may be any matrix's tensor_amax.  1 <= n_mats <= QUASAR_MAX_BATCH.  Returns
+ * a quasar_status; on error nothing is launched.
+ */
+typedef struct {
+  int64_t rows, cols;
+  void* W;
+  float* m;
+  float* v;
+  const void* g;
+  uint8_t* codes;
+  void* scales;
+  float* zeros;
+  void* r;
+  uint8_t* best_clip;
+  float* err;
+  float* tensor_scale;
+  const float* tensor_amax;
+  float* amax_out;
+} quasar_adamw_matrix;
+
+int quasar_adamw_reconstruct_batch(const quasar_desc* desc, const quasar_adamw* opt,
+                                   const quasar_adamw_matrix* mats, int n_mats, int r_dtype, void* stream);
+
+/* Host-only validation: the status quasar_adamw_reconstruct_batch would return. */
+int quasar_adamw_batch_check(const quasar_desc* desc, const quasar_adamw* opt, const quasar_adamw_matrix* mats,
+                             int n_mats, int r_dtype);
+
+/*
  * Tensor absmax (Sec. 4.2, as quasar_absmax) of up to QUASAR_MAX_BATCH NVFP4
  * matrices in one launch, e.g. ahead of quasar_reconstruct_batch.  Of each
  * quasar_matrix only rows, cols and W are read (desc gives the format and W's

@@ -168,6 +168,21 @@ int quasar_absmax_batch(const quasar_desc* d, const quasar_matrix* mats, int n_m
 
 namespace {
 
+// One AdamW step's host constants, fp64 then fp32 (the same expressions as
+// the oracle's).
+quasar::AdamWConsts adamw_consts(const quasar_adamw* opt) {
+  quasar::AdamWConsts a;
+  a.beta1 = opt->beta1;
+  a.omb1 = 1.0f - opt->beta1;
+  a.eps = opt->eps;
+  a.decay = (float)(1.0 - (double)opt->lr * (double)opt->weight_decay);
+  const double bc1 = 1.0 - pow((double)opt->beta1, (double)opt->step);
+  const double bc2 = 1.0 - pow((double)opt->beta2, (double)opt->step);
+  a.step_size = (float)((double)opt->lr / bc1);
+  a.rbc2 = (float)(1.0 / sqrt(bc2));
+  return a;
+}
+
 // The clip tables of the INT kernels: f_k and the code scale alpha_k
 // (qmax / (2 f_k), symmetric Q / f_k, fp32 division); entries past K repeat
 // the last clip.
@@ -687,20 +702,92 @@ int quasar_adamw_reconstruct(const quasar_desc* d, const quasar_adamw* opt, void
   if (s != QUASAR_OK) return s;
   quasar_desc dd = *d;
   dd.beta2 = opt->beta2;  // the optimiser's decay updates v
-  // host constants, fp64 then fp32 (the same expressions as the oracle's)
-  quasar::AdamWConsts a;
-  a.beta1 = opt->beta1;
-  a.omb1 = 1.0f - opt->beta1;
-  a.eps = opt->eps;
-  a.decay = (float)(1.0 - (double)opt->lr * (double)opt->weight_decay);
-  const double bc1 = 1.0 - pow((double)opt->beta1, (double)opt->step);
-  const double bc2 = 1.0 - pow((double)opt->beta2, (double)opt->step);
-  a.step_size = (float)((double)opt->lr / bc1);
-  a.rbc2 = (float)(1.0 / sqrt(bc2));
+  const quasar::AdamWConsts a = adamw_consts(opt);
   const int ema_mode = dd.g_dtype == QUASAR_BF16 ? 3 : 4;
   return launch_path(&dd, W, W, m, v, g, ema_mode, &a, codes, scales, zeros, r, r_dtype == QUASAR_BF16,
                      best_clip, err, tensor_scale, tensor_amax, amax_out, nullptr,
                      reinterpret_cast<hipStream_t>(stream));
+}
+
+int quasar_adamw_batch_check(const quasar_desc* d, const quasar_adamw* opt, const quasar_adamw_matrix* mats,
+                             int n_mats, int r_dtype) {
+  if (d == nullptr || opt == nullptr || mats == nullptr || n_mats < 1 || n_mats > QUASAR_MAX_BATCH)
+    return QUASAR_ERR_ARG;
+  int64_t total = 0;
+  for (int i = 0; i < n_mats; i++) {
+    const quasar_adamw_matrix& x = mats[i];
+    quasar_desc dd = *d;
+    dd.rows = x.rows;
+    dd.cols = x.cols;
+    const int s = quasar_adamw_check(&dd, opt, x.W, x.m, x.v, x.g, x.codes, x.scales, x.zeros, x.r, r_dtype,
+                                     x.best_clip, x.err, x.tensor_scale, x.tensor_amax, x.amax_out);
+    if (s != QUASAR_OK) return s;
+    // every amax_out is cleared before the pass that reads the tensor_amax
+    for (int k = 0; k < n_mats; k++)
+      if (x.amax_out != nullptr && x.amax_out == mats[k].tensor_amax) return QUASAR_ERR_ARG;
+    const int64_t upb = d->format == QUASAR_NVFP4 ? quasar::nvfp4_units_per_block()
+                                                  : quasar::int_units_per_block(d->group);
+    total += (quasar_num_groups(&dd) + upb - 1) / upb;
+  }
+  if (total >= ((int64_t)1 << 31)) return QUASAR_ERR_SHAPE;  // one grid
+  return QUASAR_OK;
+}
+
+int quasar_adamw_reconstruct_batch(const quasar_desc* d, const quasar_adamw* opt,
+                                   const quasar_adamw_matrix* mats, int n_mats, int r_dtype, void* stream) {
+  const int s = quasar_adamw_batch_check(d, opt, mats, n_mats, r_dtype);
+  if (s != QUASAR_OK) return s;
+  const quasar_adamw_matrix& x0 = mats[0];
+  if (n_mats == 1)
+    return quasar_adamw_reconstruct(d, opt, x0.W, x0.m, x0.v, x0.g, x0.codes, x0.scales, x0.zeros, x0.r, r_dtype,
+                                    x0.best_clip, x0.err, x0.tensor_scale, x0.tensor_amax, x0.amax_out, stream);
+  const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  quasar::BatchTable bt;
+  memset(&bt, 0, sizeof(bt));
+  bt.n = n_mats;
+  quasar::AbsmaxTable clear;  // the amax_out buffers given
+  memset(&clear, 0, sizeof(clear));
+  const int64_t upb =
+      d->format == QUASAR_NVFP4 ? quasar::nvfp4_units_per_block() : quasar::int_units_per_block(d->group);
+  for (int i = 0; i < n_mats; i++) {
+    const quasar_adamw_matrix& x = mats[i];
+    quasar_desc dd = *d;
+    dd.rows = x.rows;
+    dd.cols = x.cols;
+    quasar::MatrixSlot& ms = bt.s[i];
+    ms.W = x.W;
+    ms.v = x.v;
+    ms.g = x.g;
+    ms.codes = x.codes;
+    ms.scales = x.scales;
+    ms.zeros = x.zeros;
+    ms.r = x.r;
+    ms.best_clip = x.best_clip;
+    ms.err = x.err;
+    ms.tensor_scale = x.tensor_scale;
+    ms.amax = x.tensor_amax;
+    ms.m = x.m;
+    ms.Wu = x.W;
+    ms.amax_out = reinterpret_cast<unsigned*>(x.amax_out);
+    if (x.amax_out != nullptr) clear.out[clear.n++] = ms.amax_out;
+    ms.n_units = quasar_num_groups(&dd);
+    ms.block0 = bt.total_blocks;
+    ms.cols = x.cols;
+    ms.blocks_per_row = x.cols / 64;
+    bt.total_blocks += (ms.n_units + upb - 1) / upb;
+  }
+  if (clear.n > 0 && quasar::launch_clear_all(clear, st) != hipSuccess) return QUASAR_ERR_DEVICE;
+  // the shared fields come from the descriptor; slot 0 also fills the
+  // single-matrix fields (the by-products are the slots')
+  quasar_desc d0 = *d;
+  d0.rows = x0.rows;
+  d0.cols = x0.cols;
+  d0.beta2 = opt->beta2;
+  const quasar::AdamWConsts a = adamw_consts(opt);
+  const int ema_mode = d0.g_dtype == QUASAR_BF16 ? 3 : 4;
+  return launch_path(&d0, x0.W, x0.W, x0.m, x0.v, x0.g, ema_mode, &a, x0.codes, x0.scales, x0.zeros, x0.r,
+                     r_dtype == QUASAR_BF16, x0.best_clip, x0.err, x0.tensor_scale, x0.tensor_amax, nullptr,
+                     nullptr, st, &bt);
 }
 
 }  // extern "C"

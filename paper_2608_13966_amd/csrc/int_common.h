@@ -75,14 +75,16 @@ struct IntMatrix {
   uint8_t* best_clip;
   float* err;
   int64_t n_groups;
+  float* m;  // the fused AdamW step: first moment and where the updated W goes
+  void* Wu;
 };
 
 __device__ __forceinline__ IntMatrix int_matrix(const IntParams& p, int64_t& blk) {
-  IntMatrix m = {p.W, p.v, p.g, p.codes, p.scales, p.zeros, p.r, p.best_clip, p.err, p.n_groups};
+  IntMatrix m = {p.W, p.v, p.g, p.codes, p.scales, p.zeros, p.r, p.best_clip, p.err, p.n_groups, p.m, p.Wu};
   if (p.batch.n > 1) {
     const MatrixSlot& ms = batch_slot<IntParams>(blk);
     m = {ms.W, ms.v, ms.g, ms.codes, static_cast<float*>(ms.scales), ms.zeros, ms.r, ms.best_clip, ms.err,
-         ms.n_units};
+         ms.n_units, ms.m, ms.Wu};
   }
   return m;
 }
@@ -112,15 +114,15 @@ __device__ __forceinline__ void int_load(const IntParams& p, const IntMatrix& mt
     // second moment is the saliency
     float g[kIntN], m[kIntN], w[kIntN];
     load16<EMA == 3>(mtx.g, e0, g);
-    load16<false>(p.m, e0, m);
+    load16<false>(mtx.m, e0, m);
 #pragma unroll
     for (int i = 0; i < kIntN; i++) w[i] = wr.get(i);
     adamw16(w, m, v, g, p.adam, p.beta2, p.omb2);
     wr.set(w);  // bf16 W: rounded here, and the rounded value is reconstructed
     if (active) {
       store16<false>(mtx.v, e0, v);
-      store16<false>(p.m, e0, m);
-      wr.store(p.Wu, e0);
+      store16<false>(mtx.m, e0, m);
+      wr.store(mtx.Wu, e0);
     }
   }
   if (p.weighting != 0) {

@@ -96,11 +96,15 @@ void nvfp4_reconstruct_kernel(Nvfp4Params p) {
     float* tensor_scale;
     const float* amax;
     int64_t n_blocks;
-  } mtx = {p.W, p.v, p.g, p.codes, p.scales, p.r, p.best_clip, p.err, p.tensor_scale, p.amax, p.n_blocks};
+    float* m;  // the fused AdamW step
+    void* Wu;
+    unsigned* amax_out;
+  } mtx = {p.W, p.v, p.g, p.codes, p.scales, p.r, p.best_clip, p.err, p.tensor_scale, p.amax, p.n_blocks,
+           p.m, p.Wu, p.amax_out};
   if (p.batch.n > 1) {
     const MatrixSlot& ms = batch_slot<Nvfp4Params>(blk);
     mtx = {ms.W, ms.v, ms.g, ms.codes, static_cast<uint8_t*>(ms.scales), ms.r, ms.best_clip, ms.err,
-         ms.tensor_scale, ms.amax, ms.n_units};
+         ms.tensor_scale, ms.amax, ms.n_units, ms.m, ms.Wu, ms.amax_out};
   }
   int64_t bid = blk * kThreads + tid;
   const bool active = bid < mtx.n_blocks;
@@ -125,15 +129,15 @@ void nvfp4_reconstruct_kernel(Nvfp4Params p) {
     // one AdamW step first (see int_kernel.hip)
     float g[N], m[N], w[N];
     load16<EMA == 3>(mtx.g, e0, g);
-    load16<false>(p.m, e0, m);
+    load16<false>(mtx.m, e0, m);
 #pragma unroll
     for (int i = 0; i < N; i++) w[i] = wr.get(i);
     adamw16(w, m, v, g, p.adam, p.beta2, p.omb2);
     wr.set(w);
     if (active) {
       store16<false>(mtx.v, e0, v);
-      store16<false>(p.m, e0, m);
-      wr.store(p.Wu, e0);
+      store16<false>(mtx.m, e0, m);
+      wr.store(mtx.Wu, e0);
     }
   }
   if (p.weighting != 0) {  // h = v, v*v or 1 (uniform branch)
@@ -291,12 +295,12 @@ void nvfp4_reconstruct_kernel(Nvfp4Params p) {
     // by-product of the fused step: max |W'| for the next step's tensor scale.
     // One atomic per wavefront, skipped when the stored maximum is already
     // larger (|w| >= 0, so fp32 bit patterns order like unsigned integers).
-    if (p.amax_out) {
+    if (mtx.amax_out) {
       float mw = run_max<16>(m);
       mw = fmaxf(mw, __shfl_xor(mw, 16, 64));
       mw = fmaxf(mw, __shfl_xor(mw, 32, 64));
-      if ((tid & 63) == 0 && __float_as_uint(mw) > __builtin_nontemporal_load(p.amax_out))
-        atomicMax(p.amax_out, __float_as_uint(mw));
+      if ((tid & 63) == 0 && __float_as_uint(mw) > __builtin_nontemporal_load(mtx.amax_out))
+        atomicMax(mtx.amax_out, __float_as_uint(mw));
     }
   }
   if (!active) return;
@@ -426,6 +430,11 @@ hipError_t launch_nvfp4(const Nvfp4Params& p, bool w_bf16, int ema_mode, hipStre
 
 hipError_t launch_clear(unsigned* ws, hipStream_t s) {
   hipLaunchKernelGGL(absmax_clear_kernel, dim3(1), dim3(64), 0, s, ws);
+  return hipGetLastError();
+}
+
+hipError_t launch_clear_all(const AbsmaxTable& t, hipStream_t s) {
+  hipLaunchKernelGGL(absmax_clear_all_kernel, dim3(1), dim3(64), 0, s, t);
   return hipGetLastError();
 }
 

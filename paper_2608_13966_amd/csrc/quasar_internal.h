@@ -32,6 +32,11 @@ struct MatrixSlot {
   int64_t block0;
   int64_t cols;
   int64_t blocks_per_row;
+  // the fused AdamW step: first moment, where the updated W goes, and the
+  // by-product max |W'| (or NULL)
+  float* m;
+  void* Wu;
+  unsigned* amax_out;
 };
 
 // n > 1: the launch covers n matrices; workgroup b works on the last slot with
@@ -237,4 +242,6 @@ hipError_t launch_absmax(const void* W, bool w_bf16, int64_t n, unsigned* ws, hi
 // gradient, 3 = AdamW step from a bf16 gradient, 4 = AdamW step from an fp32 gradient
 // clear *ws to 0 (a kernel, so that it may be captured in a graph)
 hipError_t launch_clear(unsigned* ws, hipStream_t s);
+// Clear out[0 .. n) of the table (one one-wavefront kernel).
+hipError_t launch_clear_all(const AbsmaxTable& t, hipStream_t s);
 }  // namespace quasar

@@ -5,10 +5,10 @@ kernels behind ``quasar_reconstruct``.  Tensors are torch tensors on the GPU
 (torch supplies device memory and the current stream); there is no CPU path,
 and a missing library raises instead of falling back.
 
-The functions ``quasar_reconstruct``, ``quasar_absmax``, ``quasar_check``, ``quasar_num_groups``,
-``quasar_int_path``, ``quasar_codes_bytes``, ``quasar_workspace_bytes``, ``quasar_status_string`` and
-``quasar_version`` mirror the C entry points one to one; ``reconstruct`` is a
-convenience wrapper that allocates the outputs and calls ``quasar_reconstruct``.
+The functions named ``quasar_*`` (``EXPORTS``) mirror the C entry points one
+to one; ``reconstruct``, ``reconstruct_batch``, ``adamw_reconstruct``,
+``adamw_reconstruct_batch`` and ``absmax_batch`` are convenience wrappers that
+allocate the outputs and call them.
 """
 from __future__ import annotations
 
@@ -31,6 +31,7 @@ MAX_CLIPS = 16
 
 EXPORTS = ("quasar_reconstruct", "quasar_absmax", "quasar_check", "quasar_adamw_reconstruct", "quasar_adamw_check",
            "quasar_reconstruct_batch", "quasar_batch_check", "quasar_absmax_batch", "quasar_absmax_batch_check",
+           "quasar_adamw_reconstruct_batch", "quasar_adamw_batch_check",
            "quasar_num_groups", "quasar_int_path", "quasar_codes_bytes",
            "quasar_workspace_bytes", "quasar_status_string", "quasar_version")
 MAX_BATCH = 16
@@ -55,6 +56,14 @@ class Matrix(C.Structure):
                 ("codes", C.c_void_p), ("scales", C.c_void_p), ("zeros", C.c_void_p), ("r", C.c_void_p),
                 ("best_clip", C.c_void_p), ("err", C.c_void_p), ("tensor_scale", C.c_void_p),
                 ("tensor_amax", C.c_void_p)]
+
+
+class AdamWMatrix(C.Structure):
+    """quasar_adamw_matrix: one matrix of a batched fused AdamW call."""
+    _fields_ = [("rows", C.c_int64), ("cols", C.c_int64), ("W", C.c_void_p), ("m", C.c_void_p), ("v", C.c_void_p),
+                ("g", C.c_void_p), ("codes", C.c_void_p), ("scales", C.c_void_p), ("zeros", C.c_void_p),
+                ("r", C.c_void_p), ("best_clip", C.c_void_p), ("err", C.c_void_p), ("tensor_scale", C.c_void_p),
+                ("tensor_amax", C.c_void_p), ("amax_out", C.c_void_p)]
 
 
 class AdamW(C.Structure):
@@ -94,6 +103,11 @@ def lib():
             L.quasar_reconstruct_batch.restype = C.c_int
             L.quasar_batch_check.argtypes = [dp, mp, C.c_int]
             L.quasar_batch_check.restype = C.c_int
+            amp = C.POINTER(AdamWMatrix)
+            L.quasar_adamw_reconstruct_batch.argtypes = [dp, ap, amp, C.c_int, C.c_int, vp]
+            L.quasar_adamw_reconstruct_batch.restype = C.c_int
+            L.quasar_adamw_batch_check.argtypes = [dp, ap, amp, C.c_int, C.c_int]
+            L.quasar_adamw_batch_check.restype = C.c_int
             pp = C.POINTER(vp)
             L.quasar_absmax_batch.argtypes = [dp, mp, C.c_int, pp, vp]
             L.quasar_absmax_batch.restype = C.c_int
@@ -178,6 +192,17 @@ def quasar_adamw_check(d: Descriptor, opt: AdamW, W, m, v, g, codes, scales, zer
     return lib().quasar_adamw_check(d.ref, None if opt is None else C.byref(opt), _p(W), _p(m), _p(v), _p(g),
                                     _p(codes), _p(scales), _p(zeros), _p(r), int(r_dtype), _p(best_clip), _p(err),
                                     _p(tensor_scale), _p(tensor_amax), _p(amax_out))
+
+
+def quasar_adamw_reconstruct_batch(d: Descriptor, opt: AdamW, mats, r_dtype: int, stream) -> int:
+    arr = (AdamWMatrix * len(mats))(*mats)
+    return lib().quasar_adamw_reconstruct_batch(d.ref, C.byref(opt), arr, len(mats), int(r_dtype), stream)
+
+
+def quasar_adamw_batch_check(d: Descriptor, opt: AdamW, mats, r_dtype: int) -> int:
+    arr = (AdamWMatrix * max(1, len(mats)))(*mats)
+    return lib().quasar_adamw_batch_check(d.ref, None if opt is None else C.byref(opt), arr, len(mats),
+                                          int(r_dtype))
 
 
 def matrix(W, v, g, out, tensor_amax=None) -> Matrix:
@@ -346,6 +371,46 @@ def adamw_reconstruct(W, m, v, g, *, lr, beta1=0.9, beta2=0.999, eps=1e-8, weigh
         raise QuasarError(s, "quasar_adamw_reconstruct")
     out["desc"] = d
     return out
+
+
+def adamw_reconstruct_batch(items, *, lr, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, step=1,
+                            fmt="int", bits=4, group=128, clips=(1.0,), r_dtype=None, want_r=True, want_diag=True,
+                            want_amax_out=False, stream=None, weighting="h", param_dtype="fp32"):
+    """One batched fused AdamW step + reconstruction
+    (quasar_adamw_reconstruct_batch) over ``items``: a list of (W, m, v, g)
+    or, for NVFP4, (W, m, v, g, tensor_amax), with one W dtype and one g
+    dtype.  W, m, v are updated in place.  Returns one output dict per matrix,
+    as adamw_reconstruct()."""
+    import torch
+    W0, g0 = items[0][0], items[0][3]
+    d = Descriptor(W0.shape[0], W0.shape[1], fmt=fmt, bits=bits, group=group, clips=clips,
+                   w_dtype=_dtype_code(W0), g_dtype=_dtype_code(g0), beta2=beta2, weighting=weighting,
+                   param_dtype=param_dtype)
+    rd = BF16 if r_dtype in (None, "bf16") else F32
+    outs, mats = [], []
+    for it in items:
+        W, m, v, g = it[:4]
+        amax = it[4] if len(it) > 4 else None
+        dd = Descriptor(W.shape[0], W.shape[1], fmt=fmt, bits=bits, group=group, clips=clips,
+                        w_dtype=_dtype_code(W), g_dtype=_dtype_code(g), beta2=beta2, weighting=weighting,
+                        param_dtype=param_dtype)
+        o = alloc_outputs(dd, W, want_r=False, want_diag=want_diag, has_amax=True)
+        if want_r:
+            o["r"] = torch.empty(W.shape, dtype=torch.bfloat16 if rd == BF16 else torch.float32, device=W.device)
+        o["amax_out"] = (torch.empty(4, dtype=torch.float32, device=W.device)
+                         if (want_amax_out and fmt == "nvfp4") else None)
+        o["desc"] = dd
+        outs.append(o)
+        mats.append(AdamWMatrix(W.shape[0], W.shape[1], _p(W), _p(m), _p(v), _p(g), _p(o["codes"]),
+                                _p(o["scales"]), _p(o["zeros"]), _p(o.get("r")), _p(o["best_clip"]), _p(o["err"]),
+                                _p(o["tensor_scale"]), _p(amax), _p(o["amax_out"])))
+    if stream is None:
+        stream = torch.cuda.current_stream(W0.device).cuda_stream
+    opt = AdamW(lr, beta1, beta2, eps, weight_decay, int(step))
+    s = quasar_adamw_reconstruct_batch(d, opt, mats, rd, stream)
+    if s != OK:
+        raise QuasarError(s, "quasar_adamw_reconstruct_batch")
+    return outs
 
 
 def absmax_batch(Ws, *, stream=None):

@@ -168,6 +168,36 @@ def test_adamw_entry_point_validation():
         assert _adam_check(f32, opt) == Q.ERR_ARG, b
 
 
+def test_adamw_batch_validation():
+    opt = Q.AdamW(1e-3, 0.9, 0.999, 1e-8, 0.01, 1)
+
+    def mat(rows=64, cols=256, **kw):
+        p = dict(W=A, m=A, v=A, g=A, codes=A, scales=A, zeros=A, r=A, best_clip=A, err=A, tensor_scale=None,
+                 tensor_amax=None, amax_out=None)
+        p.update(kw)
+        return Q.AdamWMatrix(rows, cols, *[p[k] for k in ("W", "m", "v", "g", "codes", "scales", "zeros", "r",
+                                                          "best_clip", "err", "tensor_scale", "tensor_amax",
+                                                          "amax_out")])
+
+    d = _int_desc(w_dtype=Q.F32)
+    assert Q.quasar_adamw_batch_check(d, opt, [mat(), mat(rows=16, cols=128)], Q.BF16) == Q.OK
+    assert Q.quasar_adamw_batch_check(d, opt, [], Q.BF16) == Q.ERR_ARG
+    assert Q.quasar_adamw_batch_check(d, opt, [mat()] * (Q.MAX_BATCH + 1), Q.BF16) == Q.ERR_ARG
+    assert Q.quasar_adamw_batch_check(d, None, [mat()], Q.BF16) == Q.ERR_ARG
+    assert Q.quasar_adamw_batch_check(d, opt, [mat(), mat(m=None)], Q.BF16) == Q.ERR_ARG
+    assert Q.quasar_adamw_batch_check(d, opt, [mat(), mat(cols=100)], Q.BF16) == Q.ERR_SHAPE
+    assert Q.quasar_adamw_batch_check(_int_desc(), opt, [mat()], Q.F32) == Q.ERR_FORMAT  # bf16 W needs bf16 r
+    nv = _int_desc(fmt="nvfp4", w_dtype=Q.F32)
+    ok = dict(zeros=None, tensor_scale=A, tensor_amax=A)
+    assert Q.quasar_adamw_batch_check(nv, opt, [mat(**ok), mat(**ok, amax_out=A + 16)], Q.BF16) == Q.OK
+    assert Q.quasar_adamw_batch_check(nv, opt, [mat(**ok), mat(**dict(ok, tensor_amax=None))], Q.BF16) == Q.ERR_ARG
+    # an amax_out is cleared before the pass: it may be no matrix's tensor_amax
+    assert Q.quasar_adamw_batch_check(nv, opt, [mat(**dict(ok, tensor_amax=A + 32)),
+                                                mat(**ok, amax_out=A + 32)], Q.BF16) == Q.ERR_ARG
+    assert Q.quasar_adamw_batch_check(_int_desc(fmt="rubin", rows=16, cols=128), opt,
+                                      [mat(16, 128, zeros=None)], Q.BF16) == Q.ERR_FORMAT
+
+
 def test_rubin_descriptor_validation_and_sizes():
     d = _int_desc(fmt="rubin", rows=16, cols=128)
     assert _check(d, zeros=None) == Q.OK

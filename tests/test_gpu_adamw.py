@@ -131,3 +131,40 @@ def test_fused_adamw_error_leaves_state_untouched():
         Q.adamw_reconstruct(W, m, v, g, step=1, fmt="nvfp4", **HP)  # no tensor amax
     torch.cuda.synchronize()
     assert torch.equal(W, W0) and torch.equal(m, m0) and torch.equal(v, v0)
+
+
+@pytest.mark.parametrize("fmt,bits,group,clips,w_bf16", [
+    ("int", 2, 64, tuple(synth.clip_grid(1.0, 0.5, 12)), False),   # binned INT kernel
+    ("int", 4, 128, tuple(synth.clip_grid(1.0, 0.65, 8)), True),   # direct INT kernel
+    ("nvfp4", 4, 16, tuple(synth.clip_grid(1.0, 0.7, 8)), False)])
+def test_adamw_batch_equals_single_calls(fmt, bits, group, clips, w_bf16):
+    """quasar_adamw_reconstruct_batch over matrices of different shapes gives
+    bit-identical W', m, v, codes, scales, zeros, r, chosen clips, scores and
+    amax by-products to one quasar_adamw_reconstruct per matrix."""
+    shapes = [(96, 256), (32, 512), (200, 128)]
+    inputs = [_inputs(r, c, 930 + i, w_bf16, False) for i, (r, c) in enumerate(shapes)]
+    amaxes = [torch.tensor([float(oracle.absmax(host(W))), 0, 0, 0], dtype=torch.float32, device="cuda")
+              for W, _, _, _ in inputs]
+    kw = dict(step=3, fmt=fmt, bits=bits, group=group, clips=clips, want_amax_out=fmt == "nvfp4", **HP)
+    single = []
+    for (W, m, v, g), a in zip(inputs, amaxes):
+        Ws, ms, vs = W.clone(), m.clone(), v.clone()
+        o = Q.adamw_reconstruct(Ws, ms, vs, g, tensor_amax=a if fmt == "nvfp4" else None, **kw)
+        single.append((Ws, ms, vs, o))
+    items = [(W, m, v, g, a) if fmt == "nvfp4" else (W, m, v, g) for (W, m, v, g), a in zip(inputs, amaxes)]
+    print(f"[case] adamw.batch.{fmt}{bits}g{group} shapes={shapes}", flush=True)
+    outs = Q.adamw_reconstruct_batch(items, **kw)
+    torch.cuda.synchronize()
+    keys = ["codes", "scales", "zeros", "best_clip", "err", "r", "tensor_scale", "amax_out"]
+    for i, ((W, m, v, _), (Ws, ms, vs, o), ob) in enumerate(zip(inputs, single, outs)):
+        for name, a, b in (("W", W, Ws), ("m", m, ms), ("v", v, vs)):
+            assert torch.equal(a.view(torch.int16) if a.dtype == torch.bfloat16 else a.view(torch.int32),
+                               b.view(torch.int16) if b.dtype == torch.bfloat16 else b.view(torch.int32)), (i, name)
+        for k in keys:
+            x, y = o.get(k), ob.get(k)
+            assert (x is None) == (y is None), (i, k)
+            if x is None:
+                continue
+            if k in ("tensor_scale", "amax_out"):  # element 0 holds the value
+                x, y = x[:1], y[:1]
+            assert torch.equal(x.view(torch.uint8), y.view(torch.uint8)), (i, k)
