@@ -260,8 +260,9 @@ int quasar_batch_check(const quasar_desc* desc, const quasar_matrix* mats, int n
  * quasar_adamw_matrix gives a matrix's shape and buffers with the meaning and
  * requirements of the same-named quasar_adamw_reconstruct arguments (W is
  * updated in place).  Every amax_out given is cleared before the pass, so none
- * may be any matrix's tensor_amax.  1 <= n_mats <= QUASAR_MAX_BATCH.  Returns
- * a quasar_status; on error nothing is launched.
+ * may be any matrix's tensor_amax, and no two may be the same buffer.
+ * 1 <= n_mats <= QUASAR_MAX_BATCH.  Returns a quasar_status; on error nothing
+ * is launched.
  */
 typedef struct {
   int64_t rows, cols;

@@ -722,9 +722,12 @@ int quasar_adamw_batch_check(const quasar_desc* d, const quasar_adamw* opt, cons
     const int s = quasar_adamw_check(&dd, opt, x.W, x.m, x.v, x.g, x.codes, x.scales, x.zeros, x.r, r_dtype,
                                      x.best_clip, x.err, x.tensor_scale, x.tensor_amax, x.amax_out);
     if (s != QUASAR_OK) return s;
-    // every amax_out is cleared before the pass that reads the tensor_amax
-    for (int k = 0; k < n_mats; k++)
+    // every amax_out is cleared before the pass that reads the tensor_amax,
+    // and each collects one matrix's maximum
+    for (int k = 0; k < n_mats; k++) {
       if (x.amax_out != nullptr && x.amax_out == mats[k].tensor_amax) return QUASAR_ERR_ARG;
+      if (k != i && x.amax_out != nullptr && x.amax_out == mats[k].amax_out) return QUASAR_ERR_ARG;
+    }
     const int64_t upb = d->format == QUASAR_NVFP4 ? quasar::nvfp4_units_per_block()
                                                   : quasar::int_units_per_block(d->group);
     total += (quasar_num_groups(&dd) + upb - 1) / upb;

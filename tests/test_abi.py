@@ -194,6 +194,8 @@ def test_adamw_batch_validation():
     # an amax_out is cleared before the pass: it may be no matrix's tensor_amax
     assert Q.quasar_adamw_batch_check(nv, opt, [mat(**dict(ok, tensor_amax=A + 32)),
                                                 mat(**ok, amax_out=A + 32)], Q.BF16) == Q.ERR_ARG
+    assert Q.quasar_adamw_batch_check(nv, opt, [mat(**ok, amax_out=A + 16), mat(**ok, amax_out=A + 16)],
+                                      Q.BF16) == Q.ERR_ARG               # two matrices, one by-product buffer
     assert Q.quasar_adamw_batch_check(_int_desc(fmt="rubin", rows=16, cols=128), opt,
                                       [mat(16, 128, zeros=None)], Q.BF16) == Q.ERR_FORMAT
 
