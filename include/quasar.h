@@ -294,8 +294,8 @@ int quasar_adamw_batch_check(const quasar_desc* desc, const quasar_adamw* opt, c
  * quasar_matrix only rows, cols and W are read (desc gives the format and W's
  * dtype).  amax_out is a host array of n_mats device pointers (each 16-byte
  * aligned, 1 fp32): amax_out[i] receives max |W| of mats[i] (cleared first,
- * then filled by the pass).  Asynchronous on stream; on error nothing is
- * launched.
+ * then filled by the pass); no two of them may be the same buffer
+ * (QUASAR_ERR_ARG).  Asynchronous on stream; on error nothing is launched.
  */
 int quasar_absmax_batch(const quasar_desc* desc, const quasar_matrix* mats, int n_mats, float* const* amax_out,
                         void* stream);

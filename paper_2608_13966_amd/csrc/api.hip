@@ -139,6 +139,10 @@ int quasar_absmax_batch_check(const quasar_desc* d, const quasar_matrix* mats, i
     if (dd.format != QUASAR_NVFP4) return QUASAR_ERR_FORMAT;
     if (mats[i].W == nullptr || amax_out[i] == nullptr) return QUASAR_ERR_ARG;
     if (!aligned16(mats[i].W) || !aligned16(amax_out[i])) return QUASAR_ERR_ALIGN;
+    // each output is cleared and then collects one matrix's maximum: two
+    // matrices on one buffer would both get the larger of their maxima
+    for (int k = 0; k < i; k++)
+      if (amax_out[k] == amax_out[i]) return QUASAR_ERR_ARG;
     total += quasar::absmax_blocks(dd.rows * dd.cols / (dd.w_dtype == QUASAR_BF16 ? 8 : 4));
   }
   if (total >= ((int64_t)1 << 31)) return QUASAR_ERR_SHAPE;  // one grid

@@ -295,8 +295,11 @@ void nvfp4_reconstruct_kernel(Nvfp4Params p) {
     // by-product of the fused step: max |W'| for the next step's tensor scale.
     // One atomic per wavefront, skipped when the stored maximum is already
     // larger (|w| >= 0, so fp32 bit patterns order like unsigned integers).
+    // Lanes past the last block re-ran the step on a copy of the last block,
+    // whose W its owner may already have updated in place: they contribute
+    // nothing (|w| >= 0, so 0 is the identity of the maximum).
     if (mtx.amax_out) {
-      float mw = run_max<16>(m);
+      float mw = run_max<16>(active ? m : 0.0f);
       mw = fmaxf(mw, __shfl_xor(mw, 16, 64));
       mw = fmaxf(mw, __shfl_xor(mw, 32, 64));
       if ((tid & 63) == 0 && __float_as_uint(mw) > __builtin_nontemporal_load(mtx.amax_out))

@@ -270,6 +270,43 @@ def _dtype_code(t) -> int:
     raise TypeError(f"unsupported dtype {t.dtype}")
 
 
+def _check_same(items, *, slots, what):
+    """Argument checks of the batched wrappers, before anything is allocated
+    or launched: the C side applies one descriptor (W's dtype, g's dtype and
+    whether there is a g) to every matrix and reads each buffer with its
+    matrix's shape, so a mismatch would read or write out of bounds.
+    ``slots`` names the tensor positions of an item: "W", "v", "m" (fp32,
+    W's shape), "g" (W's shape, the first item's dtype, present in all or
+    none)."""
+    import torch
+    if not items:
+        raise ValueError(f"{what}: no matrices")
+    if len(items) > MAX_BATCH:
+        raise ValueError(f"{what}: at most {MAX_BATCH} matrices per call")
+    first = dict(zip(slots, items[0]))
+    W0, g0 = first["W"], first.get("g")
+    for i, it in enumerate(items):
+        t = dict(zip(slots, it))
+        W = t["W"]
+        if W.dim() != 2 or W.dtype != W0.dtype or W.device != W0.device:
+            raise ValueError(f"{what}: matrix {i}: W must be 2-D with the first matrix's dtype "
+                             f"({W0.dtype}) and device")
+        for k in ("v", "m"):
+            if k in t and (t[k].dtype != torch.float32 or t[k].shape != W.shape or t[k].device != W.device):
+                raise ValueError(f"{what}: matrix {i}: {k} must be fp32 with W's shape and device")
+        if "g" in t:
+            g = t["g"]
+            if (g is None) != (g0 is None):
+                raise ValueError(f"{what}: either every matrix has a gradient or none has")
+            if g is not None and (g.dtype != g0.dtype or g.shape != W.shape or g.device != W.device):
+                raise ValueError(f"{what}: matrix {i}: g must have W's shape and the first gradient's dtype "
+                                 f"({g0.dtype})")
+        for k in slots:
+            x = t.get(k)
+            if x is not None and not x.is_contiguous():
+                raise ValueError(f"{what}: matrix {i}: {k} must be contiguous")
+
+
 def alloc_outputs(d: Descriptor, W, *, want_r=True, want_diag=True, has_amax=False):
     """Allocate the output buffers of one call (torch, on W's device)."""
     import torch
@@ -382,6 +419,9 @@ def adamw_reconstruct_batch(items, *, lr, beta1=0.9, beta2=0.999, eps=1e-8, weig
     dtype.  W, m, v are updated in place.  Returns one output dict per matrix,
     as adamw_reconstruct()."""
     import torch
+    _check_same(items, slots=("W", "m", "v", "g"), what="adamw_reconstruct_batch")
+    if items[0][3] is None:
+        raise ValueError("adamw_reconstruct_batch: the optimiser step needs a gradient")
     W0, g0 = items[0][0], items[0][3]
     d = Descriptor(W0.shape[0], W0.shape[1], fmt=fmt, bits=bits, group=group, clips=clips,
                    w_dtype=_dtype_code(W0), g_dtype=_dtype_code(g0), beta2=beta2, weighting=weighting,
@@ -418,6 +458,7 @@ def absmax_batch(Ws, *, stream=None):
     (quasar_absmax_batch); returns one device fp32 tensor [4] per matrix,
     the value in element 0."""
     import torch
+    _check_same([(W,) for W in Ws], slots=("W",), what="absmax_batch")
     W0 = Ws[0]
     d = Descriptor(W0.shape[0], W0.shape[1], fmt="nvfp4", w_dtype=_dtype_code(W0))
     outs = [torch.zeros(4, dtype=torch.float32, device=W0.device) for _ in Ws]
@@ -438,6 +479,11 @@ def reconstruct_batch(items, *, fmt="int", bits=4, group=128, clips=(1.0,), beta
     batched absmax pass first.  Returns one output dict per matrix, as
     reconstruct()."""
     import torch
+    _check_same([tuple(it[:3]) for it in items], slots=("W", "v", "g"), what="reconstruct_batch")
+    for i, it in enumerate(items):
+        a = it[3] if len(it) > 3 else None
+        if a is not None and (a.dtype != torch.float32 or a.device != it[0].device):
+            raise ValueError(f"reconstruct_batch: matrix {i}: tensor_amax must be an fp32 tensor on W's device")
     W0, g0 = items[0][0], items[0][2]
     d = Descriptor(W0.shape[0], W0.shape[1], fmt=fmt, bits=bits, group=group, clips=clips,
                    w_dtype=_dtype_code(W0), g_dtype=_dtype_code(g0) if g0 is not None else BF16, beta2=beta2,

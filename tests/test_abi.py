@@ -259,16 +259,70 @@ def test_batch_entry_point_validation():
 def test_absmax_batch_validation():
     nv = _int_desc(fmt="nvfp4")
     mats = [_mat(), _mat(rows=1, cols=16), _mat(rows=5, cols=48)]
-    assert Q.quasar_absmax_batch_check(nv, mats, [A] * 3) == Q.OK
+    assert Q.quasar_absmax_batch_check(nv, mats, [A, A + 16, A + 32]) == Q.OK
     assert Q.quasar_absmax_batch_check(nv, [], []) == Q.ERR_ARG
     assert Q.quasar_absmax_batch_check(nv, [_mat()] * 17, [A] * 17) == Q.ERR_ARG
     assert Q.quasar_absmax_batch_check(nv, mats, [A, None, A]) == Q.ERR_ARG    # an output missing
-    assert Q.quasar_absmax_batch_check(nv, mats, [A, A, A + 4]) == Q.ERR_ALIGN
+    assert Q.quasar_absmax_batch_check(nv, mats, [A, A + 16, A + 36]) == Q.ERR_ALIGN
     assert Q.quasar_absmax_batch_check(nv, [_mat(W=A + 8)], [A]) == Q.ERR_ALIGN
     assert Q.quasar_absmax_batch_check(nv, [_mat(W=None)], [A]) == Q.ERR_ARG
     assert Q.quasar_absmax_batch_check(nv, [_mat(cols=24)], [A]) == Q.ERR_SHAPE  # not whole 16-blocks
     assert Q.quasar_absmax_batch_check(nv, [_mat(rows=0)], [A]) == Q.ERR_SHAPE
     assert Q.quasar_absmax_batch_check(_int_desc(), [_mat()], [A]) == Q.ERR_FORMAT
+    # one output buffer for two matrices would hold the larger of both maxima
+    assert Q.quasar_absmax_batch_check(nv, mats, [A, A + 16, A]) == Q.ERR_ARG
+    assert Q.quasar_absmax_batch_check(nv, mats, [A, A + 16, A + 32]) == Q.OK
+
+
+def test_status_values():
+    """The numeric status codes, as include/quasar.h declares them (QUASAR_OK
+    0, then ERR_ARG -1, ERR_SHAPE -2, ERR_ALIGN -3, ERR_FORMAT -4,
+    ERR_WORKSPACE -5, ERR_DEVICE -6), read from the header itself and from the
+    library's status strings."""
+    src = open(os.path.join(ROOT, "include", "quasar.h")).read()
+    body = re.search(r"typedef enum \{(.*?)\} quasar_status;", src, flags=re.S).group(1)
+    body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
+    declared = {k: int(v) for k, v in re.findall(r"(QUASAR_[A-Z_]+)\s*=\s*(-?\d+)", body)}
+    assert declared == {"QUASAR_OK": 0, "QUASAR_ERR_ARG": -1, "QUASAR_ERR_SHAPE": -2, "QUASAR_ERR_ALIGN": -3,
+                        "QUASAR_ERR_FORMAT": -4, "QUASAR_ERR_WORKSPACE": -5, "QUASAR_ERR_DEVICE": -6}
+    assert (Q.OK, Q.ERR_ARG, Q.ERR_SHAPE, Q.ERR_ALIGN, Q.ERR_FORMAT, Q.ERR_WORKSPACE, Q.ERR_DEVICE) == \
+        (0, -1, -2, -3, -4, -5, -6)
+    assert "workspace" in Q.quasar_status_string(-5) and "launch" in Q.quasar_status_string(-6)
+
+
+def test_batch_wrappers_reject_mixed_matrices_before_launch():
+    """The batched Python wrappers apply one descriptor to every matrix; a
+    matrix whose dtype or shape differs from what that descriptor says is
+    refused before anything is allocated or launched (CPU tensors here: the
+    checks run first, so no device is touched)."""
+    import torch
+    W32 = torch.zeros(8, 128, dtype=torch.float32)
+    W16 = torch.zeros(8, 128, dtype=torch.bfloat16)
+    v = torch.zeros(8, 128, dtype=torch.float32)
+    g = torch.zeros(8, 128, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="dtype"):
+        Q.reconstruct_batch([(W32, v, None), (W16, v, None)], fmt="int", bits=4, group=128)
+    with pytest.raises(ValueError, match="gradient"):
+        Q.reconstruct_batch([(W16, v, g), (W16, v, None)], fmt="int", bits=4, group=128)
+    with pytest.raises(ValueError, match="g must"):
+        Q.reconstruct_batch([(W16, v, g), (W16, v, g.float())], fmt="int", bits=4, group=128)
+    with pytest.raises(ValueError, match="v must"):
+        Q.reconstruct_batch([(W16, v, g), (W16, v[:4], g)], fmt="int", bits=4, group=128)
+    with pytest.raises(ValueError, match="contiguous"):
+        Q.reconstruct_batch([(W16, v, g), (W16.t().contiguous().t(), v, g)], fmt="int", bits=4, group=128)
+    with pytest.raises(ValueError, match="tensor_amax"):
+        Q.reconstruct_batch([(W16, v, None, torch.zeros(4, dtype=torch.float64))], fmt="nvfp4")
+    m = torch.zeros_like(v)
+    with pytest.raises(ValueError, match="dtype"):
+        Q.adamw_reconstruct_batch([(W32, m, v, g), (W16, m, v, g)], lr=1e-3, fmt="int", bits=4, group=128)
+    with pytest.raises(ValueError, match="m must"):
+        Q.adamw_reconstruct_batch([(W32, m, v, g), (W32, m.double(), v, g)], lr=1e-3, fmt="int", bits=4,
+                                  group=128)
+    with pytest.raises(ValueError, match="g must"):
+        Q.adamw_reconstruct_batch([(W32, m, v, g), (W32, m, v, g.float())], lr=1e-3, fmt="int", bits=4,
+                                  group=128)
+    with pytest.raises(ValueError, match="dtype"):
+        Q.absmax_batch([W16, W32])
 
 
 def _with_path(value, fn):

@@ -157,6 +157,9 @@ def test_adamw_batch_equals_single_calls(fmt, bits, group, clips, w_bf16):
     torch.cuda.synchronize()
     keys = ["codes", "scales", "zeros", "best_clip", "err", "r", "tensor_scale", "amax_out"]
     for i, ((W, m, v, _), (Ws, ms, vs, o), ob) in enumerate(zip(inputs, single, outs)):
+        if fmt == "nvfp4":  # the by-product is exactly max |W'|, also where the last workgroup is partly idle
+            want = W.float().abs().max().reshape(1).view(torch.int32).item()
+            assert ob["amax_out"][:1].view(torch.int32).item() == want, (i, "amax_out")
         for name, a, b in (("W", W, Ws), ("m", m, ms), ("v", v, vs)):
             assert torch.equal(a.view(torch.int16) if a.dtype == torch.bfloat16 else a.view(torch.int32),
                                b.view(torch.int16) if b.dtype == torch.bfloat16 else b.view(torch.int32)), (i, name)
@@ -168,3 +171,53 @@ def test_adamw_batch_equals_single_calls(fmt, bits, group, clips, w_bf16):
             if k in ("tensor_scale", "amax_out"):  # element 0 holds the value
                 x, y = x[:1], y[:1]
             assert torch.equal(x.view(torch.uint8), y.view(torch.uint8)), (i, k)
+
+
+@pytest.mark.parametrize("w_bf16", [False, True])
+def test_adamw_amax_by_product_exact_and_repeatable(w_bf16):
+    """The by-product max |W'| of the fused NVFP4 step is exactly the largest
+    magnitude of the updated weights, on shapes whose last workgroup is
+    partly idle (200 x 128: 64 of its 256 lanes hold a block; 37 x 384: 120),
+    and two runs from the same state give identical bytes, single-matrix and
+    batched.  Lanes past the last block re-run the step on a copy of the last
+    block, whose weights its owner may already have updated in place; they
+    must not reach the by-product."""
+    shapes = [(200, 128), (37, 384), (16, 64)]
+    clips = tuple(synth.clip_grid(1.0, 0.7, 8))
+    state = [_inputs(r, c, 960 + i, w_bf16, False) for i, (r, c) in enumerate(shapes)]
+    amaxes = [torch.tensor([float(oracle.absmax(host(W))), 0, 0, 0], dtype=torch.float32, device="cuda")
+              for W, _, _, _ in state]
+    kw = dict(step=2, fmt="nvfp4", clips=clips, want_amax_out=True, **HP)
+
+    def single_run():
+        res = []
+        for (W, m, v, g), a in zip(state, amaxes):
+            Ws, ms, vs = W.clone(), m.clone(), v.clone()
+            o = Q.adamw_reconstruct(Ws, ms, vs, g, tensor_amax=a, **kw)
+            res.append((Ws, ms, vs, o))
+        torch.cuda.synchronize()
+        return res
+
+    def batch_run():
+        cl = [(W.clone(), m.clone(), v.clone(), g, a) for (W, m, v, g), a in zip(state, amaxes)]
+        outs = Q.adamw_reconstruct_batch(cl, **kw)
+        torch.cuda.synchronize()
+        return [(W, m, v, o) for (W, m, v, _, _), o in zip(cl, outs)]
+
+    print(f"[case] adamw.amax-by-product w={'bf16' if w_bf16 else 'f32'} shapes={shapes}", flush=True)
+    runs = [single_run(), single_run(), batch_run(), batch_run()]
+    keys = ["codes", "scales", "best_clip", "err", "r", "tensor_scale", "amax_out"]
+    for i in range(len(shapes)):
+        Wn = runs[0][i][0]
+        want = Wn.float().abs().max().reshape(1).view(torch.int32).item()
+        for ri, run in enumerate(runs):
+            W, m, v, o = run[i]
+            got = o["amax_out"][:1].view(torch.int32).item()
+            assert got == want, f"run {ri} matrix {i} {shapes[i]}: amax_out {got:#x}, max |W'| {want:#x}"
+            for name, a, b in (("W", W, Wn), ("m", m, runs[0][i][1]), ("v", v, runs[0][i][2])):
+                assert torch.equal(a.view(torch.uint8), b.view(torch.uint8)), (ri, i, name)
+            for k in keys:
+                x, y = o[k], runs[0][i][3][k]
+                if k in ("tensor_scale", "amax_out"):
+                    x, y = x[:1], y[:1]
+                assert torch.equal(x.view(torch.uint8), y.view(torch.uint8)), (ri, i, k)

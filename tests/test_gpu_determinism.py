@@ -48,3 +48,35 @@ def test_repeat_batched_runs_identical():
     torch.cuda.synchronize()
     for i, (a, b) in enumerate(zip(*outs)):
         _same(f"batch.rubin.{i}", a, b, KEYS)
+
+
+@pytest.mark.parametrize("fmt", ["int", "nvfp4"])
+@pytest.mark.parametrize("by_product", [True, False])
+def test_repeat_adamw_batched_runs_identical(fmt, by_product):
+    """The batched fused AdamW step, from the same optimiser state, twice:
+    identical W', m', v', outputs and (NVFP4) max |W'| by-products, with and
+    without the by-product."""
+    shapes = [(96, 256), (37, 384), (200, 128)]
+    state = []
+    for i, (r, c) in enumerate(shapes):
+        W, v, g = synth.gen_matrix(r, c, 4400 + i, w_bf16=False, ema=True, device="cuda")
+        m, v = synth.gen_adamw_state(r, c, 4400 + i, v, device="cuda")
+        a = torch.zeros(4, dtype=torch.float32, device="cuda")
+        a[0] = W.abs().max()
+        state.append((W, m, v, g, a))
+    kw = dict(lr=3e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.05, step=4, fmt=fmt, bits=2, group=64,
+              clips=tuple(synth.clip_grid(1.0, 0.5, 12)) if fmt == "int" else tuple(synth.clip_grid(1.0, 0.7, 8)),
+              want_amax_out=by_product and fmt == "nvfp4")
+    print(f"[case] determinism adamw batch {fmt} by_product={by_product}", flush=True)
+    runs = []
+    for rep in range(2):
+        items = [(W.clone(), m.clone(), v.clone(), g, a) if fmt == "nvfp4" else (W.clone(), m.clone(), v.clone(), g)
+                 for W, m, v, g, a in state]
+        outs = Q.adamw_reconstruct_batch(items, **kw)
+        torch.cuda.synchronize()
+        runs.append((items, outs))
+    for i in range(len(shapes)):
+        (ia, oa), (ib, ob) = runs[0], runs[1]
+        for t in range(3):
+            assert torch.equal(ia[i][t].view(torch.int32), ib[i][t].view(torch.int32)), (i, "Wmv"[t])
+        _same(f"adamw.{fmt}.{i}", oa[i], ob[i], KEYS + ("amax_out",))
