@@ -67,7 +67,8 @@ __device__ __forceinline__ double paired(double x, bool low) {
 // the values of members j+1 .. L-1.  Members 2i and 2i+1 share a row of 16
 // (8 lanes apart), so member j's suffix is its row partner's value (j even)
 // plus the totals of the later rows, exchanged between rows and halves
-// without LDS.  The values are integers below 2^51: every sum is exact.
+// without LDS.  The values are the chunk totals (integers rounded once to
+// fp64), and the member order of the additions is fixed.
 template <int L>
 __device__ __forceinline__ double members_excl_suffix(double x, int j) {
   static_assert(kSpread, "members 8 lanes apart");
@@ -95,22 +96,20 @@ __device__ __forceinline__ uint64_t scaled_to_i64(double x, double scale) {
   const uint64_t b = (uint64_t)__double_as_longlong(__builtin_fma(x, scale, kMagic));
   return ((uint64_t)((uint32_t)(b >> 32) - kMagicHi) << 32) | (uint32_t)b;
 }
-// ... and back (exact for |n| < 2^51)
+// ... and back, correctly rounded: the high word exactly times 2^32 plus the
+// low word, one rounding (sums of the cells reach 2^58)
 __device__ __forceinline__ double i64_to_double(uint64_t n) {
-  return __longlong_as_double((long long)(n + ((uint64_t)kMagicHi << 32))) - kMagic;
+  return __builtin_fma((double)(int32_t)(uint32_t)(n >> 32), 4294967296.0, (double)(uint32_t)n);
 }
 
 template <bool W_BF16, int EMA, int BITS, int G, bool SYM>
-__global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void int_cells_kernel(IntParams p) {
   constexpr int L = G / N;     // lanes per group
   constexpr int GPW = 64 / L;  // groups per wavefront
   constexpr int QMAX = SYM ? (1 << (BITS - 1)) - 1 : (1 << BITS) - 1;
   constexpr int NB = SYM ? 2 * QMAX : QMAX;  // code steps per clip
   constexpr int OWN = kMaxClips / L;         // clips a lane may own
   constexpr int CPL = kCellsPerLane;         // most cells per lane
-  constexpr float kQmax = (float)QMAX;
-  constexpr float kQmin = SYM ? -(float)QMAX : 0.0f;
-  constexpr float kBeta = 0.5f * (float)QMAX;
   static_assert(kThreads == kCellBuckets && kThreads == kMaxClips * kCellSteps, "one table entry per thread");
 
   extern __shared__ double s_hist[];  // [wave][group slot][cell][h, h w]
@@ -200,13 +199,13 @@ __global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
 
   // ---- h and h w of every weight into its cell, as exact integers --------------
   // h and h w are scaled by powers of two that bring the group's largest |h|
-  // and |h| max|w| below 2^B, B = 51 - log2(G), rounded to integers and added
-  // as int64: every sum of at most G of them is exact and below 2^51, whatever
-  // the order of the atomics and of the scan, and stays exact in fp64.  Clips
-  // whose codes agree on the whole group get bit-identical moments, so their
-  // scores tie exactly and the lowest index wins, as in the exact definition.
-  // A term loses at most 2^-B of the largest one (about 6e-14).
-  constexpr int B = 51 - (G == 64 ? 6 : 7);
+  // and |h| max|w| below 2^B, B = 51, rounded to integers and added as int64:
+  // every cell sum is exact (below 2^58), whatever the order of the atomics,
+  // and is rounded once to fp64 in the scan.  Clips whose codes agree on the
+  // whole group get bit-identical moments, so their scores tie exactly and the
+  // lowest index wins, as in the exact definition.  A term loses at most
+  // 2^-52 of the largest one; the fit below checks what that can do to it.
+  constexpr int B = 51;
   float hmax = 0.0f;
 #pragma unroll
   for (int i = 0; i < N; i++) hmax = fmaxf(hmax, v[i]);
@@ -228,7 +227,7 @@ __global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
   }
   wave_lds_fence();
 
-  // ---- suffix sums over the cells (exact integers, in fp64 from here on):
+  // ---- suffix sums over the cells (exact integer cells, rounded once to fp64):
   // the chunk totals first, then the members above this one, then a second
   // pass that writes the suffix sums -------------------------------------------
   {
@@ -265,59 +264,21 @@ __global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
   mo.Svww = M::sum(Svww);
   mo.thr = 1e-12 * mo.Sv * mo.Sv * (double)QMAX * (double)QMAX;
   mo.rSv = rcp_f64(mo.Sv);
+  // each term of sum h and of sum h w is off by at most half a unit of its
+  // fixed point; the sums and the fit's products carry fp64 roundings
+  mo.qh = 0.5 * (double)G * rsh;
+  mo.qhw = 0.5 * (double)G * rshw;
+  mo.rel = 0x1p-47;
+  mo.wabs = (double)wabs;
+  int_fit_bounds<QMAX>(mo);
 
-  // ---- a weight among merged thresholds (rare): its group's moments are summed
-  // directly for every clip and left in the group's cells, 3 per clip ---------
+  // A weight among merged thresholds (rare) has a cell that does not fix
+  // every clip's code: its group takes the exact path below.
   const bool group_unsafe = M::max(unsafe ? 1.0f : 0.0f) > 0.0f;
-  if (group_unsafe) {
-    // the saliencies again (v' when this kernel stored it: the fence makes
-    // this lane's own stores visible to its loads; an inactive lane's group
-    // is recomputed but never stored)
-    __threadfence();
-    float hv[N];
-    load16<false>(mtx.v, e0, hv);
-    if (p.weighting != 0) {
-#pragma unroll
-      for (int i = 0; i < N; i++) hv[i] = weight_of(hv[i], p.weighting);
-    }
-    wave_lds_fence();
-#pragma unroll 1
-    for (int k = 0; k < K; k++) {
-      const float al = s_alpha[k];
-      double a0 = 0.0, a1 = 0.0, a2 = 0.0;
-#pragma unroll
-      for (int i = 0; i < N; i++) {
-        const float w = wr.get(i);
-        const float u = int_u<SYM>(w, rg);
-        const float x = SYM ? u * al : __builtin_fmaf(u, al, kBeta);
-        const double Q = (double)__builtin_amdgcn_fmed3f(__builtin_rintf(x), kQmin, kQmax);
-        const double V = (double)hv[i];
-        const double VQ = V * Q;
-        a0 += VQ;
-        a1 = __builtin_fma(VQ, Q, a1);
-        a2 = __builtin_fma(V * (double)w, Q, a2);
-      }
-      a0 = M::sum(a0);
-      a1 = M::sum(a1);
-      a2 = M::sum(a2);
-      if (j == 0) {
-        hist[3 * k] = a0;
-        hist[3 * k + 1] = a1;
-        hist[3 * k + 2] = a2;
-      }
-    }
-    wave_lds_fence();
-  }
 
   // ---- the clips this lane owns: moments from NB suffix sums ------------------
   auto moments = [&](int k, double& A0, double& A1, double& A2) {
     A0 = A1 = A2 = 0.0;
-    if (group_unsafe) {
-      A0 = hist[3 * k];
-      A1 = hist[3 * k + 1];
-      A2 = hist[3 * k + 2];
-      return;
-    }
     const uint4 tw4 = *reinterpret_cast<const uint4*>(s_tp + k * kCellSteps);
     const uint32_t tw[4] = {tw4.x, tw4.y, tw4.z, tw4.w};
 #pragma unroll
@@ -345,18 +306,23 @@ __global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
   // to the lowest index), fits and scores only its best one, and the group's
   // argmin runs over keys made from D / num^2.  Groups with a clip whose fit
   // degenerates (no saliency, all of it on one code), and deployed
-  // precisions other than fp32, score every clip (int_fit_score).
+  // precisions other than fp32, score every clip (int_fit_score).  A group
+  // with a clip whose fit the moments cannot fix accurately enough
+  // (int_fit_ill), or with a weight among merged thresholds, evaluates every
+  // clip straight from its weights (int_exact_all).
   IntBest best = int_best_init();
   bool full = p.param_dtype != 0;
+  bool ill = group_unsafe;
   int bk = -1;
   double bn = 0.0, bd = 1.0;
-  if (!full) {
+  if (!full && !group_unsafe) {
 #pragma unroll 1
     for (int t = 0; t < OWN; t++) {
       const int k = j + L * t;
       if (k < K) {
         double A0, A1, A2;
         moments(k, A0, A1, A2);
+        ill |= int_fit_ill<SYM, QMAX>(mo, A0, A1, A2);
         const double D = SYM ? A1 : mo.Sv * A1 - A0 * A0;
         const double num = SYM ? A2 : mo.Sv * A2 - A0 * mo.Svw;
         const bool degenerate = SYM ? (A1 == 0.0) : (mo.Sv == 0.0 || D <= mo.thr);
@@ -371,22 +337,40 @@ __global__ __launch_bounds__(kThreads) void int_cells_kernel(IntParams p) {
       }
     }
   }
-  if (M::max(full ? 1.0f : 0.0f) > 0.0f) {
+  ill = M::max(ill ? 1.0f : 0.0f) > 0.0f;
+  if (!ill) {
+    if (M::max(full ? 1.0f : 0.0f) > 0.0f) {
 #pragma unroll 1
-    for (int t = 0; t < OWN; t++) {
-      const int k = j + L * t;
-      if (k < K) {
-        double A0, A1, A2;
-        moments(k, A0, A1, A2);
-        int_fit_score<SYM, QMAX>(p, k, s_clip[k], rg, mo, A0, A1, A2, best);
+      for (int t = 0; t < OWN; t++) {
+        const int k = j + L * t;
+        if (k < K) {
+          double A0, A1, A2;
+          moments(k, A0, A1, A2);
+          int_fit_score<SYM, QMAX>(p, k, s_clip[k], rg, mo, A0, A1, A2, best);
+        }
       }
+      ill = M::max(best.ill ? 1.0f : 0.0f) > 0.0f;
+    } else if (bk >= 0) {
+      double b0, b1, b2;
+      moments(bk, b0, b1, b2);
+      int_fit_score<SYM, QMAX>(p, bk, s_clip[bk], rg, mo, b0, b1, b2, best);
+      // rank by D / num^2 (num = 0: the worst fit, kept finite)
+      best.key = make_key(fmin(bd * rcp_f64(bn), 1e300), bk);
     }
-  } else if (bk >= 0) {
-    double b0, b1, b2;
-    moments(bk, b0, b1, b2);
-    int_fit_score<SYM, QMAX>(p, bk, s_clip[bk], rg, mo, b0, b1, b2, best);
-    // rank by D / num^2 (num = 0: the worst fit, kept finite)
-    best.key = make_key(fmin(bd * rcp_f64(bn), 1e300), bk);
+  }
+  {
+    // The wavefront's cell areas are no longer needed: they stage the
+    // flagged groups.  A member lane reads its saliencies again (v' when this
+    // kernel stored it: a lane's load after its own store to the same
+    // address returns the stored value).
+    auto load_h = [&](float (&hv)[N]) {
+      load16<false>(mtx.v, e0, hv);
+#pragma unroll
+      for (int i = 0; i < N; i++) hv[i] = weight_of(hv[i], p.weighting);
+    };
+    float* stage = reinterpret_cast<float*>(s_hist + (size_t)wave * GPW * int_cells_stride<L>(cpl) * 2);
+    int_exact_wave<L, SYM, QMAX, kSpread, W_BF16>(p, wr, load_h, rg, s_alpha, s_clip, lane,
+                                                  ill && active && !rg.constant, stage, best);
   }
 
   int_finish<W_BF16, BITS, G, SYM, kSpread>(p, mtx, wr, rg, mo.Sv, best, s_alpha, s_win[wave][slot], j, gid, e0,

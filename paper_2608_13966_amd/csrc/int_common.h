@@ -183,25 +183,273 @@ __device__ __forceinline__ float int_u(float w, const IntRange& g) {
   return SYM ? w * g.rrho : __builtin_fmaf(w, g.rrho, g.nc);
 }
 
-// Clip-independent moments of the group: sum h, sum h w, sum h w^2 (fp64).
+// Clip-independent moments of the group: sum h, sum h w, sum h w^2 (fp64),
+// and what bounds the error of the moments the fit is formed from: each
+// term of sum h may be off by qh / G in absolute value and each term of
+// sum h w by qhw / G (so qh and qhw bound the sums over the group: the
+// binned kernel's fixed-point rounding; 0 where the terms are exact), and
+// every fp64 sum, product and difference by rel times the magnitude of its
+// terms (wabs = max |w| over the group bounds those of sum h w, sum h q w).
 struct IntMoments {
   double Sv, Svw, Svww;
   double thr;  // rank-deficiency threshold 1e-12 (sum h)^2 qmax^2
   double rSv;  // 1 / sum h
+  double qh, qhw, rel, wabs;
+  // per-group parts of the error bounds of int_fit_ill (int_fit_bounds)
+  double eD0, eN0, eN1;
 };
 
 // Best candidate so far of one lane: the key (score with the clip index in
-// its low bits), the emitted (s, z) and the score as fp32.
+// its low bits), the emitted (s, z) and the score as fp32; `ill` marks a
+// candidate whose fit the moments cannot fix to the required accuracy.
 struct IntBest {
   double key;
   float a, b, err;
+  bool ill;
 };
 
 __device__ __forceinline__ IntBest int_best_init() {
   IntBest b;
   b.key = __longlong_as_double(0x7ff0000000000000ll);  // +inf
   b.a = b.b = b.err = 0.0f;
+  b.ill = false;
   return b;
+}
+
+// Relative accuracy the fast forms must guarantee for the two quantities the
+// fit of Eq. ridgefit divides (the determinant and the slope's numerator);
+// the fitted (s, z) then agree with an exact evaluation far inside fp32.
+constexpr double kFitTol = 1e-8;
+// ... and for the score of the emitted dequantiser (expanded from the
+// moments), relative to itself, or, for a score below 1e-13 sum h w^2 (a fit
+// that is exact to that level), to that floor.
+constexpr double kScoreTol = 1e-8;
+constexpr double kScoreFloor = 1e-13;
+
+// Whether the score of the emitted (s, z), expanded from the moments, may be
+// off by more than kScoreTol of itself.  It differs from sum h (s q + z - w)^2
+// of the exact moments by sum_i [dh_i r_i^2 - 2 d(hw)_i r_i] with
+// r_i = s q_i + z, |r_i| <= |s| qmax + |z|, and by the fp64 roundings of its
+// six terms.
+__device__ __forceinline__ bool int_score_ill(const IntMoments& mo, double s, double z, double qmax, double A0,
+                                              double A1, double A2, double score) {
+  const double R = fabs(s) * qmax + fabs(z);
+  const double e = mo.qh * R * R + 2.0 * mo.qhw * R +
+                   mo.rel * (mo.Svww + s * s * A1 + z * z * mo.Sv + 2.0 * fabs(s * z) * A0 + 2.0 * fabs(s * A2) +
+                             2.0 * fabs(z * mo.Svw));
+  return e > fmax(kScoreTol * score, kScoreFloor * mo.Svww);
+}
+
+// Whether the fit of one candidate from moments A0 = sum h q, A1 = sum h q^2,
+// A2 = sum h q w is ill-conditioned: the error bounds of the determinant
+// D = Sv A1 - A0^2 or of the numerator Sv A2 - A0 Svw exceed kFitTol of their
+// values, or D lies so close to the rank-deficiency threshold that its side
+// is not certain (symmetric: sum h q^2 and sum h q w against their bounds).
+// Perturbing h_i moves D by Sv ((q_i - qbar)^2 + var) <= 2 qmax^2 Sv per unit
+// of h_i, and the numerator by A2 - q_i Svw (|.| <= wabs (A0 + qmax Sv)) per
+// unit of h_i and by Sv q_j - A0 (|.| <= qmax Sv) per unit of h_j w_j; the
+// fp64 roundings add rel times the magnitudes of the products.  The parts
+// that do not depend on the clip are formed once per group:
+//   eD = eD0 + rel (Sv A1 + A0^2),   eN = eN0 + eN1 A0.
+template <int QMAX>
+__device__ __forceinline__ void int_fit_bounds(IntMoments& mo) {
+  constexpr double Q = (double)QMAX;
+  mo.eD0 = 2.0 * Q * Q * mo.qh * mo.Sv;
+  mo.eN0 = (mo.wabs * mo.qh + mo.qhw) * Q * mo.Sv;
+  mo.eN1 = mo.wabs * (mo.qh + 4.0 * mo.rel * mo.Sv);
+}
+
+template <bool SYM, int QMAX>
+__device__ __forceinline__ bool int_fit_ill(const IntMoments& mo, double A0, double A1, double A2) {
+  constexpr double Q = (double)QMAX;
+  if constexpr (SYM) {
+    const double e1 = mo.qh * Q * Q + mo.rel * A1, e2 = mo.qhw * Q + mo.rel * mo.wabs * Q * mo.Sv;
+    return A1 > 0.0 && (e1 > kFitTol * A1 || e2 > kFitTol * fabs(A2));
+  } else {
+    const double Sv = mo.Sv;
+    if (Sv == 0.0) return false;  // every candidate keeps its RTN dequantiser and scores 0
+    const double p1 = Sv * A1, p2 = A0 * A0;
+    const double D = p1 - p2;
+    const double eD = __builtin_fma(mo.rel, p1 + p2, mo.eD0);
+    if (D + eD <= mo.thr) return false;  // certainly rank-deficient
+    if (D - eD <= mo.thr) return true;   // either side of the threshold
+    const double num = Sv * A2 - A0 * mo.Svw;
+    const double eN = __builtin_fma(mo.eN1, A0, mo.eN0);
+    return eD > kFitTol * D || eN > kFitTol * fabs(num);
+  }
+}
+
+// Every clip of a group evaluated the way Eq. ridgefit and Eq. fisher-obj
+// read, in fp64 straight from the group's weights: the codes, the weighted
+// means qbar and wbar, the centred sums sum h (q - qbar)^2 and
+// sum h (q - qbar)(w - wbar) (symmetric: sum h q^2, sum h q w), the fit,
+// its rank-deficiency decision, and the score as a sum of weighted squared
+// residuals of the emitted dequantiser.  The path for the rare groups whose
+// moments from the fast forms cannot fix the fit to the required accuracy
+// (nearly all saliency on one code) or that the binned form cannot bin.
+//
+// The whole wavefront takes the flagged groups (`flagged`, uniform per
+// group) one at a time: the group's members stage its G weights and
+// saliencies in LDS (`stage`, 2 G floats the wavefront no longer needs;
+// load_h(hv) gives a member lane's 16 saliencies), and lane l evaluates clip
+// k0 + l / P (P = G / 16) over part l % P of the group, its sums combined
+// over the clip's P lanes with DPP, then an argmin over the clips across the
+// wavefront.  The group's members receive the winner in `best` (the key in
+// member 0 only).
+template <int L, bool SYM, int QMAX, bool SPREAD, bool W_BF16, typename LoadH>
+__device__ __forceinline__ void int_exact_wave(const IntParams& p, const WRegs<W_BF16>& wr, LoadH load_h,
+                                               const IntRange& g, const float* s_alpha, const float* s_clip,
+                                               int lane, bool flagged, float* stage, IntBest& best) {
+  using M = Members<L, SPREAD>;
+  constexpr int G = L * kIntN;
+  constexpr int P = L;               // parts of 16 weights per group
+  constexpr int CPW = 64 / P;        // clips per pass of the wavefront
+  constexpr float kQmax = (float)QMAX;
+  constexpr float kQmin = SYM ? -(float)QMAX : 0.0f;
+  constexpr float kBeta = 0.5f * (float)QMAX;
+  const int j = M::member(lane), slot = M::slot(lane);
+  const int K = p.n_clips;
+  uint64_t todo = __ballot(flagged && j == 0);  // member 0 of every flagged group
+#pragma unroll 1
+  while (todo != 0) {
+    const int s_lane = __ffsll((unsigned long long)todo) - 1;
+    todo &= todo - 1;
+    const bool mine = slot == M::slot(s_lane);
+    wave_lds_fence();  // earlier use of the stage by this wavefront is done
+    if (mine) {
+      float hv[kIntN];
+      load_h(hv);
+#pragma unroll
+      for (int c = 0; c < kIntN / 4; c++) {
+        *reinterpret_cast<float4*>(stage + j * kIntN + 4 * c) =
+            make_float4(wr.get(4 * c), wr.get(4 * c + 1), wr.get(4 * c + 2), wr.get(4 * c + 3));
+        *reinterpret_cast<float4*>(stage + G + j * kIntN + 4 * c) =
+            make_float4(hv[4 * c], hv[4 * c + 1], hv[4 * c + 2], hv[4 * c + 3]);
+      }
+    }
+    wave_lds_fence();
+    // the group's range, from its member 0 (uniform from here on)
+    IntRange gg;
+    gg.mn = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, g.mn), s_lane));
+    gg.mx = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, g.mx), s_lane));
+    gg.c = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, g.c), s_lane));
+    gg.rho = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, g.rho), s_lane));
+    gg.rrho = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, g.rrho), s_lane));
+    gg.nc = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, g.nc), s_lane));
+    gg.constant = false;
+    // this lane's part of the group
+    const int part = lane % P;
+    float w[kIntN], h[kIntN];
+#pragma unroll
+    for (int c = 0; c < kIntN / 4; c++) {
+      const float4 a = *reinterpret_cast<const float4*>(stage + part * kIntN + 4 * c);
+      const float4 b = *reinterpret_cast<const float4*>(stage + G + part * kIntN + 4 * c);
+      w[4 * c] = a.x; w[4 * c + 1] = a.y; w[4 * c + 2] = a.z; w[4 * c + 3] = a.w;
+      h[4 * c] = b.x; h[4 * c + 1] = b.y; h[4 * c + 2] = b.z; h[4 * c + 3] = b.w;
+    }
+    double sh = 0.0, shw = 0.0;
+#pragma unroll
+    for (int i = 0; i < kIntN; i++) {
+      sh += (double)h[i];
+      shw += (double)h[i] * (double)w[i];
+    }
+    sh = run_sum<P>(sh);
+    shw = run_sum<P>(shw);
+    IntBest lb = int_best_init();
+#pragma unroll 1
+    for (int k0 = 0; k0 < K; k0 += CPW) {
+      const int k = k0 + lane / P;
+      const int kc = k < K ? k : K - 1;  // lanes past the last clip repeat it; never kept
+      const float al = s_alpha[kc], f = s_clip[kc];
+      // the codes and the fp64 forms are formed again in every pass (the
+      // values are made opaque between passes), one weight at a time, so
+      // that few registers are live
+      auto fresh = [&]() {
+#pragma unroll
+        for (int i = 0; i < kIntN; i++) asm volatile("" : "+v"(w[i]), "+v"(h[i]));
+      };
+      auto code = [&](int i) {
+        const float u = int_u<SYM>(w[i], gg);
+        const float x = SYM ? u * al : __builtin_fmaf(u, al, kBeta);
+        return (double)__builtin_amdgcn_fmed3f(__builtin_rintf(x), kQmin, kQmax);
+      };
+      double a, b = 0.0;
+      if constexpr (SYM) {
+        double sqq = 0.0, sqw = 0.0;
+        fresh();
+#pragma unroll
+        for (int i = 0; i < kIntN; i++) {
+          const double Q = code(i), H = (double)h[i];
+          sqq += H * Q * Q;
+          sqw += H * Q * (double)w[i];
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        sqq = run_sum<P>(sqq);
+        sqw = run_sum<P>(sqw);
+        a = (sqq == 0.0) ? (double)((f * gg.mx) / kQmax) : sqw / sqq;
+      } else {
+        const float fr = f * gg.rho;
+        const float s_rtn = (2.0f * fr) / kQmax;
+        if (sh == 0.0) {
+          a = (double)s_rtn;
+          b = (double)(gg.c - fr);
+        } else {
+          double shq = 0.0;
+          fresh();
+#pragma unroll
+          for (int i = 0; i < kIntN; i++) {
+            shq += (double)h[i] * code(i);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          shq = run_sum<P>(shq);
+          const double qbar = shq / sh, wbar = shw / sh;
+          double sqq = 0.0, sqw = 0.0;
+          fresh();
+#pragma unroll
+          for (int i = 0; i < kIntN; i++) {
+            const double dq = code(i) - qbar, dw = (double)w[i] - wbar, H = (double)h[i];
+            sqq += H * dq * dq;
+            sqw += H * dq * dw;
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          sqq = run_sum<P>(sqq);
+          sqw = run_sum<P>(sqw);
+          a = (sqq <= 1e-12 * sh * (double)QMAX * (double)QMAX) ? (double)s_rtn : sqw / sqq;
+          b = wbar - a * qbar;
+        }
+      }
+      const float af = round_param((float)a, p.param_dtype);
+      const float bf = SYM ? 0.0f : round_param((float)b, p.param_dtype);
+      double sc = 0.0;
+      fresh();
+#pragma unroll
+      for (int i = 0; i < kIntN; i++) {
+        const double e = (double)af * code(i) + (double)bf - (double)w[i];
+        sc += (double)h[i] * e * e;
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      sc = run_sum<P>(sc);
+      const double key = make_key(sc, k);
+      if (k < K && part == 0 && key < lb.key) {
+        lb.key = key;
+        lb.a = af;
+        lb.b = bf;
+        lb.err = (float)sc;
+      }
+    }
+    // argmin over the clips (keys order by score, then by clip index)
+    const double kmin = rows_min_f64(run_min_f64<16>(lb.key));
+    const int win = __ffsll((unsigned long long)__ballot(lb.key == kmin)) - 1;
+    const float wa = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, lb.a), win));
+    const float wb = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, lb.b), win));
+    const float we = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, lb.err), win));
+    if (mine) {
+      best.key = j == 0 ? kmin : __longlong_as_double(0x7ff0000000000000ll);
+      best.a = wa;
+      best.b = wb;
+      best.err = we;
+    }
+  }
 }
 
 // Fit (Eq. ridgefit) and score (Eq. fisher-obj) of clip k from its
@@ -212,6 +460,7 @@ __device__ __forceinline__ void int_fit_score(const IntParams& p, int k, float f
                                               const IntMoments& mo, double A0, double A1, double A2,
                                               IntBest& best) {
   constexpr float kQmax = (float)QMAX;
+  best.ill |= int_fit_ill<SYM, QMAX>(mo, A0, A1, A2);
   if constexpr (SYM) {
     // scale-only fit: s* = sum h q w / sum h q^2 (the RTN scale f m / Q
     // when sum h q^2 = 0); the score of r = s q is Svww + s (s A1 - 2 A2)
@@ -219,6 +468,7 @@ __device__ __forceinline__ void int_fit_score(const IntParams& p, int k, float f
     const float af = round_param((float)a, p.param_dtype);
     const double ad = (double)af;
     const double score = mo.Svww + ad * (ad * A1 - 2.0 * A2);
+    best.ill |= int_score_ill(mo, ad, 0.0, (double)QMAX, 0.0, A1, A2, score);
     const double key = make_key(score, k);
     if (key < best.key) {
       best.key = key;
@@ -249,6 +499,7 @@ __device__ __forceinline__ void int_fit_score(const IntParams& p, int k, float f
     const double ad = (double)af, bd = (double)bf;
     // Eq. fisher-obj of the emitted dequantiser, expanded in fp64
     const double score = mo.Svww + ad * (ad * A1 + 2.0 * bd * A0 - 2.0 * A2) + bd * (bd * Sv - 2.0 * Svw);
+    best.ill |= int_score_ill(mo, ad, bd, (double)QMAX, A0, A1, A2, score);
     const double key = make_key(score, k);
     if (key < best.key) {
       best.key = key;
@@ -331,16 +582,25 @@ __device__ __forceinline__ void int_finish(const IntParams& p, const IntMatrix& 
       }
     }
   }
+  // INT3: members 2i and 2i + 1 hold bits [96 i, 96 i + 96) of the group's
+  // stream, three whole dwords; the even member needs the odd one's low bits
+  uint32_t partner_lo = 0;
+  if constexpr (BITS == 3) {
+    partner_lo = SPREAD ? dpp_u32<kDppRor8>((uint32_t)bits) : dpp_u32<kDppXor1>((uint32_t)bits);
+  }
   if (!active) return;
   if constexpr (BITS == 4) {
     *reinterpret_cast<uint2*>(mtx.codes + gid * (G / 2) + j * 8) = make_uint2((uint32_t)bits, (uint32_t)(bits >> 32));
   } else if constexpr (BITS == 2) {
     *reinterpret_cast<uint32_t*>(mtx.codes + gid * (G / 4) + j * 4) = (uint32_t)bits;
-  } else {  // BITS == 3: 48 bits per lane at byte offset 6 j of the group's stream
-    uint16_t* dst = reinterpret_cast<uint16_t*>(mtx.codes + gid * (3 * G / 8) + j * 6);
-    dst[0] = (uint16_t)bits;
-    dst[1] = (uint16_t)(bits >> 16);
-    dst[2] = (uint16_t)(bits >> 32);
+  } else {  // BITS == 3: lane j's 48 bits start at bit 48 j of the group's stream
+    uint32_t* dst = reinterpret_cast<uint32_t*>(mtx.codes + gid * (3 * G / 8) + (j >> 1) * 12);
+    if ((j & 1) == 0) {
+      dst[0] = (uint32_t)bits;
+      dst[1] = ((uint32_t)(bits >> 32) & 0xffffu) | (partner_lo << 16);
+    } else {
+      dst[2] = (uint32_t)(bits >> 16);
+    }
   }
   if (j == 0) {
     mtx.scales[gid] = a;

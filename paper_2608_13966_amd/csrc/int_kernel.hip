@@ -73,7 +73,10 @@ void int_reconstruct_kernel(IntParams p) {
   const IntRange rg = int_range<L, SYM>(wr);
 
   // clip-independent moments (fp64), accumulated in the first pass
-  IntMoments mo = {0.0, 0.0, 0.0, 0.0, 0.0};
+  // every moment is an fp64 sum of at most 20 exact products: no fixed-point
+  // rounding, and fp64 rounding inside 2^-47 of the terms' magnitude
+  IntMoments mo = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0x1p-47, (double)fmaxf(fabsf(rg.mn), fabsf(rg.mx)),
+                   0.0, 0.0, 0.0};
   IntBest best = int_best_init();
   double* red = s_red[wave];
 
@@ -127,6 +130,7 @@ void int_reconstruct_kernel(IntParams p) {
       mo.Svww = run_sum<L>(mo.Svww);
       mo.thr = 1e-12 * mo.Sv * mo.Sv * (double)QMAX * (double)QMAX;
       mo.rSv = rcp_f64(mo.Sv);
+      int_fit_bounds<QMAX>(mo);
     }
 
     // ---- combine the L partials: lane j sums the clips kk = j + L t ---------
@@ -164,6 +168,18 @@ void int_reconstruct_kernel(IntParams p) {
   if constexpr (MULTI) {
 #pragma unroll 1
     for (int k0 = KC; k0 < K; k0 += KC) pass(k0, std::false_type{});
+  }
+
+  // a group whose fit the moments cannot fix accurately enough: every clip
+  // again, straight from the weights
+  {
+    auto load_h = [&](float (&hv)[N]) {
+#pragma unroll
+      for (int i = 0; i < N; i++) hv[i] = v[i];
+    };
+    const bool ill = run_max<L>(best.ill ? 1.0f : 0.0f) > 0.0f;
+    int_exact_wave<L, SYM, QMAX, false, W_BF16>(p, wr, load_h, rg, s_alpha, s_clip, lane,
+                                                ill && active && !rg.constant, reinterpret_cast<float*>(red), best);
   }
 
   int_finish<W_BF16, BITS, G, SYM>(p, mtx, wr, rg, mo.Sv, best, s_alpha, s_win[wave][slot], j, gid, e0, active);

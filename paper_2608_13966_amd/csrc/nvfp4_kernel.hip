@@ -2,10 +2,10 @@
 //
 // Tensor level: S_t = amax / (6 * 448) from the tensor absmax (not optimised).
 // E2M1 rounding uses the gfx950 FP4 conversion instructions (round to nearest
-// even, saturating at 6), which agree with the format definition on every
-// finite input; the block scale is rounded to E4M3 with the gfx950 FP8
-// conversion (round to nearest even; checked equal to the format definition
-// up to 464, clamped to 448 above).
+// even, saturating at 6); the block scale is rounded to E4M3 with the gfx950
+// FP8 conversion (round to nearest even, the input clamped to 448 first,
+// since the conversion returns NaN from 464 up).  The GPU tests drive both
+// through this kernel at the formats' midpoints, subnormals and saturation.
 // Per 16-element block: for every clip factor f the search scale f m / 6
 // (m = block absmax) gives E2M1 codes; the block scale is fitted to the same
 // saliency-weighted objective (scale only: s* = sum h q w / sum h q^2) and
@@ -18,7 +18,6 @@
 #include <cstring>
 
 #include "device_common.h"
-#include "formats.h"
 #include "quasar_internal.h"
 
 namespace quasar {
@@ -229,7 +228,12 @@ void nvfp4_reconstruct_kernel(Nvfp4Params p) {
         // flip that choice only next to a rounding midpoint.  x >= 0 (q has
         // the sign of w); the clamp to 448, the saturated value, keeps it
         // below 464, above which the conversion returns NaN.
-        const float xr = (float)Sqw * __builtin_amdgcn_rcpf((float)Sqq * st);
+        // One residual step after the reciprocal: a quotient that is exactly
+        // an fp32 value (an E4M3 midpoint among them) comes out exactly.
+        const float xn = (float)Sqw, xd = (float)Sqq * st;
+        const float xrd = __builtin_amdgcn_rcpf(xd);
+        const float xq = xn * xrd;
+        const float xr = __builtin_fmaf(__builtin_fmaf(-xd, xq, xn), xrd, xq);
         xc[t] = __builtin_amdgcn_fmed3f((Sqq == 0.0) ? fs[kk + t] * mx : xr, 0.0f, 448.0f);
       }
       // nearest E4M3FN (RNE) of both

@@ -52,9 +52,25 @@ class int_path:
             os.environ["QUASAR_INT_PATH"] = self.old
 
 
+def gpu_rows(out, row_step, rows_t, gidx_t, R, code_bytes_per_row, want_r, fmt):
+    """The GPU outputs of the checked rows (selected on the device), as host arrays."""
+    def sel(t, idx):
+        return (t if row_step == 1 else t.index_select(0, idx)).cpu().numpy()
+
+    gpu = {"codes": sel(out["codes"].view(R, code_bytes_per_row), rows_t).ravel(),
+           "scales": sel(out["scales"], gidx_t), "best_clip": sel(out["best_clip"], gidx_t),
+           "err": sel(out["err"], gidx_t),
+           "r": host(out["r"] if row_step == 1 else out["r"].index_select(0, rows_t)) if want_r else None}
+    if fmt == "nvfp4":
+        gpu["tensor_scale"] = out["tensor_scale"].cpu().numpy()[0]
+    else:
+        gpu["zeros"] = sel(out["zeros"], gidx_t)
+    return gpu
+
+
 def run_case(name, rows, cols, seed, *, fmt="int", bits=4, group=128, clips=(1.0, 0.9, 0.8), w_bf16=True,
              ema=False, g_fp32=False, row_step=1, supply_amax=False, want_r=True, W=None, v=None, g=None,
-             weighting="h", param_dtype="fp32", paths=None):
+             weighting="h", param_dtype="fp32", paths=None, near_limit=None):
     """GPU against the oracle on the same bytes.  INT formats run through
     every kernel that can serve the grid (the library's own choice first, then
     the direct and the binned kernel where they differ from it) unless `paths`
@@ -65,24 +81,34 @@ def run_case(name, rows, cols, seed, *, fmt="int", bits=4, group=128, clips=(1.0
         W, v, g = synth.gen_matrix(rows, cols, seed, w_bf16=w_bf16, ema=ema, device=dev)
         if g is not None and g_fp32:
             g = g.float()
-    Wh, vh, gh = host(W), host(v), host(g)
-    amax_t = None
-    amax = None
-    if fmt == "nvfp4":
-        amax = oracle.absmax(Wh)
-        if supply_amax:
-            amax_t = torch.tensor([amax, 0, 0, 0], dtype=torch.float32, device=dev)
     G = 16 if fmt == "nvfp4" else group
     nb = 4 if fmt == "nvfp4" else bits
     R, Cc = W.shape
     rows_idx = np.arange(0, R, row_step)
+    rows_t = torch.from_numpy(rows_idx).to(dev)
     gpr = Cc // G
     gidx = (rows_idx[:, None] * gpr + np.arange(gpr)[None, :]).ravel()
-    o = oracle.reconstruct(Wh[rows_idx], vh[rows_idx], fmt=fmt, bits=bits, group=group, clips=clips,
-                           g=None if gh is None else gh[rows_idx], beta2=0.999, tensor_amax=amax,
-                           want_scores=True, want_diag=True, n_threads=THREADS, weighting=weighting,
-                           param_dtype=param_dtype)
-    h = o["v_out"] if g is not None else vh[rows_idx]
+    gidx_t = torch.from_numpy(gidx).to(dev)
+
+    def rows_of(t):  # the checked rows, selected on the device and copied to the host
+        if t is None:
+            return None
+        return host(t if row_step == 1 else t.index_select(0, rows_t))
+
+    # the oracle's inputs: the checked rows only (v before any GPU run, which
+    # overwrites it with the EMA)
+    Wh, vh, gh = rows_of(W), rows_of(v), rows_of(g)
+    amax_t = None
+    amax = None
+    if fmt == "nvfp4":
+        amax = float(W.float().abs().max())  # a maximum: exact in any order
+        assert row_step != 1 or amax == oracle.absmax(Wh)
+        if supply_amax:
+            amax_t = torch.tensor([amax, 0, 0, 0], dtype=torch.float32, device=dev)
+    o = oracle.reconstruct(Wh, vh, fmt=fmt, bits=bits, group=group, clips=clips, g=gh, beta2=0.999,
+                           tensor_amax=amax, want_scores=True, want_diag=True, n_threads=THREADS,
+                           weighting=weighting, param_dtype=param_dtype)
+    h = o["v_out"] if g is not None else vh
     if weighting == "h2":
         h = (h * h).astype(np.float32)
     elif weighting == "none":
@@ -111,21 +137,14 @@ def run_case(name, rows, cols, seed, *, fmt="int", bits=4, group=128, clips=(1.0
             out = Q.reconstruct(W, vv, g, fmt=fmt, bits=bits, group=group, clips=clips, tensor_amax=amax_t,
                                 want_r=want_r, weighting=weighting, param_dtype=param_dtype)
             torch.cuda.synchronize()
-        codes = out["codes"].cpu().numpy().reshape(R, Cc * nb // 8)[rows_idx].ravel()
-        gpu = {"codes": codes, "scales": out["scales"].cpu().numpy()[gidx],
-               "best_clip": out["best_clip"].cpu().numpy()[gidx], "err": out["err"].cpu().numpy()[gidx],
-               "r": host(out["r"])[rows_idx] if want_r else None}
-        if fmt == "nvfp4":
-            gpu["tensor_scale"] = out["tensor_scale"].cpu().numpy()[0]
-        else:
-            gpu["zeros"] = out["zeros"].cpu().numpy()[gidx]
-        v_gpu = host(vv)[rows_idx] if g is not None else None
-        fails, st = _parity.compare(fmt=fmt, bits=bits, group=group, W=Wh[rows_idx], h=h, o=o, gpu=gpu,
-                                    v_out_gpu=v_gpu)
+        gpu = gpu_rows(out, row_step, rows_t, gidx_t, R, Cc * nb // 8, want_r, fmt)
+        v_gpu = rows_of(vv) if g is not None else None
+        fails, st = _parity.compare(fmt=fmt, bits=bits, group=group, W=Wh, h=h, o=o, gpu=gpu, v_out_gpu=v_gpu)
         record(name if path == "auto" else f"{name}.{path}", st)
         assert not fails, f"path {path}:\n" + "\n".join(fails)
         # exceptions are rare by construction
-        assert st["near_tie"] + st["near_e4m3"] <= max(2, 0.001 * st["groups"]), dict(st)
+        limit = max(2, 0.001 * st["groups"]) if near_limit is None else near_limit
+        assert st["near_tie"] + st["near_tie_floor"] + st["near_e4m3"] <= limit, dict(st)
         if result is None:
             result = (out, o)
     return result
@@ -151,24 +170,32 @@ def test_c2_qwen_layer_set_full():
                  w_bf16=wl.w_bf16, ema=wl.ema)
 
 
-@pytest.mark.parametrize("wl_name", ["c3", "c4"])
-def test_llama_layer_set_sampled(wl_name):
-    """Full-size matrices in the benchmark's launch configuration; every 61st
-    row is checked against the oracle."""
+LLAMA = [(wl, i) for wl in ("c3", "c4") for i in range(7)]
+
+
+@pytest.mark.parametrize("wl_name,mi", LLAMA, ids=[f"{w}-{synth.LAYER_ORDER[i]}" for w, i in LLAMA])
+def test_llama_layer_set_full(wl_name, mi):
+    """Every group (c3) or 16-block (c4) of every full-size matrix of the
+    Llama-3.1-8B layer set against the oracle, through each kernel that can
+    serve the grid."""
     wl = _wl(wl_name)
-    for (name, r, c), seed in zip(wl.shapes, wl.seeds):
-        run_case(f"{wl_name}.{name}", r, c, seed, fmt=wl.fmt, bits=wl.bits, group=wl.group, clips=wl.clips,
-                 w_bf16=wl.w_bf16, ema=wl.ema, row_step=61)
-        torch.cuda.empty_cache()
+    name, r, c = wl.shapes[mi]
+    run_case(f"{wl_name}.{name}", r, c, wl.seeds[mi], fmt=wl.fmt, bits=wl.bits, group=wl.group, clips=wl.clips,
+             w_bf16=wl.w_bf16, ema=wl.ema)
+    torch.cuda.empty_cache()
 
 
-def test_c5_first_and_last_layer_sampled():
+@pytest.mark.parametrize("layer", range(32))
+def test_c5_every_matrix_sampled(layer):
+    """All 224 matrices of the 32-layer Llama-3.1-8B step: every 127th row of
+    each (layers 0 and 31 every 31st) against the oracle."""
     wl = _wl("c5")
     for (name, r, c), seed in zip(wl.shapes, wl.seeds):
-        if not (name.startswith("L0.") or name.startswith("L31.")):
+        if not name.startswith(f"L{layer}."):
             continue
         run_case(f"c5.{name}", r, c, seed, fmt=wl.fmt, bits=wl.bits, group=wl.group, clips=wl.clips,
-                 w_bf16=wl.w_bf16, ema=wl.ema, row_step=127)
+                 w_bf16=wl.w_bf16, ema=wl.ema, row_step=31 if layer in (0, 31) else 127,
+                 paths=None if layer in (0, 31) else ("auto",))
         torch.cuda.empty_cache()
 
 
@@ -320,6 +347,40 @@ def test_weights_among_tie_thresholds():
                  g=g.cuda(), w_bf16=False, ema=True)
     Wb = W.to(torch.bfloat16).cuda()
     run_case("tie-cluster.int2.bf16", 0, 0, 0, bits=2, group=64, clips=clips, W=Wb, v=v.cuda(), w_bf16=True)
+
+
+@pytest.mark.parametrize("fmt,bits,group", [("int", 2, 64), ("int", 3, 128), ("int", 4, 128), ("int", 4, 64),
+                                             ("int_sym", 3, 128), ("int_sym", 4, 64)])
+def test_nearly_rank_deficient_groups(fmt, bits, group):
+    """Groups whose saliency sits almost entirely on one weight: the share of
+    the others falls from 1e-2 down to 1e-13 of the total, and near the
+    rank-deficiency threshold of the fit, so that the weighted code variance
+    is tiny and the closed-form fit (Eq. ridgefit) divides two small
+    differences.  The fast forms detect that their moments cannot fix the
+    fit accurately enough and evaluate such groups straight from the weights;
+    both INT kernels must match the oracle to the usual tolerances."""
+    torch.manual_seed(17)
+    rows, cols = 48, 4 * group
+    W = (torch.randn(rows, cols) * 0.02).float()
+    W[:, 3] *= 10.0
+    v = torch.empty(rows, cols)
+    shares = [10.0 ** -e for e in range(2, 14)] + [3e-12, 1e-12, 5e-13, 2e-13]
+    for r in range(rows):
+        for gi in range(cols // group):
+            share = shares[(r * 4 + gi) % len(shares)]
+            seg = torch.rand(group) * share / group
+            seg[(r + 5 * gi) % group] = 1.0
+            v[r, gi * group:(gi + 1) * group] = seg
+    Wg, vg = _place(W, v)
+    clips = tuple(synth.clip_grid(1.0, 0.5, 8))
+    # Scores of different clips can coincide to fp64 rounding here (the fit
+    # passes through the dominant weight whatever the codes), so near-ties --
+    # each still within the protocol's window -- are not limited in number.
+    run_case(f"rank-deficient.{fmt}{bits}g{group}.f32", 0, 0, 0, fmt=fmt, bits=bits, group=group, clips=clips,
+             W=Wg, v=vg.clone(), w_bf16=False, near_limit=rows * cols // group)
+    Wb = Wg.to(torch.bfloat16)
+    run_case(f"rank-deficient.{fmt}{bits}g{group}.bf16", 0, 0, 0, fmt=fmt, bits=bits, group=group, clips=clips,
+             W=Wb, v=vg.clone(), w_bf16=True, near_limit=rows * cols // group)
 
 
 def test_tiny_shapes():
