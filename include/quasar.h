@@ -153,6 +153,24 @@ int quasar_reconstruct(const quasar_desc* desc, const void* W, float* v, const v
                        size_t workspace_bytes, void* stream);
 
 /*
+ * quasar_reconstruct for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same arguments and results without the workspace, whose
+ * role a library-owned static device array of 256 bytes per GPU takes (held
+ * until the process ends).  Only NVFP4 without tensor_amax uses it; a call
+ * that would need more than 256 bytes returns QUASAR_ERR_WORKSPACE.  The call
+ * itself allocates nothing (no hipMalloc, no allocating library routine);
+ * the array's address is looked up once per device.  Every call on a GPU
+ * shares that GPU's array: calls that overlap on one GPU (other streams,
+ * other threads) race on it and must be serialised by the caller.  Returns a
+ * quasar_status; QUASAR_ERR_DEVICE also when the array's address cannot be
+ * obtained.
+ */
+int quasar_reconstruct_noalloc(const quasar_desc* desc, const void* W, float* v, const void* g, uint8_t* codes,
+                               void* scales, float* zeros, void* r, uint8_t* best_clip, float* err,
+                               float* tensor_scale, const float* tensor_amax, void* stream);
+
+/*
  * Tensor absmax for NVFP4 (Sec. 4.2: the fp32 tensor scale is set from the
  * tensor's absolute maximum).  Writes max |W| over the whole matrix, as fp32,
  * to amax_out (device, 1 float, 16-byte aligned), for use as the tensor_amax

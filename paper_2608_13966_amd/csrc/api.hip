@@ -6,6 +6,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 
 #include "quasar.h"
 #include "quasar_internal.h"
@@ -597,6 +598,60 @@ int quasar_reconstruct(const quasar_desc* d, const void* W, float* v, const void
   const int ema_mode = g == nullptr ? 0 : (d->g_dtype == QUASAR_BF16 ? 1 : 2);
   return launch_path(d, W, nullptr, nullptr, v, g, ema_mode, nullptr, codes, scales, zeros, r,
                      d->w_dtype == QUASAR_BF16, best_clip, err, tensor_scale, tensor_amax, nullptr, workspace,
+                     reinterpret_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"
+
+// ---- the entry point that allocates nothing --------------------------------
+// Its scratch memory (the NVFP4 tensor absmax of a call without tensor_amax)
+// is this file-scope device array, one copy per GPU, held until the process
+// ends.  In host code its name is not a device address: the address is taken
+// once per device with hipGetSymbolAddress and kept here.
+namespace {
+
+constexpr size_t kScratchBytes = 256;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's address of `scratch` (NULL on a HIP error).
+void* scratch_ptr() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return nullptr;
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+int quasar_reconstruct_noalloc(const quasar_desc* d, const void* W, float* v, const void* g, uint8_t* codes,
+                               void* scales, float* zeros, void* r, uint8_t* best_clip, float* err,
+                               float* tensor_scale, const float* tensor_amax, void* stream) {
+  const size_t need = quasar_workspace_bytes(d, tensor_amax != nullptr);
+  if (need > kScratchBytes) return QUASAR_ERR_WORKSPACE;  // more scratch than the static array holds
+  void* ws = nullptr;
+  if (need > 0) {
+    ws = scratch_ptr();
+    if (ws == nullptr) return QUASAR_ERR_DEVICE;
+  }
+  // the same validation and launches as quasar_reconstruct, with the static
+  // array as its workspace (the absmax pass clears it with a kernel first)
+  const int s = quasar_check(d, W, v, g, codes, scales, zeros, r, best_clip, err, tensor_scale, tensor_amax, ws,
+                             need);
+  if (s != QUASAR_OK) return s;
+  const int ema_mode = g == nullptr ? 0 : (d->g_dtype == QUASAR_BF16 ? 1 : 2);
+  return launch_path(d, W, nullptr, nullptr, v, g, ema_mode, nullptr, codes, scales, zeros, r,
+                     d->w_dtype == QUASAR_BF16, best_clip, err, tensor_scale, tensor_amax, nullptr, ws,
                      reinterpret_cast<hipStream_t>(stream));
 }
 

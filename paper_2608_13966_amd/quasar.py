@@ -29,7 +29,7 @@ WEIGHTINGS = {"h": WEIGHT_H, "h2": WEIGHT_H2, "none": WEIGHT_NONE}
 PARAM_DTYPES = {"fp32": F32, "fp16": F16, "bf16": BF16}
 MAX_CLIPS = 16
 
-EXPORTS = ("quasar_reconstruct", "quasar_absmax", "quasar_check", "quasar_adamw_reconstruct", "quasar_adamw_check",
+EXPORTS = ("quasar_reconstruct", "quasar_reconstruct_noalloc", "quasar_absmax", "quasar_check", "quasar_adamw_reconstruct", "quasar_adamw_check",
            "quasar_reconstruct_batch", "quasar_batch_check", "quasar_absmax_batch", "quasar_absmax_batch_check",
            "quasar_adamw_reconstruct_batch", "quasar_adamw_batch_check",
            "quasar_num_groups", "quasar_int_path", "quasar_codes_bytes",
@@ -88,6 +88,8 @@ def lib():
             vp, dp = C.c_void_p, C.POINTER(Desc)
             L.quasar_reconstruct.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, C.c_size_t, vp]
             L.quasar_reconstruct.restype = C.c_int
+            L.quasar_reconstruct_noalloc.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+            L.quasar_reconstruct_noalloc.restype = C.c_int
             L.quasar_absmax.argtypes = [dp, vp, vp, vp]
             L.quasar_absmax.restype = C.c_int
             L.quasar_check.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, C.c_size_t]
@@ -167,6 +169,12 @@ def quasar_reconstruct(d: Descriptor, W, v, g, codes, scales, zeros, r, best_cli
     return lib().quasar_reconstruct(d.ref, _p(W), _p(v), _p(g), _p(codes), _p(scales), _p(zeros), _p(r),
                                     _p(best_clip), _p(err), _p(tensor_scale), _p(tensor_amax), _p(workspace),
                                     int(workspace_bytes), stream)
+
+
+def quasar_reconstruct_noalloc(d: Descriptor, W, v, g, codes, scales, zeros, r, best_clip, err, tensor_scale,
+                               tensor_amax, stream) -> int:
+    return lib().quasar_reconstruct_noalloc(d.ref, _p(W), _p(v), _p(g), _p(codes), _p(scales), _p(zeros), _p(r),
+                                            _p(best_clip), _p(err), _p(tensor_scale), _p(tensor_amax), stream)
 
 
 def quasar_absmax(d: Descriptor, W, amax_out, stream) -> int:
