@@ -863,3 +863,273 @@ def test_sym_sign_symmetry_and_never_worse_than_rtn():
 def test_sym_zero_group():
     o = run_group(np.zeros(64, np.float32), np.ones(64, np.float32), fmt="int_sym", bits=2, clips=(1.0, 0.5))
     assert o["scale"][0] == 0.0 and np.all(o["codes"] == 0) and np.all(o["r"] == 0) and o["err"][0] == 0.0
+
+
+# ---------------------------------------------------------------- literal fp32 mode, diagnostics, normal equations
+
+def _f(x):
+    """Exact value of an fp32/fp64 number as a Fraction."""
+    return Fraction(float(x))
+
+
+def _r32(x: Fraction) -> Fraction:
+    """Round a rational once to fp32 (nearest even) and return it exactly."""
+    return Fraction(X.fp32_from_fraction(x))
+
+
+def _fma32(a, b, c) -> Fraction:
+    return _r32(_f(a) * _f(b) + _f(c))
+
+
+def _int_fp32_group(w, h, bits, clips):
+    """The literal fp32 reading of Alg. 1 for one INT group, every fp32
+    operation rounded exactly once (Fraction arithmetic): the codes by the
+    fp32 recipe, the raw moments sum h, sum h q, sum h q^2, sum h w, sum h q w
+    accumulated sequentially in fp32, the closed-form solve of Eq. ridgefit
+    in fp32, and the score of Eq. fisher-obj accumulated in fp32.  Returns
+    (scores per clip, index of the first minimum, its (s, z))."""
+    qmax = (1 << bits) - 1
+    Q = Fraction(qmax)
+    wf = [_f(x) for x in w]
+    hf = [_f(x) for x in h]
+    mn, mx = min(wf), max(wf)
+    c = _r32(Fraction(1, 2) * (mx + mn))
+    rho = _r32(Fraction(1, 2) * (mx - mn))
+    rr = _r32(1 / rho)
+    nc = -_r32(c * rr)
+    u = [_r32(x * rr + nc) for x in wf]
+    thr_c = Fraction(float(np.float32(1e-12)))
+    out = []
+    for f in clips:
+        f = _f(f)
+        al = _r32(Q / _r32(2 * f))
+        q = [min(max(X.round_half_even(_r32(x * al + Q / 2)), 0), qmax) for x in u]
+        sh = shq = shqq = shw = shqw = Fraction(0)
+        for wi, hi, qi in zip(wf, hf, q):
+            hq = _r32(hi * qi)
+            sh = _r32(sh + hi)
+            shq = _r32(shq + hq)
+            shqq = _r32(shqq + _r32(hq * qi))
+            shw = _r32(shw + _r32(hi * wi))
+            shqw = _r32(shqw + _r32(hq * wi))
+        fr = _r32(f * rho)
+        s_rtn = _r32(_r32(2 * fr) / Q)
+        lo = _r32(c - fr)
+        if sh == 0:
+            a, b = s_rtn, lo
+        else:
+            d = _r32(_r32(sh * shqq) - _r32(shq * shq))
+            thr = _r32(_r32(_r32(_r32(thr_c * sh) * sh) * Q) * Q)
+            a = s_rtn if d <= thr else _r32(_r32(_r32(sh * shqw) - _r32(shq * shw)) / d)
+            b = _r32(_r32(shw - _r32(a * shq)) / sh)
+        s = Fraction(0)
+        for wi, hi, qi in zip(wf, hf, q):
+            e = _r32(_r32(a * qi + b) - wi)
+            s = _r32(s + _r32(_r32(hi * e) * e))
+        out.append((float(s), float(a), float(b)))
+    scores = [x[0] for x in out]
+    k = scores.index(min(scores))
+    return scores, k, out[k][1], out[k][2]
+
+
+@pytest.mark.parametrize("bits,group", [(4, 32), (3, 16), (2, 16)])
+def test_fp32_mode_int_against_exact_fp32_emulation(bits, group):
+    """The oracle's literal fp32 mode (a reported diagnostic) against the same
+    reading evaluated with exactly one rounding per fp32 operation: every
+    clip's score, the choice and the emitted (s, z) are bit-identical."""
+    clips = tuple(synth.clip_grid(1.0, 0.6, 5))
+    Wh, vh, _ = small_matrix(2, 4 * group, 40 + bits)
+    o = oracle.reconstruct(Wh, vh, bits=bits, group=group, clips=clips, fp32_mode=True, want_scores=True)
+    w, h = Wh.reshape(-1, group), vh.reshape(-1, group)
+    for gi in range(w.shape[0]):
+        scores, k, a, b = _int_fp32_group(w[gi], h[gi], bits, clips)
+        assert o["scores"][gi].tolist() == scores, gi
+        assert int(o["best"][gi]) == k
+        assert float(o["scale"][gi]) == a and float(o["zero"][gi]) == b
+
+
+def test_fp32_mode_int_exact_data_gives_the_exact_fit():
+    """With small dyadic weights and power-of-two saliencies every fp32 sum
+    and product of the fp32 mode is exact, so its slope is the exact weighted
+    least-squares slope (Eq. ridgefit) rounded once, and it equals the fp64
+    mode's."""
+    rng = np.random.default_rng(5)
+    for _ in range(20):
+        w = (rng.integers(-64, 65, size=16) / 64.0).astype(np.float32)
+        h = (2.0 ** rng.integers(-3, 4, size=16)).astype(np.float32)
+        o32 = run_group(w, h, bits=2, clips=(1.0,), fp32_mode=True)
+        o64 = run_group(w, h, bits=2, clips=(1.0,))
+        q = [int(x) for x in o32["codes"][0]]
+        sh = sum(_f(x) for x in h)
+        shq = sum(_f(x) * qi for x, qi in zip(h, q))
+        shqq = sum(_f(x) * qi * qi for x, qi in zip(h, q))
+        shw = sum(_f(x) * _f(y) for x, y in zip(h, w))
+        shqw = sum(_f(x) * qi * _f(y) for x, qi, y in zip(h, q, w))
+        d = sh * shqq - shq * shq
+        if d == 0:
+            continue
+        a_exact = (sh * shqw - shq * shw) / d
+        assert float(o32["scale"][0]) == X.fp32_from_fraction(a_exact)
+        assert float(o32["scale"][0]) == float(o64["scale"][0])
+
+
+def _nvfp4_fp32_block(w, h, st, clips):
+    """The literal fp32 reading of Sec. 4.2 for one 16-block: codes by brute
+    force on the fp32 products w (1/m) (6/f), scale-only moments accumulated
+    in fp32, s* = sum h q w / sum h q^2 in fp32, the E4M3 value nearest to
+    s*/S_t by brute force (ties to the even mantissa, saturating), and the
+    score accumulated in fp32.  Returns (scores, first argmin, its E4M3 byte)."""
+    wf = [_f(x) for x in w]
+    hf = [_f(x) for x in h]
+    m = max(abs(x) for x in wf)
+    rm = _r32(1 / m)
+    u = [_r32(x * rm) for x in wf]
+    levels = X.e4m3_levels()
+    stf = _f(st)
+    res = []
+    for f in clips:
+        ck = _r32(6 / _f(f))
+        qv = []
+        for x in u:
+            y = _r32(x * ck)
+            qv.append(Fraction(X.E2M1_LEVELS[X.e2m1_nearest_index(float(abs(y)))]) * (1 if y >= 0 else -1))
+        sqq = sqw = Fraction(0)
+        for wi, hi, qi in zip(wf, hf, qv):
+            hq = _r32(hi * qi)
+            sqq = _r32(sqq + _r32(hq * qi))
+            sqw = _r32(sqw + _r32(hq * wi))
+        sstar = _r32(_r32(_f(f) * m) / 6) if sqq == 0 else _r32(sqw / sqq)
+        x = _r32(sstar / stf)
+        # nearest E4M3 value to x >= 0, ties to the even mantissa, saturating at 448
+        best = None
+        for val, code in levels:
+            dist = abs(_f(val) - x)
+            if best is None or dist < best[0] or (dist == best[0] and code % 2 == 0):
+                best = (dist, code, val)
+        e_code, e_val = best[1], best[2]
+        sblk = _r32(stf * _f(e_val))
+        s = Fraction(0)
+        for wi, hi, qi in zip(wf, hf, qv):
+            dd = _r32(_r32(sblk * qi) - wi)
+            s = _r32(s + _r32(_r32(hi * dd) * dd))
+        res.append((float(s), e_code))
+    scores = [r[0] for r in res]
+    k = scores.index(min(scores))
+    return scores, k, res[k][1]
+
+
+def test_fp32_mode_nvfp4_against_exact_fp32_emulation():
+    clips = tuple(synth.clip_grid(1.0, 0.7, 4))
+    Wh, vh, _ = small_matrix(2, 64, 61, bf16=True)
+    o = oracle.reconstruct(Wh, vh, fmt="nvfp4", clips=clips, fp32_mode=True, want_scores=True)
+    w, h = w_as_f32(Wh).reshape(-1, 16), vh.reshape(-1, 16)
+    st = float(o["tensor_scale"])
+    for gi in range(w.shape[0]):
+        scores, k, e = _nvfp4_fp32_block(w[gi], h[gi], st, clips)
+        assert o["scores"][gi].tolist() == scores, gi
+        assert int(o["best"][gi]) == k and int(o["e4m3"][gi]) == e
+
+
+def test_nvfp4_diag_ratio_is_the_exact_fitted_ratio():
+    """diag[2] (the ratio s*/S_t of the chosen clip, which the parity protocol
+    uses to recognise an E4M3 midpoint) against exact rationals: s* =
+    sum h q w / sum h q^2 over the chosen codes, or the search scale f m / 6
+    when no weight with saliency has a non-zero code (one block here)."""
+    Wh, vh, _ = small_matrix(4, 128, 62, bf16=True)
+    w = w_as_f32(Wh).reshape(-1, 16)
+    h = vh.reshape(-1, 16).copy()
+    clips = tuple(synth.clip_grid(1.0, 0.7, 8))
+    # block 3: saliency only where the code is 0 at every clip (|y| < 0.25 f)
+    small = np.abs(w[3]) < 0.2 * 0.7 * np.abs(w[3]).max() / 6
+    assert small.any()
+    h[3] = np.where(small, h[3], 0.0)
+    o = oracle.reconstruct(Wh, h.reshape(vh.shape), fmt="nvfp4", clips=clips, want_scores=True, want_diag=True)
+    st = _f(o["tensor_scale"])
+    codes = o["codes"].reshape(-1, 16)
+    for gi in range(w.shape[0]):
+        k = int(o["best"][gi])
+        qv = [Fraction(X.E2M1_LEVELS[c & 7]) * (-1 if c & 8 else 1) for c in codes[gi]]
+        sqq = sum(_f(hi) * qi * qi for hi, qi in zip(h[gi], qv))
+        sqw = sum(_f(hi) * qi * _f(wi) for hi, qi, wi in zip(h[gi], qv, w[gi]))
+        m = max(abs(_f(x)) for x in w[gi])
+        sstar = _f(clips[k]) * m / 6 if sqq == 0 else sqw / sqq
+        x = float(sstar / st)
+        if gi == 3:
+            assert sqq == 0
+        assert abs(o["diag"][gi, 2] - x) <= 1e-13 * abs(x), (gi, o["diag"][gi, 2], x)
+
+
+def test_int_standard_qat_diag_against_exact_rtn():
+    """diag[0] (the score of Standard QAT, Sec. 3.1: the min-max range with
+    its own scale (max - min)/qmax and zero min, no fit) against the exact
+    rational score; the oracle forms scale and zero in fp32, so the root
+    scores may differ by sqrt(sum h) times a few fp32 roundings of |w|.
+    Groups with a weight within 1e-5 code units of a rounding boundary are
+    skipped (the fp32 recipe may round it the other way)."""
+    for bits, group in ((4, 128), (3, 64), (2, 64)):
+        qmax = (1 << bits) - 1
+        w, h, o = _int_groups(bits, group, tuple(synth.clip_grid(1.0, 0.7, 4)), seed=70 + bits)
+        checked = 0
+        for gi in range(w.shape[0]):
+            mn, mx = _f(w[gi].min()), _f(w[gi].max())
+            s1 = (mx - mn) / qmax
+            q, dist = X.rtn_codes_exact(w[gi], mn, s1, qmax)
+            if dist.min() < 1e-5:
+                continue
+            ex = sum(_f(hi) * (s1 * int(qi) + mn - _f(wi)) ** 2 for hi, qi, wi in zip(h[gi], q, w[gi]))
+            delta = 2.0 ** -20 * (float(mx - mn) + float(abs(mn)) + float(abs(mx)))
+            bound = math.sqrt(float(np.sum(h[gi], dtype=np.float64))) * delta
+            assert abs(math.sqrt(o["diag"][gi, 0]) - math.sqrt(float(ex))) <= bound, gi
+            checked += 1
+        assert checked >= 0.8 * w.shape[0]
+        np.testing.assert_array_equal(o["diag"][:, 1], o["scores"][:, 0])  # diag[1]: the first clip's score
+
+
+def test_nvfp4_standard_qat_diag_against_exact():
+    """diag[0] for NVFP4: codes of the search scale m/6, the E4M3 value
+    nearest to (m/6)/S_t (brute force, ties to even), the fp32 product S_t e
+    as the block's dequantiser, score in exact rationals."""
+    Wh, vh, _ = small_matrix(4, 128, 63, bf16=True)
+    o = oracle.reconstruct(Wh, vh, fmt="nvfp4", clips=(1.0, 0.8), want_diag=True)
+    w, h = w_as_f32(Wh).reshape(-1, 16), vh.reshape(-1, 16)
+    st = float(o["tensor_scale"])
+    levels = X.e4m3_levels()
+    mids = [Fraction(1, 4), Fraction(3, 4), Fraction(5, 4), Fraction(7, 4), Fraction(5, 2), Fraction(7, 2), Fraction(5)]
+    for gi in range(w.shape[0]):
+        m = max(abs(_f(x)) for x in w[gi])
+        ys = [_f(x) * 6 / m for x in w[gi]]
+        if any(abs(abs(y) - t) < Fraction(1, 10 ** 5) for y in ys for t in mids):
+            continue
+        qv = [Fraction(X.E2M1_LEVELS[X.e2m1_nearest_index(float(abs(y)))]) * (1 if y >= 0 else -1) for y in ys]
+        x = (m / 6) / _f(st)
+        best = min(levels, key=lambda lc: (abs(_f(lc[0]) - x), lc[1] % 2))
+        sblk = _f(np.float32(np.float32(st) * np.float32(best[0])))
+        ex = sum(_f(hi) * (sblk * qi - _f(wi)) ** 2 for hi, qi, wi in zip(h[gi], qv, w[gi]))
+        assert abs(o["diag"][gi, 0] - float(ex)) <= 1e-12 * float(ex) + 1e-300, gi
+
+
+@pytest.mark.parametrize("bits,group", [(4, 128), (3, 128), (2, 64)])
+def test_normal_equations_of_the_emitted_fit(bits, group):
+    """Eq. ridgefit's solution makes the weighted residuals orthogonal to 1
+    and to q: sum h e = sum h q e = 0.  The emitted (s, z) are that solution
+    rounded to fp32, so with e = s q + z - w in exact arithmetic,
+    |sum h e| <= u (Sv |z| + Svq |s|) and |sum h q e| <= u (Svq |z| + Svqq |s|),
+    u = 2^-24 (plus the fp64 evaluation's share).  Rank-deficient fits are
+    skipped."""
+    qmax = (1 << bits) - 1
+    w, h, o = _int_groups(bits, group, tuple(synth.clip_grid(1.0, 0.5, 6)), seed=80 + bits)
+    codes = o["codes"].reshape(-1, group)
+    for gi in range(w.shape[0]):
+        if o["diag"][gi, 3] != 0:
+            continue
+        s, z = _f(o["scale"][gi]), _f(o["zero"][gi])
+        hq = [(_f(hi), int(qi), _f(wi)) for hi, qi, wi in zip(h[gi], codes[gi], w[gi])]
+        sv = sum(x for x, _, _ in hq)
+        svq = sum(x * q for x, q, _ in hq)
+        svqq = sum(x * q * q for x, q, _ in hq)
+        g1 = sum(x * (s * q + z - y) for x, q, y in hq)
+        g2 = sum(x * q * (s * q + z - y) for x, q, y in hq)
+        u = 2.0 ** -24 * 1.001
+        slack = 1e-12 * float(sv) * (abs(float(s)) * qmax + abs(float(z)))
+        assert abs(float(g1)) <= u * float(sv * abs(z) + svq * abs(s)) + slack, (gi, float(g1))
+        assert abs(float(g2)) <= u * float(svq * abs(z) + svqq * abs(s)) + qmax * slack, (gi, float(g2))
