@@ -151,6 +151,19 @@ def kernel_bytes_per_weight(wl) -> float:
     return algorithmic_bytes_per_weight(wl, amax_pass=False)
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (Linux /proc/cpuinfo), or the platform's."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or platform.machine()
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=int(os.environ.get("WORLD_SIZE", "1")))
@@ -166,8 +179,8 @@ def main(argv=None):
                     help="saliency weighting variant (h: the method's default)")
     ap.add_argument("--param-dtype", default="fp32", choices=["fp32", "fp16", "bf16"],
                     help="deployed precision of the INT dequantiser (s, z)")
-    ap.add_argument("--cpu-detail", action="store_true",
-                    help="also time the oracle's literal fp32 mode and one thread (reported in cpu_baseline)")
+    ap.add_argument("--no-cpu-detail", action="store_true",
+                    help="skip the oracle's literal fp32 mode and one-thread timings (reported in cpu_baseline)")
     ap.add_argument("--diagnostics", action="store_true",
                     help="report the chosen-clip histogram (GPU, whole step) and the mean score ratio to "
                          "min-max RTN at clip 1.0 (oracle sample)")
@@ -319,6 +332,29 @@ def main(argv=None):
         if s != Q.OK:
             raise Q.QuasarError(s, "quasar_reconstruct_batch")
 
+    # ---- plain copy of the same byte count: achievable bandwidth.  Measured
+    # before the warmup steps, so that the GPU runs at its working clocks by
+    # the time the timed steps start (it is untimed work for the step) -------
+    amax_pass = wl.fmt == "nvfp4" and not wl.adamw
+    bpw = algorithmic_bytes_per_weight(wl, amax_pass)
+    copy_gbps = None
+    if not args.no_copy_baseline:
+        nbytes = min(int(n_per_step * bpw / 2), 4 << 30)
+        src = torch.empty(nbytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        reps = 10
+        for _ in range(reps):
+            dst.copy_(src)
+        b.record(stream)
+        torch.cuda.synchronize()
+        copy_gbps = 2 * nbytes * reps / (a.elapsed_time(b) * 1e-3) / 1e9
+        del src, dst
+
     # ---- warmup ----------------------------------------------------------------
     if wl.adamw and wl.fmt == "nvfp4":
         for m in mats:
@@ -368,8 +404,6 @@ def main(argv=None):
         step_k.append(sum(launch_ms[sl]) + (sum(amax_ms[sl]) if amax_ms else 0.0))
     step_pct = [round(float(x), 4) for x in np.percentile(step_k, [10, 50, 90])]
 
-    amax_pass = wl.fmt == "nvfp4" and not wl.adamw
-    bpw = algorithmic_bytes_per_weight(wl, amax_pass)
     gw_s = n_per_step / (ms_per_step * 1e-3) / 1e9
     gbps = gw_s * bpw
     # dominant kernel: the reconstruct kernel; its algorithmic bytes over the
@@ -381,30 +415,14 @@ def main(argv=None):
     k_gbps = k_bytes / k_time / 1e9
     avg_launch_us = 1e3 * sum(launch_ms) / len(launch_ms)
 
-    # ---- plain copy of the same byte count: achievable bandwidth -----------------
-    copy_gbps = None
-    if not args.no_copy_baseline:
-        nbytes = min(int(n_per_step * bpw / 2), 4 << 30)
-        src = torch.empty(nbytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        reps = 10
-        for _ in range(reps):
-            dst.copy_(src)
-        b.record(stream)
-        torch.cuda.synchronize()
-        copy_gbps = 2 * nbytes * reps / (a.elapsed_time(b) * 1e-3) / 1e9
-        del src, dst
-
     # ---- CPU oracle on a bounded row sample (reported baseline) ----------------
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
-        threads = min(16, os.cpu_count() or 1)
+        # the CPUs this process may use, at most 16 (a one-GPU machine's share of
+        # its host: worker pools there are sized to 16 whatever the host has)
+        allowed = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+        threads = max(1, min(16, allowed))
 
         def oracle_rows(m, step, n_threads=None, fp32_mode=False, diag_out=None):
             nthr = threads if n_threads is None else n_threads
@@ -458,7 +476,7 @@ def main(argv=None):
                 break
             step = max(1, int(step * spent / args.cpu_seconds))
         detail = {}
-        if args.cpu_detail and wl.fmt in ("int", "nvfp4", "int_sym") and not wl.adamw:
+        if not args.no_cpu_detail and wl.fmt in ("int", "nvfp4", "int_sym") and not wl.adamw:
             # the same sample with the literal fp32 accumulation mode, and a
             # sparser sample on one thread
             fw, ft = 0, 0.0
@@ -475,7 +493,8 @@ def main(argv=None):
             detail["single_thread_value"] = round(sw / stt / 1e9, 6)
             detail["single_thread_sample"] = f"rows 0, {16 * step}, ... of every matrix ({sw} weights, {stt:.1f} s)"
         cpu = {"value": round(sample_w / t_cpu / 1e9, 6), "unit": "G weights/s", "cores": threads,
-               "kind": "oracle",
+               "kind": "oracle", "host_cpus": os.cpu_count(), "cpus_allowed": allowed, "cpu_model": cpu_model(),
+               "threads_rule": "min(16, CPUs this process may use): the host share of one GPU",
                "sample": f"{'block ' if wl.fmt == 'rubin' else ''}rows 0, {step}, {2 * step}, ... of every matrix "
                          f"of {args.workload} ({sample_w} weights, "
                          f"{t_cpu:.1f} s wall = {t_cpu * threads:.0f} thread-s on {threads} threads; "
@@ -487,6 +506,7 @@ def main(argv=None):
     t_hbm, t_alu = kbpw / (PEAK_HBM_GBPS * 1e9), ops_w / (PEAK_VALU_TOPS * 1e12)
     traffic = None
     traffic_ratio = None
+    prof = None
     try:
         with open(TRAFFIC_FILE) as f:
             tr = json.load(f)
@@ -495,6 +515,17 @@ def main(argv=None):
             # measured HBM bytes per weight (calibrated FETCH_SIZE + WRITE_SIZE) per launch
             traffic = round(ent["bytes_per_weight"] * sum(launch_w) / len(launch_w))
             traffic_ratio = round(ent["bytes_per_weight"] / kbpw, 4)
+            if ent.get("rocprof_avg_us") and (args.weighting, args.param_dtype) == ("h", "fp32"):
+                # the committed rocprofv3 kernel trace of this workload: its
+                # average kernel duration, the frac it gives, and the bench
+                # line taken in the same session without the profiler
+                pw = ent["rocprof_weights_per_launch"]
+                prof = {"rocprof_avg_us": ent["rocprof_avg_us"],
+                        "frac": round(pw * kbpw / (ent["rocprof_avg_us"] * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4),
+                        "same_session_bench_avg_launch_us": ent.get("bench_avg_launch_us"),
+                        "trace_overhead": ent.get("trace_overhead"),
+                        "valu_lane_ops_per_weight_measured": ent.get("valu_lane_ops_per_weight"),
+                        "file": f"profiles/{ent['kernel']}_{args.workload}_kernel_stats.txt"}
     except (OSError, ValueError, KeyError):
         pass
     if wl.fmt in ("int", "int_sym"):
@@ -513,6 +544,8 @@ def main(argv=None):
                     "valu_frac": round(ops_w * k_wps / 1e12 / PEAK_VALU_TOPS, 4)}
     roofline.update({"kernel": kname, "bytes_per_weight": kbpw, "valu_ops_per_weight": ops_w,
                      "traffic_over_algorithmic": traffic_ratio, "avg_launch_us": round(avg_launch_us, 2)})
+    if prof is not None:
+        roofline["profile"] = prof
     if absmax_us is not None:
         roofline["absmax_avg_launch_us"] = round(absmax_us, 2)
     line = {

@@ -340,4 +340,72 @@ __device__ __forceinline__ void wave_lds_fence() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// ---- coalesced stores of a wavefront's stretch of a tensor -------------------
+// A wavefront whose lanes hold 16 consecutive elements each covers one
+// contiguous stretch of 1024 elements: lane l's 16 start at element
+// 16 idx(l) of it, idx a permutation of the lanes.  Stored straight from the
+// registers, every store instruction writes a 16-byte piece of each of 64
+// different cache lines, and the lines are completed by later instructions.
+// Written into LDS in stretch order and read back 16 bytes per lane in memory
+// order, each store instruction writes 1 KB of whole lines instead.  One
+// 16-byte pad after every PER chunks of 16 bytes keeps the LDS writes free of
+// bank conflicts: PER is the chunks of one group (spread layouts, where lanes
+// 0..7 hold the first chunks of eight groups) or of one lane (consecutive
+// layouts).
+struct WaveImage {
+  uint4* stage;  // this wavefront's LDS area: wave_stage_chunks() chunks of 16 bytes
+  int64_t e0;    // the stretch's first element
+  int64_t n;     // how many of its 1024 elements exist (<= 0: none)
+  int idx;       // this lane's 16 elements start at element 16 idx of the stretch
+  int lane;
+};
+
+template <int ESZ, int PER>
+__host__ __device__ constexpr int wave_stage_chunks() {
+  return 64 * ESZ + 64 * ESZ / PER;  // ESZ chunks per lane for 16 elements of ESZ bytes
+}
+
+// Every lane of the wavefront takes part; `base` is the tensor (16-byte
+// aligned), and elements of the stretch at or past n are not written.
+// wave_put writes the lane's chunk c (c < ESZ: its elements 16 c / ESZ
+// onwards) into the stage, after a wave_lds_fence() that follows any earlier
+// use of the stage; wave_flush then stores the whole stretch and leaves the
+// stage free.  wave_store does both for the lane's 16 elements given as
+// 4 ESZ dwords in element order.
+template <int ESZ, int PER>
+__device__ __forceinline__ void wave_put(const WaveImage& im, int c, uint4 x) {
+  const int ch = im.idx * ESZ + c;
+  im.stage[ch + ch / PER] = x;
+}
+template <int ESZ, int PER>
+__device__ __forceinline__ void wave_flush(const WaveImage& im, void* base) {
+  static_assert(ESZ == 2 || ESZ == 4, "bf16 or fp32 elements");
+  wave_lds_fence();
+  // one chunk in flight at a time: fewer live registers than reading all
+  // chunks first, which the kernels around this cannot spare
+  uint4* out = reinterpret_cast<uint4*>(base) + (im.e0 * ESZ) / 16;
+#pragma unroll
+  for (int t = 0; t < ESZ; t++) {
+    const int ch = im.lane + 64 * t;
+    const uint4 x = im.stage[ch + ch / PER];
+    if ((int64_t)ch * (16 / ESZ) < im.n) out[ch] = x;
+  }
+  wave_lds_fence();
+}
+template <int ESZ, int PER>
+__device__ __forceinline__ void wave_store(const WaveImage& im, void* base, const uint32_t (&d)[4 * ESZ]) {
+  wave_lds_fence();  // earlier reads of the stage by this wavefront are done
+#pragma unroll
+  for (int c = 0; c < ESZ; c++) wave_put<ESZ, PER>(im, c, make_uint4(d[4 * c], d[4 * c + 1], d[4 * c + 2], d[4 * c + 3]));
+  wave_flush<ESZ, PER>(im, base);
+}
+
+template <int PER>
+__device__ __forceinline__ void wave_store_f32(const WaveImage& im, float* base, const float (&x)[16]) {
+  uint32_t d[16];
+#pragma unroll
+  for (int i = 0; i < 16; i++) d[i] = as_u32(x[i]);
+  wave_store<4, PER>(im, base, d);
+}
+
 }  // namespace quasar

@@ -111,8 +111,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   constexpr int OWN = kMaxClips / L;         // clips a lane may own
   constexpr int CPL = kCellsPerLane;         // most cells per lane
   static_assert(kThreads == kCellBuckets && kThreads == kMaxClips * kCellSteps, "one table entry per thread");
+  static_assert((size_t)int_stage_bytes<kSpread, G>() == int_cells_stage_bytes(G), "the launch sizes the stage");
 
-  extern __shared__ double s_hist[];  // [wave][group slot][cell][h, h w]
+  extern __shared__ __align__(16) double s_hist[];  // [wave][group slot][cell][h, h w], or the store stage
   __shared__ uint4 s_bucket[kCellBuckets];
   __shared__ uint8_t s_tp[kMaxClips * kCellSteps];
   __shared__ float s_alpha[kMaxClips], s_clip[kMaxClips];
@@ -138,21 +139,27 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
 
   int64_t blk = blockIdx.x;
   const IntMatrix mtx = int_matrix(p, blk);
-  int64_t gid = (blk * (kThreads / 64) + wave) * GPW + slot;
+  const int64_t wave_g0 = (blk * (kThreads / 64) + wave) * GPW;
+  int64_t gid = wave_g0 + slot;
   const bool active = gid < mtx.n_groups;
   if (!active) gid = mtx.n_groups - 1;  // recompute the last group; nothing is stored
   const int64_t e0 = gid * G + (int64_t)j * N;
 
+  // this wavefront's LDS: its groups' cells, before that the stage of the
+  // EMA's store, and after them the stage of the exact path and of r's store
+  const int cpl = p.cells.cpl;
+  double* const s_wave = s_hist + (size_t)wave * (int_cells_wave_bytes(G, cpl) / sizeof(double));
+  const WaveImage im = int_image<L>(s_wave, wave_g0, mtx.n_groups, slot, j, lane);
+
   WRegs<W_BF16> wr;
   float v[N];
-  int_load<W_BF16, EMA>(p, mtx, e0, active, wr, v);
+  int_load<W_BF16, EMA, kSpread, G>(p, mtx, im, e0, wr, v);
   const IntRange rg = int_range<L, SYM, W_BF16, kSpread>(wr);
 
   // ---- this group's cells: lane j owns cells [j cpl, (j + 1) cpl) -----------
   // Groups are int_cells_stride(cpl) cells apart, an odd number, so that the
   // same cell of the wavefront's groups falls in different LDS banks.
-  const int cpl = p.cells.cpl;
-  double* hist = s_hist + (size_t)(wave * GPW + slot) * int_cells_stride<L>(cpl) * 2;
+  double* hist = s_wave + (size_t)slot * int_cells_stride<L>(cpl) * 2;
   double* mine = hist + 2 * j * cpl;
 #pragma unroll
   for (int i = 0; i < CPL; i++)
@@ -360,20 +367,26 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   }
   {
     // The wavefront's cell areas are no longer needed: they stage the
-    // flagged groups.  A member lane reads its saliencies again (v' when this
-    // kernel stored it: a lane's load after its own store to the same
-    // address returns the stored value).
+    // flagged groups.  A member lane reads its saliencies again: v' when this
+    // kernel stored it, written by another lane of this wavefront, which the
+    // workgroup-scope fences make visible (the workgroup's waves share the
+    // compute unit's vector cache).
     auto load_h = [&](float (&hv)[N]) {
+      if constexpr (EMA != 0) {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+      }
       load16<false>(mtx.v, e0, hv);
 #pragma unroll
       for (int i = 0; i < N; i++) hv[i] = weight_of(hv[i], p.weighting);
     };
-    float* stage = reinterpret_cast<float*>(s_hist + (size_t)wave * GPW * int_cells_stride<L>(cpl) * 2);
     int_exact_wave<L, SYM, QMAX, kSpread, W_BF16>(p, wr, load_h, rg, s_alpha, s_clip, lane,
-                                                  ill && active && !rg.constant, stage, best);
+                                                  ill && active && !rg.constant, reinterpret_cast<float*>(s_wave),
+                                                  best);
   }
 
-  int_finish<W_BF16, BITS, G, SYM, kSpread>(p, mtx, wr, rg, mo.Sv, best, s_alpha, s_win[wave][slot], j, gid, e0,
+  int_finish<W_BF16, BITS, G, SYM, kSpread>(p, mtx, wr, rg, mo.Sv, best, s_alpha, s_win[wave][slot], j, gid, im,
                                          active);
 }
 

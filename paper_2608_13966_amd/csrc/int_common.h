@@ -89,13 +89,32 @@ __device__ __forceinline__ IntMatrix int_matrix(const IntParams& p, int64_t& blk
   return m;
 }
 
+// Pads of the store stage (wave_store) for the INT kernels' layouts: a group
+// is G ESZ / 16 chunks of 16 bytes, a lane of a consecutive layout ESZ.
+template <bool SPREAD, int G, int ESZ>
+__host__ __device__ constexpr int int_stage_per() { return SPREAD ? G * ESZ / 16 : ESZ; }
+// LDS of one wavefront's store stage (fp32 stretches, the larger)
+template <bool SPREAD, int G>
+__host__ __device__ constexpr int int_stage_bytes() { return 16 * wave_stage_chunks<4, int_stage_per<SPREAD, G, 4>()>(); }
+
+// The wavefront's stretch of the matrix: groups wave_g0 .. wave_g0 + 64 / L - 1.
+template <int L>
+__device__ __forceinline__ WaveImage int_image(void* stage, int64_t wave_g0, int64_t n_groups, int slot, int j,
+                                               int lane) {
+  constexpr int G = L * kIntN;
+  const int64_t left = (n_groups - wave_g0) * G;
+  return WaveImage{reinterpret_cast<uint4*>(stage), wave_g0 * G, left < 1024 ? left : 1024, slot * L + j, lane};
+}
+
 // Load the lane's 16 weights and saliencies (each byte of W, v, g once, with
 // 128-bit loads), run the fused EMA (EMA 1/2) or AdamW step (EMA 3/4) and
-// store their results, then apply the saliency weighting: h = v, v*v
-// (App. A.3) or 1 (Table 5).  W stays in its storage format in registers.
-template <bool W_BF16, int EMA>
-__device__ __forceinline__ void int_load(const IntParams& p, const IntMatrix& mtx, int64_t e0, bool active,
+// store their results (coalesced through the wavefront's stage), then apply
+// the saliency weighting: h = v, v*v (App. A.3) or 1 (Table 5).  W stays in
+// its storage format in registers.
+template <bool W_BF16, int EMA, bool SPREAD, int G>
+__device__ __forceinline__ void int_load(const IntParams& p, const IntMatrix& mtx, const WaveImage& im, int64_t e0,
                                          WRegs<W_BF16>& wr, float (&v)[kIntN]) {
+  constexpr int P4 = int_stage_per<SPREAD, G, 4>(), P2 = int_stage_per<SPREAD, G, 2>();
   wr.load(mtx.W, e0);
   load16<false>(mtx.v, e0, v);
   if constexpr (EMA == 1 || EMA == 2) {
@@ -108,7 +127,7 @@ __device__ __forceinline__ void int_load(const IntParams& p, const IntMatrix& mt
       float u = p.omb2 * t;
       v[i] = __builtin_fmaf(p.beta2, v[i], u);
     }
-    if (active) store16<false>(mtx.v, e0, v);
+    wave_store_f32<P4>(im, mtx.v, v);
   } else if constexpr (EMA >= 3) {
     // one AdamW step first; the updated W is reconstructed and the updated
     // second moment is the saliency
@@ -119,11 +138,12 @@ __device__ __forceinline__ void int_load(const IntParams& p, const IntMatrix& mt
     for (int i = 0; i < kIntN; i++) w[i] = wr.get(i);
     adamw16(w, m, v, g, p.adam, p.beta2, p.omb2);
     wr.set(w);  // bf16 W: rounded here, and the rounded value is reconstructed
-    if (active) {
-      store16<false>(mtx.v, e0, v);
-      store16<false>(mtx.m, e0, m);
-      wr.store(mtx.Wu, e0);
-    }
+    wave_store_f32<P4>(im, mtx.v, v);
+    wave_store_f32<P4>(im, mtx.m, m);
+    if constexpr (W_BF16)
+      wave_store<2, P2>(im, mtx.Wu, wr.d);
+    else
+      wave_store_f32<P4>(im, static_cast<float*>(mtx.Wu), wr.f);
   }
   if (p.weighting != 0) {
 #pragma unroll
@@ -517,8 +537,9 @@ __device__ __forceinline__ void int_fit_score(const IntParams& p, int k, float f
 template <bool W_BF16, int BITS, int G, bool SYM, bool SPREAD = false>
 __device__ __forceinline__ void int_finish(const IntParams& p, const IntMatrix& mtx, const WRegs<W_BF16>& wr,
                                            const IntRange& g, double Sv, const IntBest& best, const float* s_alpha,
-                                           float* win, int j, int64_t gid, int64_t e0, bool active) {
+                                           float* win, int j, int64_t gid, const WaveImage& im, bool active) {
   constexpr int L = G / kIntN;
+  constexpr int P4 = int_stage_per<SPREAD, G, 4>(), P2 = int_stage_per<SPREAD, G, 2>();
   constexpr int QMAX = SYM ? (1 << (BITS - 1)) - 1 : (1 << BITS) - 1;
   constexpr float kQmax = (float)QMAX;
   constexpr float kQmin = SYM ? -(float)QMAX : 0.0f;
@@ -544,7 +565,9 @@ __device__ __forceinline__ void int_finish(const IntParams& p, const IntMatrix& 
   }
 
   // two chunks of 8 weights: codes and r of a chunk are formed and its r
-  // stored before the next chunk, which keeps few values live at once
+  // staged before the next chunk, which keeps few values live at once
+  const bool r_bf16 = W_BF16 || p.r_bf16;
+  if (mtx.r) wave_lds_fence();  // the stage's earlier use is done
   uint64_t bits = 0;  // this lane's 16 codes, code i at bits [BITS i, BITS i + BITS)
 #pragma unroll
   for (int h = 0; h < 2; h++) {
@@ -570,17 +593,21 @@ __device__ __forceinline__ void int_finish(const IntParams& p, const IntMatrix& 
       }
       bits |= (uint64_t)qi << (BITS * i);
     }
-    if (active && mtx.r) {
-      if (W_BF16 || p.r_bf16) {
-        uint16_t* pr = reinterpret_cast<uint16_t*>(mtx.r) + e0 + 8 * h;
-        st128(pr, make_uint4(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]), pack_bf16x2(r[4], r[5]),
-                             pack_bf16x2(r[6], r[7])));
+    if (mtx.r) {
+      if (r_bf16) {
+        wave_put<2, P2>(im, h, make_uint4(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]), pack_bf16x2(r[4], r[5]),
+                                          pack_bf16x2(r[6], r[7])));
       } else {
-        float* pr = reinterpret_cast<float*>(mtx.r) + e0 + 8 * h;
-        st128(pr, make_uint4(as_u32(r[0]), as_u32(r[1]), as_u32(r[2]), as_u32(r[3])));
-        st128(pr + 4, make_uint4(as_u32(r[4]), as_u32(r[5]), as_u32(r[6]), as_u32(r[7])));
+        wave_put<4, P4>(im, 2 * h, make_uint4(as_u32(r[0]), as_u32(r[1]), as_u32(r[2]), as_u32(r[3])));
+        wave_put<4, P4>(im, 2 * h + 1, make_uint4(as_u32(r[4]), as_u32(r[5]), as_u32(r[6]), as_u32(r[7])));
       }
     }
+  }
+  if (mtx.r) {
+    if (r_bf16)
+      wave_flush<2, P2>(im, mtx.r);
+    else
+      wave_flush<4, P4>(im, mtx.r);
   }
   // INT3: members 2i and 2i + 1 hold bits [96 i, 96 i + 96) of the group's
   // stream, three whole dwords; the even member needs the odd one's low bits

@@ -43,7 +43,10 @@ void int_reconstruct_kernel(IntParams p) {
   constexpr float kQmin = SYM ? -(float)QMAX : 0.0f;
   constexpr float kBeta = 0.5f * (float)QMAX;
 
-  __shared__ double s_red[kThreads / 64][64 * KC];
+  // per wavefront: the moment transpose, the exact path's stage, the stage of
+  // the coalesced stores
+  constexpr int RED = 64 * KC > int_stage_bytes<false, G>() / 8 ? 64 * KC : int_stage_bytes<false, G>() / 8;
+  __shared__ __align__(16) double s_red[kThreads / 64][RED];
   __shared__ float s_alpha[kMaxClips], s_clip[kMaxClips];
   __shared__ float s_win[kThreads / 64][GPW][4];
 
@@ -60,16 +63,19 @@ void int_reconstruct_kernel(IntParams p) {
 
   int64_t blk = blockIdx.x;
   const IntMatrix mtx = int_matrix(p, blk);
-  int64_t gid = (blk * (kThreads / 64) + wave) * GPW + slot;
+  const int64_t wave_g0 = (blk * (kThreads / 64) + wave) * GPW;
+  int64_t gid = wave_g0 + slot;
   const bool active = gid < mtx.n_groups;
   if (!active) gid = mtx.n_groups - 1;  // recompute the last group; nothing is stored
   const int64_t e0 = gid * G + (int64_t)j * N;
+  double* red = s_red[wave];
+  const WaveImage im = int_image<L>(red, wave_g0, mtx.n_groups, slot, j, lane);
 
   // W stays in its storage format in registers (bf16: 8 dwords) and is widened
   // on use, which keeps the kernel inside 128 VGPRs (4 waves per SIMD).
   WRegs<W_BF16> wr;
   float v[N];
-  int_load<W_BF16, EMA>(p, mtx, e0, active, wr, v);
+  int_load<W_BF16, EMA, false, G>(p, mtx, im, e0, wr, v);
   const IntRange rg = int_range<L, SYM>(wr);
 
   // clip-independent moments (fp64), accumulated in the first pass
@@ -78,7 +84,6 @@ void int_reconstruct_kernel(IntParams p) {
   IntMoments mo = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0x1p-47, (double)fmaxf(fabsf(rg.mn), fabsf(rg.mx)),
                    0.0, 0.0, 0.0};
   IntBest best = int_best_init();
-  double* red = s_red[wave];
 
   // One pass over the lane's 16 weights for clips k0 .. k0+KC-1 (entries past
   // the last clip repeat it and are never selected).
@@ -182,7 +187,7 @@ void int_reconstruct_kernel(IntParams p) {
                                                 ill && active && !rg.constant, reinterpret_cast<float*>(red), best);
   }
 
-  int_finish<W_BF16, BITS, G, SYM>(p, mtx, wr, rg, mo.Sv, best, s_alpha, s_win[wave][slot], j, gid, e0, active);
+  int_finish<W_BF16, BITS, G, SYM>(p, mtx, wr, rg, mo.Sv, best, s_alpha, s_win[wave][slot], j, gid, im, active);
 }
 
 template <bool W_BF16, int EMA, int BITS, int G>

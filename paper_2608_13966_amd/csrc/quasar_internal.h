@@ -102,11 +102,18 @@ struct IntCells {
 template <int L>
 __host__ __device__ constexpr int int_cells_stride(int cpl) { return (L * cpl) | 1; }
 
-// LDS of one workgroup of the binned kernel: 64 / L groups per wavefront,
-// h and h w in fp64 per cell.
+// LDS of one wavefront of the binned kernel: 64 / L groups' cells (h and h w
+// in fp64 per cell), or, where that is less, the stage of its coalesced
+// stores (a 1024-element fp32 stretch plus one 16-byte pad per group).
+constexpr size_t int_cells_stage_bytes(int group) { return (size_t)(256 + 1024 / group) * 16; }
+constexpr size_t int_cells_wave_bytes(int group, int cpl) {
+  const size_t cells = (size_t)(64 / (group / 16)) *
+                       (size_t)(group == 64 ? int_cells_stride<4>(cpl) : int_cells_stride<8>(cpl)) * 16;
+  return cells > int_cells_stage_bytes(group) ? cells : int_cells_stage_bytes(group);
+}
+// ... and of one workgroup
 constexpr size_t int_cells_lds_bytes(int group, int cpl) {
-  return (size_t)(kThreads / 64) * (size_t)(64 / (group / 16)) *
-         (size_t)(group == 64 ? int_cells_stride<4>(cpl) : int_cells_stride<8>(cpl)) * 16;
+  return (size_t)(kThreads / 64) * int_cells_wave_bytes(group, cpl);
 }
 
 // Per-call parameters of the INT-b kernels (passed by value as the kernel argument).
