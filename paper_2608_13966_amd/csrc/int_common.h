@@ -565,7 +565,12 @@ __device__ __forceinline__ void int_finish(const IntParams& p, const IntMatrix& 
   }
 
   // two chunks of 8 weights: codes and r of a chunk are formed and its r
-  // staged before the next chunk, which keeps few values live at once
+  // staged before the next chunk, which keeps few values live at once.  The
+  // positions u are formed again here from opaque copies of the range: the
+  // same expression earlier in the kernel would otherwise be kept, 16 values
+  // held in registers through everything in between.
+  float rrho = g.rrho, nc = g.nc;
+  asm volatile("" : "+v"(rrho), "+v"(nc));
   const bool r_bf16 = W_BF16 || p.r_bf16;
   if (mtx.r) wave_lds_fence();  // the stage's earlier use is done
   uint64_t bits = 0;  // this lane's 16 codes, code i at bits [BITS i, BITS i + BITS)
@@ -577,14 +582,14 @@ __device__ __forceinline__ void int_finish(const IntParams& p, const IntMatrix& 
       const int i = 8 * h + t;
       uint32_t qi;
       if constexpr (SYM) {
-        const float ui = wr.get(i) * g.rrho;
+        const float ui = wr.get(i) * rrho;
         // + 0.0f turns a rounded -0 into +0, so a zero code gives r = s * (+0)
         float q = __builtin_amdgcn_fmed3f(__builtin_rintf(ui * alpha), kQmin, kQmax) + 0.0f;
         if (g.constant) q = 0.0f;
         qi = (uint32_t)(int)q & ((1u << BITS) - 1u);  // two's complement in BITS bits
         r[t] = a * q;
       } else {
-        const float ui = __builtin_fmaf(wr.get(i), g.rrho, g.nc);
+        const float ui = __builtin_fmaf(wr.get(i), rrho, nc);
         float x = __builtin_fmaf(ui, alpha, kBeta);
         float q = __builtin_amdgcn_fmed3f(__builtin_rintf(x), 0.0f, kQmax);
         if (g.constant) q = 0.0f;
