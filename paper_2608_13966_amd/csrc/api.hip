@@ -388,9 +388,11 @@ int cell_bucket(float u) {
 //
 // With odd qmax every clip has a threshold just below u = 0, where the fp32
 // code rounding ties at qmax/2: T(k, (qmax+1)/2) lies in (-2^-20, 0).  These
-// tie thresholds are merged into one cell boundary at their least value;
-// a weight between the least and the greatest of them (the unsafe interval;
-// a few in ten million) makes the kernel sum its group's moments directly.
+// tie thresholds are merged into one cell boundary at their least value, and
+// the float after the greatest of them is one more boundary: the cell between
+// the two (the unsafe cell) holds the u for which the cell does not fix every
+// clip's code (a few weights in ten million), and a group with saliency there
+// has its moments summed directly.
 void int_cells(quasar::IntParams& p, int K, int bits, bool sym, int group) {
   memset(&p.cells, 0, sizeof(p.cells));
   const char* force = getenv("QUASAR_INT_PATH");
@@ -404,7 +406,7 @@ void int_cells(quasar::IntParams& p, int K, int bits, bool sym, int group) {
   {
     // at most K nb thresholds (the tie ones count once): when even that many
     // fit, or when they cannot fit at all, this is decided before any search
-    const int m_upper = K * nb - (tie > 0 ? K - 1 : 0);
+    const int m_upper = K * nb - (tie > 0 ? K - 2 : 0);
     const int limit = any_fit ? quasar::kCellsPerLane : quasar::kCellsPerLaneAuto;
     if ((m_upper + 1 + L - 1) / L > limit) return;
   }
@@ -446,6 +448,7 @@ void int_cells(quasar::IntParams& p, int K, int bits, bool sym, int group) {
   float srt[quasar::kMaxClips * quasar::kCellSteps];
   int m = 0;
   for (int i = 0; i < n; i++) srt[m++] = (merge && t[i] >= ulo && t[i] <= uhi) ? ulo : t[i];
+  if (merge) srt[m++] = nextafterf(uhi, INFINITY);  // the unsafe cell's upper end
   std::sort(srt, srt + m);
   m = (int)(std::unique(srt, srt + m) - srt);
   if (merge) {
@@ -474,8 +477,9 @@ void int_cells(quasar::IntParams& p, int K, int bits, bool sym, int group) {
   for (int i = 0; i < quasar::kCellThr; i++) p.cells.thr[i] = i < m ? srt[i] : NAN;
   p.cells.cpl = cpl;
   p.cells.cmax = cmax;
-  p.cells.unsafe_lo = merge ? ulo : INFINITY;
-  p.cells.unsafe_hi = merge ? uhi : INFINITY;
+  // cells count the thresholds at or below u: the unsafe cell is the one
+  // just above ulo
+  p.cells.unsafe_cell = merge ? (int)(std::lower_bound(srt, srt + m, ulo) - srt) + 1 : -1;
   p.cells.n_cells = m + 1;
 }
 

@@ -109,7 +109,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   constexpr int QMAX = SYM ? (1 << (BITS - 1)) - 1 : (1 << BITS) - 1;
   constexpr int NB = SYM ? 2 * QMAX : QMAX;  // code steps per clip
   constexpr int OWN = kMaxClips / L;         // clips a lane may own
-  constexpr int CPL = kCellsPerLane;         // most cells per lane
   static_assert(kThreads == kCellBuckets && kThreads == kMaxClips * kCellSteps, "one table entry per thread");
   static_assert((size_t)int_stage_bytes<kSpread, G>() == int_cells_stage_bytes(G), "the launch sizes the stage");
 
@@ -158,51 +157,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
 
   // ---- this group's cells: lane j owns cells [j cpl, (j + 1) cpl) -----------
   // Groups are int_cells_stride(cpl) cells apart, an odd number, so that the
-  // same cell of the wavefront's groups falls in different LDS banks.
+  // same cell of the wavefront's groups falls in different LDS banks.  The
+  // wavefront clears its whole area, 16 bytes per lane and step.
   double* hist = s_wave + (size_t)slot * int_cells_stride<L>(cpl) * 2;
   double* mine = hist + 2 * j * cpl;
-#pragma unroll
-  for (int i = 0; i < CPL; i++)
-    if (i < cpl) *reinterpret_cast<double2*>(mine + 2 * i) = make_double2(0.0, 0.0);
-  wave_lds_fence();
-
-  // ---- the cell of every weight (four bucket reads in flight at a time) -----
-  // Thresholds outside u's bucket lie on the far side of u and the table's
-  // padding is NaN, so cmax compares never pass the last threshold.
-  const float ulo = p.cells.unsafe_lo, uhi = p.cells.unsafe_hi;
-  bool unsafe = false;
-  uint32_t cells[N / 4];  // four cells per register, one byte each
-  auto bin = [&](auto cmax_tag) {
-    constexpr int C = decltype(cmax_tag)::value;
-#pragma unroll
-    for (int c4 = 0; c4 < N / 4; c4++) {
-      float u[4];
-      uint4 e[4];
-#pragma unroll
-      for (int t = 0; t < 4; t++) {
-        u[t] = int_u<SYM>(wr.get(4 * c4 + t), rg);
-        e[t] = s_bucket[cell_bucket(u[t])];
-      }
-      uint32_t packed = 0;
-#pragma unroll
-      for (int t = 0; t < 4; t++) {
-        uint32_t cell = e[t].x + (u[t] >= as_f32(e[t].y) ? 1u : 0u);
-        if constexpr (C > 1) cell += (u[t] >= as_f32(e[t].z) ? 1u : 0u);
-        if constexpr (C > 2) cell += (u[t] >= as_f32(e[t].w) ? 1u : 0u);
-        packed |= cell << (8 * t);
-        unsafe |= (u[t] >= ulo) & (u[t] <= uhi);
-      }
-      cells[c4] = packed;
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  };
-  const int cmax = p.cells.cmax;
-  if (cmax == 1)
-    bin(std::integral_constant<int, 1>{});
-  else if (cmax == 2)
-    bin(std::integral_constant<int, 2>{});
-  else
-    bin(std::integral_constant<int, 3>{});
+  {
+    const int n16 = GPW * int_cells_stride<L>(cpl);
+    uint4* z = reinterpret_cast<uint4*>(s_wave);
+#pragma unroll 1
+    for (int i = lane; i < n16; i += 64) z[i] = make_uint4(0u, 0u, 0u, 0u);
+  }
 
   // ---- h and h w of every weight into its cell, as exact integers --------------
   // h and h w are scaled by powers of two that bring the group's largest |h|
@@ -222,6 +186,44 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   const int eh = __builtin_amdgcn_frexp_expf(hmax), ew = __builtin_amdgcn_frexp_expf(wabs);
   const double sh = __builtin_amdgcn_ldexp(1.0, B - eh), shw = __builtin_amdgcn_ldexp(1.0, B - eh - ew);
   double Svww = 0.0;
+  wave_lds_fence();  // the cells are clear
+
+  // ---- the cell of every weight (four bucket reads in flight at a time) -----
+  // Thresholds outside u's bucket lie on the far side of u and the table's
+  // padding is NaN, so cmax compares never pass the last threshold.
+  uint32_t cells[N / 4];  // four cells per register, one byte each
+  auto bin = [&](auto cmax_tag) {
+    constexpr int C = decltype(cmax_tag)::value;
+#pragma unroll
+    for (int c4 = 0; c4 < N / 4; c4++) {
+      float u[4];
+      uint4 e[4];
+#pragma unroll
+      for (int t = 0; t < 4; t++) {
+        u[t] = int_u<SYM>(wr.get(4 * c4 + t), rg);
+        e[t] = s_bucket[cell_bucket(u[t])];
+      }
+      uint32_t packed = 0;
+#pragma unroll
+      for (int t = 0; t < 4; t++) {
+        uint32_t cell = e[t].x + (u[t] >= as_f32(e[t].y) ? 1u : 0u);
+        if constexpr (C > 1) cell += (u[t] >= as_f32(e[t].z) ? 1u : 0u);
+        if constexpr (C > 2) cell += (u[t] >= as_f32(e[t].w) ? 1u : 0u);
+        packed |= cell << (8 * t);
+      }
+      cells[c4] = packed;
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  const int cmax = p.cells.cmax;
+  if (cmax == 1)
+    bin(std::integral_constant<int, 1>{});
+  else if (cmax == 2)
+    bin(std::integral_constant<int, 2>{});
+  else
+    bin(std::integral_constant<int, 3>{});
+
+  // ---- h and h w of every weight into its cell --------------------------------
 #pragma unroll
   for (int i = 0; i < N; i++) {
     const int cell = (int)((cells[i >> 2] >> (8 * (i & 3))) & 0xffu);
@@ -234,27 +236,51 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   }
   wave_lds_fence();
 
+  // A weight among merged thresholds (rare) lies in the unsafe cell, where the
+  // cell does not fix every clip's code: its group takes the exact path below
+  // unless its saliency is 0 (h >= 0, so the cell's sum of h is 0 exactly when
+  // every weight in it has h = 0, and those weights add nothing to any moment).
+  const int ucell = p.cells.unsafe_cell;
+  // (read with the suffix pass's access type, which then cannot move above it)
+  const bool group_unsafe = ucell >= 0 && reinterpret_cast<const ulonglong2*>(hist)[ucell].x != 0;
+
   // ---- suffix sums over the cells (exact integer cells, rounded once to fp64):
   // the chunk totals first, then the members above this one, then a second
-  // pass that writes the suffix sums -------------------------------------------
+  // pass that writes the suffix sums.  The lane's cells are read four at a
+  // time, all four reads in flight before the first is used; an index past
+  // the lane's last cell reads that cell again and contributes nothing, and
+  // in the second pass (from the top down) its write to that cell comes
+  // before the cell's own.
   {
+    // one access type for the reads and the writes: the writes may not be
+    // moved above reads of the same cell
+    ulonglong2* mc = reinterpret_cast<ulonglong2*>(mine);
     uint64_t ih = 0, iw = 0;  // exact integer chunk totals
+#pragma unroll 1
+    for (int b = 0; b < cpl; b += 4) {
+      ulonglong2 t[4];
 #pragma unroll
-    for (int i = 0; i < CPL; i++) {
-      if (i < cpl) {
-        const ulonglong2 t = *reinterpret_cast<const ulonglong2*>(mine + 2 * i);
-        ih += t.x;
-        iw += t.y;
+      for (int c = 0; c < 4; c++) t[c] = mc[min(b + c, cpl - 1)];
+#pragma unroll
+      for (int c = 0; c < 4; c++) {
+        const bool in = b + c < cpl;
+        ih += in ? t[c].x : 0ull;
+        iw += in ? t[c].y : 0ull;
       }
     }
     double eh2 = members_excl_suffix<L>(i64_to_double(ih), j), ew2 = members_excl_suffix<L>(i64_to_double(iw), j);
+#pragma unroll 1
+    for (int b = (cpl - 1) & ~3; b >= 0; b -= 4) {
+      ulonglong2 t[4];
 #pragma unroll
-    for (int i = CPL - 1; i >= 0; i--) {
-      if (i < cpl) {
-        const ulonglong2 t = *reinterpret_cast<const ulonglong2*>(mine + 2 * i);
-        eh2 += i64_to_double(t.x);
-        ew2 += i64_to_double(t.y);
-        *reinterpret_cast<double2*>(mine + 2 * i) = make_double2(eh2, ew2);
+      for (int c = 0; c < 4; c++) t[c] = mc[min(b + c, cpl - 1)];
+#pragma unroll
+      for (int c = 3; c >= 0; c--) {
+        const bool in = b + c < cpl;
+        eh2 += in ? i64_to_double(t[c].x) : 0.0;
+        ew2 += in ? i64_to_double(t[c].y) : 0.0;
+        mc[min(b + c, cpl - 1)] = make_ulonglong2((unsigned long long)__double_as_longlong(eh2),
+                                                  (unsigned long long)__double_as_longlong(ew2));
       }
     }
   }
@@ -278,10 +304,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   mo.rel = 0x1p-47;
   mo.wabs = (double)wabs;
   int_fit_bounds<QMAX>(mo);
-
-  // A weight among merged thresholds (rare) has a cell that does not fix
-  // every clip's code: its group takes the exact path below.
-  const bool group_unsafe = M::max(unsafe ? 1.0f : 0.0f) > 0.0f;
 
   // ---- the clips this lane owns: moments from NB suffix sums ------------------
   auto moments = [&](int k, double& A0, double& A1, double& A2) {

@@ -84,10 +84,10 @@ struct IntCells {
   int n_cells;  // M + 1; 0 = use the direct kernel
   int cpl;      // cells per lane: the group's L lanes scan L * cpl >= M + 1 cells
   int cmax;     // compares per weight, 1 .. 3
-  // u in [unsafe_lo, unsafe_hi] (closed) lies among merged thresholds, where
-  // the cell does not fix every clip's code; a group with such a weight has
-  // its moments summed directly (empty interval: +inf, +inf)
-  float unsafe_lo, unsafe_hi;
+  // the cell of the u among merged thresholds, where the cell does not fix
+  // every clip's code (-1: none); a group with saliency in it has its moments
+  // summed directly
+  int unsafe_cell;
   // per bucket b = clamp(floor(128 u), -128, 127) + 128: for u in the
   // bucket the cell is base plus the number of t_base .. t_base+cmax-1 at
   // or below u

@@ -349,6 +349,35 @@ def test_weights_among_tie_thresholds():
     run_case("tie-cluster.int2.bf16", 0, 0, 0, bits=2, group=64, clips=clips, W=Wb, v=v.cuda(), w_bf16=True)
 
 
+def test_zero_saliency_among_tie_thresholds():
+    """As above, but in every other such group the weights among the tie
+    thresholds have zero saliency (v = 0 and g = 0, so v' = 0 after the EMA).
+    They add nothing to any moment, so the binned kernel keeps such a group on
+    its fast path; the groups whose tie-span weights carry saliency still take
+    the exact path.  Both must match the oracle."""
+    torch.manual_seed(12)
+    rows, cols = 24, 384
+    W = (torch.randn(rows, cols) * 0.3).float()
+    v = torch.rand(rows, cols).float() + 0.01
+    g = (torch.randn(rows, cols) * 1e-3).to(torch.bfloat16)
+    tie = -torch.linspace(3.2e-8, 1.7e-8, 62)
+    for r in range(0, rows, 2):
+        c0 = 64 * (r % 6)
+        W[r, c0] = -1.0
+        W[r, c0 + 1] = 1.0
+        W[r, c0 + 2:c0 + 64] = tie[torch.randperm(62)]
+        if (r // 2) % 2 == 0:
+            v[r, c0 + 2:c0 + 64] = 0.0
+            g[r, c0 + 2:c0 + 64] = 0.0
+    clips = tuple(synth.clip_grid(1.0, 0.5, 12))
+    for bits in (2, 3):
+        Wg, vg = _place(W, v)
+        run_case(f"tie-cluster-zero-h.int{bits}.f32", 0, 0, 0, bits=bits, group=64, clips=clips, W=Wg,
+                 v=vg.clone(), g=g.cuda(), w_bf16=False, ema=True)
+        run_case(f"tie-cluster-zero-h.int{bits}.noema", 0, 0, 0, bits=bits, group=64, clips=clips, W=Wg,
+                 v=vg.clone(), w_bf16=False)
+
+
 @pytest.mark.parametrize("fmt,bits,group", [("int", 2, 64), ("int", 3, 128), ("int", 4, 128), ("int", 4, 64),
                                              ("int_sym", 3, 128), ("int_sym", 4, 64)])
 def test_nearly_rank_deficient_groups(fmt, bits, group):
