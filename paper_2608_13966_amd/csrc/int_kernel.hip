@@ -44,8 +44,13 @@ void int_reconstruct_kernel(IntParams p) {
   constexpr float kBeta = 0.5f * (float)QMAX;
 
   // per wavefront: the moment transpose, the exact path's stage, the stage of
-  // the coalesced stores
-  constexpr int RED = 64 * KC > int_stage_bytes<false, G>() / 8 ? 64 * KC : int_stage_bytes<false, G>() / 8;
+  // the coalesced stores.  The transpose holds group slot s, clip kk, member j
+  // at s KC (L + 1) + kk (L + 1) + j: one pad word per clip row, so that the
+  // reads (a lane's clip row, L + 1 words apart from its neighbours') and the
+  // writes (a clip's row per slot) spread over all the banks
+  constexpr int ROW = L + 1;
+  constexpr int TRANS = GPW * KC * ROW;
+  constexpr int RED = TRANS > int_stage_bytes<false, G>() / 8 ? TRANS : int_stage_bytes<false, G>() / 8;
   __shared__ __align__(16) double s_red[kThreads / 64][RED];
   __shared__ float s_alpha[kMaxClips], s_clip[kMaxClips];
   __shared__ float s_win[kThreads / 64][GPW][4];
@@ -147,7 +152,7 @@ void int_reconstruct_kernel(IntParams p) {
 #pragma unroll
     for (int m = 3 - NM; m < 3; m++) {
 #pragma unroll
-      for (int kk = 0; kk < KC; kk++) red[(slot * KC + kk) * L + j] = acc[kk][m];
+      for (int kk = 0; kk < KC; kk++) red[(slot * KC + kk) * ROW + j] = acc[kk][m];
       wave_lds_fence();
 #pragma unroll
       for (int t = 0; t < OWN; t++) {
@@ -155,7 +160,7 @@ void int_reconstruct_kernel(IntParams p) {
         const int kr = kk < KC ? kk : KC - 1;
         double s = 0.0;
 #pragma unroll
-        for (int jj = 0; jj < L; jj++) s += red[(slot * KC + kr) * L + jj];
+        for (int jj = 0; jj < L; jj++) s += red[(slot * KC + kr) * ROW + jj];
         own[t][m] = s;
       }
       wave_lds_fence();
