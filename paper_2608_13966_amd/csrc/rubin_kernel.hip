@@ -445,11 +445,18 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
     bits |= q << (3 * i);
     r[i] = lutf[q];
   }
-  // 24 bits per lane at byte offset 3 lane of the block's 192-byte stream
-  uint8_t* cp = mtx.codes + bid * 192 + lane * 3;
-  cp[0] = (uint8_t)bits;
-  cp[1] = (uint8_t)(bits >> 8);
-  cp[2] = (uint8_t)(bits >> 16);
+  // 24 bits per lane at byte offset 3 lane of the block's 192-byte stream:
+  // lanes 4i .. 4i + 3 hold its dwords 3i .. 3i + 2, which lanes 4i, 4i + 1 and
+  // 4i + 2 store whole, each with its upper neighbour's bits (row_shl:1:
+  // lane l reads lane l + 1 of its row of 16; lane 4i + 3 stores nothing)
+  {
+    const uint32_t up = dpp_u32<0x101>(bits);
+    const int part = lane & 3;
+    if (part < 3) {
+      const uint32_t d = (bits >> (8 * part)) | (up << (24 - 8 * part));
+      *reinterpret_cast<uint32_t*>(mtx.codes + bid * 192 + (lane >> 2) * 12 + part * 4) = d;
+    }
+  }
   if (mtx.r) {
     if constexpr (W_BF16) {
       st128(reinterpret_cast<uint16_t*>(mtx.r) + e0,
