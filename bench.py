@@ -168,7 +168,7 @@ def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=int(os.environ.get("WORLD_SIZE", "1")))
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5", "c6", "c7", "c8", "c9"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
@@ -520,8 +520,12 @@ def main(argv=None):
                 # average kernel duration, the frac it gives, and the bench
                 # line taken in the same session without the profiler
                 pw = ent["rocprof_weights_per_launch"]
+                p_wps = pw / (ent["rocprof_avg_us"] * 1e-6)  # weights/s inside the kernel, from the trace
+                p_hbm = pw * kbpw / (ent["rocprof_avg_us"] * 1e-6) / 1e9 / PEAK_HBM_GBPS
                 prof = {"rocprof_avg_us": ent["rocprof_avg_us"],
-                        "frac": round(pw * kbpw / (ent["rocprof_avg_us"] * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4),
+                        # the same roof as the line's frac (set below), from the trace's duration
+                        "frac": round(ops_w * p_wps / 1e12 / PEAK_VALU_TOPS if t_alu > t_hbm else p_hbm, 4),
+                        "hbm_frac": round(p_hbm, 4),
                         "same_session_bench_avg_launch_us": ent.get("bench_avg_launch_us"),
                         "trace_overhead": ent.get("trace_overhead"),
                         "valu_lane_ops_per_weight_measured": ent.get("valu_lane_ops_per_weight"),
