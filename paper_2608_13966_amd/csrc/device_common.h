@@ -17,6 +17,12 @@ __device__ __forceinline__ float uniform_f32(float x) {
   return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(x)));
 }
 
+// The wavefront's index in its workgroup, in a scalar register: the compiler
+// does not see that threadIdx.x / 64 is the same in every lane, and would
+// otherwise do the arithmetic derived from it (addresses, a block index
+// division) per lane.
+__device__ __forceinline__ int wave_index() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }
+
 // The bucket of u among 256 equal slices of [-1, 1]: clamp(floor(u * 128),
 // -128, 127) + 128 (u * 128 is exact, so a boundary falls exactly at u = 0);
 // any u, NaN included, gives an index in [0, 256).

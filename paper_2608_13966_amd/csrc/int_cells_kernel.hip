@@ -120,7 +120,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
 
   using M = Members<L, kSpread>;
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63, wave = wave_index();
   const int j = M::member(lane), slot = M::slot(lane);
   const int K = p.n_clips;
 

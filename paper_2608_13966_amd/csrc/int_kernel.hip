@@ -56,7 +56,7 @@ void int_reconstruct_kernel(IntParams p) {
   __shared__ float s_win[kThreads / 64][GPW][4];
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63, wave = wave_index();
   const int j = lane % L, slot = lane / L;
   const int K = p.n_clips;
 

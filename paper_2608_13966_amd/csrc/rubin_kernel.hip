@@ -32,7 +32,8 @@
 // codebook entry's sums (differences of exact prefix sums) carry a single
 // rounding.  Only a saliency below 2^-101 of the block's largest is lost; a
 // codebook entry whose weights all have such a saliency is recomputed
-// directly in fp64 (it is detected from a per-cell flag of positive h).
+// directly in fp64 (it is detected from a per-cell flag, set by a weight with
+// h > 0 whose limbs are both 0).
 //
 // Work decomposition: one wavefront per block, lane l holding row l/8 of the
 // block and its 8 consecutive columns 8 (l % 8) .. 8 (l % 8) + 7.  The
@@ -101,14 +102,17 @@ __device__ __forceinline__ void scan_step(int64_t (&x)[4], int& xf) {
 
 // BK: the bucket form of the cells (RubinParams::buckets), else the tree form.
 template <bool W_BF16, int EMA, bool BK>
-__global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams p) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(5))) void rubin_reconstruct_kernel(RubinParams p) {
   static_assert(kThreads == kCellBuckets, "one bucket entry per thread");
   // per cell: h = hh + hl 2^-50 and h w = wh + wl 2^-50 in scaled units (one
   // array per limb, so that lanes on different cells spread over the banks),
-  // then their exclusive prefix sums; a flag for an h > 0, then its prefix count
-  // rows of kCells + 2 entries keep every row 16-byte aligned for the
-  // two-cell (128-bit) accesses of the scan
-  __shared__ int64_t s_limb[kWaves][2][4][kCells + 2];
+  // then their exclusive prefix sums; a flag for an h > 0 lost to the fixed
+  // point, then its prefix count.  Rows of kCells + 2 entries keep every row
+  // 16-byte aligned for the two-cell (128-bit) accesses of the scan.  One copy
+  // of the cells per wavefront: at 23 KB per workgroup five wavefronts per
+  // SIMD fit (a second copy for the odd lanes, which halves the atomics that
+  // meet on one address, measured slower once it set the occupancy)
+  __shared__ int64_t s_limb[kWaves][4][kCells + 2];
   __shared__ int s_flag[kWaves][kCells + 2];
   __shared__ float s_thr[BK ? 1 : kCells];        // tree form: thresholds in search-tree order
   __shared__ uint4 s_bucket[BK ? kCellBuckets : 1];  // bucket form: first cell, next three thresholds
@@ -118,7 +122,7 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
   __shared__ float s_alpha[kMaxClips], s_clip[kMaxClips];
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63, wave = wave_index();
   const int K = p.n_clips;
   if (tid < kMaxClips) {
     s_alpha[tid] = p.alpha[tid];
@@ -254,14 +258,10 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
     const int sh_exp = kHiBits - eh, sw_exp = kHiBits - eh - ew;
 
     // ---- cells: clear, then add every weight's limbs into its cell ------------
-    // two copies of the cell sums (even / odd lanes) halve the atomics that
-    // meet on one address; the prefix sums go to copy 0
-    int64_t(*limb)[kCells + 2] = s_limb[wave][0];
-    int64_t(*limb1)[kCells + 2] = s_limb[wave][1];
-    int64_t(*mine)[kCells + 2] = s_limb[wave][lane & 1];
+    int64_t(*limb)[kCells + 2] = s_limb[wave];
     int* flag = s_flag[wave];
 #pragma unroll
-    for (int j = 0; j < 4; j++) *cell_pair(limb[j], lane) = *cell_pair(limb1[j], lane) = ll2{0, 0};
+    for (int j = 0; j < 4; j++) *cell_pair(limb[j], lane) = ll2{0, 0};
     *reinterpret_cast<int2*>(flag + 2 * lane) = make_int2(0, 0);
     wave_lds_fence();
     // the cell of every weight: the number of thresholds <= u
@@ -321,8 +321,8 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
       split_limbs(__builtin_ldexp(HW[i], sw_exp), x[2], x[3]);
 #pragma unroll
       for (int j = 0; j < 4; j++)
-        atomicAdd(reinterpret_cast<unsigned long long*>(&mine[j][pos[i]]), (unsigned long long)x[j]);
-      if (v[i] > 0.0f) flag[pos[i]] = 1;
+        atomicAdd(reinterpret_cast<unsigned long long*>(&limb[j][pos[i]]), (unsigned long long)x[j]);
+      if (v[i] > 0.0f && x[0] == 0 && x[1] == 0) flag[pos[i]] = 1;  // rare: h below the fixed point
     }
     wave_lds_fence();
 
@@ -331,9 +331,9 @@ __global__ __launch_bounds__(kThreads) void rubin_reconstruct_kernel(RubinParams
       int64_t a[4], x[4], t[4];
 #pragma unroll
       for (int j = 0; j < 4; j++) {
-        const ll2 c0 = *cell_pair(limb[j], lane), c1 = *cell_pair(limb1[j], lane);
-        a[j] = c0.x + c1.x;
-        x[j] = t[j] = a[j] + c0.y + c1.y;
+        const ll2 c0 = *cell_pair(limb[j], lane);
+        a[j] = c0.x;
+        x[j] = t[j] = a[j] + c0.y;
       }
       const int2 fl = *reinterpret_cast<const int2*>(flag + 2 * lane);
       const int fa = fl.x;
