@@ -529,6 +529,9 @@ def main(argv=None):
                         "same_session_bench_avg_launch_us": ent.get("bench_avg_launch_us"),
                         "trace_overhead": ent.get("trace_overhead"),
                         "valu_lane_ops_per_weight_measured": ent.get("valu_lane_ops_per_weight"),
+                        # the VALU load by the issued count (SQ_INSTS_VALU), at this line's kernel rate
+                        "valu_frac_measured": (round(ent["valu_lane_ops_per_weight"] * k_wps / 1e12 / PEAK_VALU_TOPS, 4)
+                                               if ent.get("valu_lane_ops_per_weight") else None),
                         "file": f"profiles/{ent['kernel']}_{args.workload}_kernel_stats.txt"}
     except (OSError, ValueError, KeyError):
         pass
