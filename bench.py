@@ -419,8 +419,8 @@ def main(argv=None):
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
-        # the CPUs this process may use, at most 16 (a one-GPU machine's share of
-        # its host: worker pools there are sized to 16 whatever the host has)
+        # the CPUs this process may use, at most 16 (the host share of one
+        # GPU: worker pools are sized to 16 whatever the host has)
         allowed = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
         threads = max(1, min(16, allowed))
 

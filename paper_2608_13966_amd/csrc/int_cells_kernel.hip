@@ -345,7 +345,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   int bk = -1;
   double bn = 0.0, bd = 1.0;
   if (!full && !group_unsafe) {
-#pragma unroll 1
+    // unrolled: the clips' LDS reads and fp64 chains interleave
+#pragma unroll
     for (int t = 0; t < OWN; t++) {
       const int k = j + L * t;
       if (k < K) {
