@@ -356,8 +356,7 @@ __device__ __forceinline__ float chunk_absmax(uint4 t) {
 // One workgroup per span of kAbsChunks 16-byte chunks of one matrix: lane t
 // loads chunks t, t + 256, ... (each load instruction reads 1 KB contiguous per
 // wavefront), kAbsBatch loads in flight at a time; then a DPP / LDS maximum
-// and one atomicMax on the fp32 bit pattern per workgroup (a larger span means
-// fewer workgroups meeting on one address).
+// and at most one atomicMax on the fp32 bit pattern per workgroup.
 constexpr int64_t kAbsChunks = (int64_t)kThreads * kAbsSpan;
 
 template <bool W_BF16>
@@ -397,8 +396,11 @@ __global__ __launch_bounds__(kThreads) void absmax_kernel(AbsmaxTable t) {
     float x = s_m[0];
 #pragma unroll
     for (int i = 1; i < kThreads / 64; i++) x = fmaxf(x, s_m[i]);
-    // |w| >= 0: the fp32 bit patterns order like unsigned integers
-    atomicMax(kt->out[mi], __float_as_uint(x));
+    // |w| >= 0: the fp32 bit patterns order like unsigned integers.  The
+    // stored maximum only grows, so a workgroup whose maximum does not exceed
+    // the value it reads skips its atomic (most do: the atomics on one
+    // address otherwise serialise)
+    if (__float_as_uint(x) > __builtin_nontemporal_load(kt->out[mi])) atomicMax(kt->out[mi], __float_as_uint(x));
   }
 }
 

@@ -236,8 +236,8 @@ struct AbsmaxTable {
 };
 // 16-byte chunks one lane of the absmax kernel loads, and the workgroups it
 // needs for a matrix of n_chunks chunks
-constexpr int kAbsSpan = 32;   // 16-byte chunks per thread of the absmax pass
-constexpr int kAbsBatch = 32;  // of which in flight at a time (all: 93 us for the Llama set, against 96-101 for other splits)
+constexpr int kAbsSpan = 16;   // 16-byte chunks per thread of the absmax pass
+constexpr int kAbsBatch = 16;  // of which in flight at a time (all)
 constexpr int64_t absmax_blocks(int64_t n_chunks) {
   return (n_chunks + (int64_t)kThreads * kAbsSpan - 1) / ((int64_t)kThreads * kAbsSpan);
 }
