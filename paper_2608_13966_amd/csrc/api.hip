@@ -245,6 +245,55 @@ void eytzinger_fill(float* tree, const float* sorted, int& next, int node) {
 
 int cell_bucket(float u);
 
+// Extra cell boundaries for the Rubin kernel.  A boundary that is no clip's
+// threshold leaves every code constant on both of its sides, so no result
+// changes; what changes is how many of a block's weights share a cell, and
+// the lanes of one 64-bit LDS atomic that land on one cell serialise.  Every
+// clip's middle threshold lies at u = 0 and its next ones at +-f/3.5 or
+// further, so on a grid of clips down to f = 0.3 the two cells beside 0 hold
+// about a tenth of a bell-shaped block each.  Each cell is weighted by the
+// share an N(0, 0.3^2) model of u puts in it (u = (w - c) / rho, with rho
+// about three standard deviations for a bell-shaped block of 512), and the
+// heaviest cell is halved until none holds more than 1.2% or the cells run
+// out.  A split never falls inside [ulo, uhi] (the merged tie span); when
+// `cnt` (thresholds per bucket, the bucket form) is given, it never takes a
+// bucket above `cmax` thresholds.  Inserts into the sorted s[0 .. m) and
+// returns the new m (at most m_max).
+int rubin_split_cells(float* s, int m, int m_max, int* cnt, int cmax, float ulo, float uhi) {
+  constexpr double kSigma = 0.3, kTarget = 0.012;
+  auto cdf = [&](double x) { return 0.5 * std::erfc(-x / (kSigma * std::sqrt(2.0))); };
+  bool frozen[quasar::kRubinThresholds + 1] = {};  // cells found not to split
+  while (m < m_max) {
+    int best = -1;
+    double best_mass = kTarget;
+    for (int i = 0; i <= m; i++) {  // cell i = [s[i - 1], s[i]), the ends taken at -1 and 1
+      const double a = i == 0 ? -1.0 : s[i - 1], b = i == m ? 1.0 : s[i];
+      if (frozen[i] || !(b > a)) continue;
+      const double mass = cdf(b) - cdf(a);
+      if (mass > best_mass) {
+        best_mass = mass;
+        best = i;
+      }
+    }
+    if (best < 0) break;
+    const float a = best == 0 ? -1.0f : s[best - 1], b = best == m ? 1.0f : s[best];
+    const float mid = 0.5f * (a + b);
+    bool ok = mid > a && mid < b && !(mid >= ulo && mid <= uhi);
+    if (ok && cnt != nullptr) ok = cnt[cell_bucket(mid)] < cmax;
+    if (!ok) {
+      frozen[best] = true;
+      continue;
+    }
+    if (cnt != nullptr) cnt[cell_bucket(mid)]++;
+    for (int j = m; j > best; j--) s[j] = s[j - 1];
+    s[best] = mid;
+    for (int j = m + 1; j > best + 1; j--) frozen[j] = frozen[j - 1];
+    frozen[best] = frozen[best + 1] = false;
+    m++;
+  }
+  return m;
+}
+
 // The bucket form of the Rubin kernel's cells from the thresholds t[7 k + b]
 // = T(k, b) (see RubinParams): the tie-cluster thresholds T(k, 3) are merged
 // into one at their least value, and every other bucket may hold at most
@@ -273,13 +322,20 @@ bool rubin_buckets(quasar::RubinParams& p, const float* t, int K) {
   int cnt[quasar::kCellBuckets] = {0};
   int cmax = 1, below = 0;
   for (int i = 0; i < m; i++) cnt[cell_bucket(srt[i])]++;
+  for (int b = 0; b < quasar::kCellBuckets; b++) cmax = std::max(cmax, cnt[b]);
+  if (cmax > 3) return false;
+  cmax = std::max(cmax, 2);
+  // a bucket whose first cell is c reads thr[c .. c + 2], so the list keeps
+  // two NaN entries of padding after its last threshold (c <= m)
+  m = rubin_split_cells(srt, m, quasar::kRubinThresholds - 3, cnt, cmax, merge ? ulo : INFINITY,
+                        merge ? uhi : INFINITY);
+  cmax = 1;
   uint8_t base[quasar::kCellBuckets];
   for (int b = 0; b < quasar::kCellBuckets; b++) {
     cmax = std::max(cmax, cnt[b]);
     base[b] = (uint8_t)below;
     below += cnt[b];
   }
-  if (cmax > 3) return false;
   for (int k = 0; k < quasar::kMaxClips; k++) {
     for (int b = 0; b < 9; b++) {
       int c = 0;
@@ -333,23 +389,28 @@ void rubin_thresholds(quasar::RubinParams& p, int K) {
       t[n++] = f32_from_order_key(hi);
     }
   }
+  if (rubin_buckets(p, t, K)) return;
+  // the tree form: every threshold (repeats included) plus the extra
+  // boundaries; a weight's cell is the number of them at or below u
+  float all[quasar::kRubinThresholds];
+  std::copy(t, t + n, all);
+  std::sort(all, all + n);
+  const int na = rubin_split_cells(all, n, quasar::kRubinThresholds - 1, nullptr, 0, INFINITY, INFINITY);
   for (int k = 0; k < quasar::kMaxClips; k++) {
     for (int b = 0; b < 9; b++) {
       int cnt = 0;
       if (k < K && b >= 1 && b <= 7) {
         const float tb = t[7 * k + b - 1];
-        for (int i = 0; i < n; i++) cnt += t[i] <= tb;
+        for (int i = 0; i < na; i++) cnt += all[i] <= tb;
       } else if (k < K && b == 8) {
-        cnt = n + 1;
+        cnt = na + 1;
       }
       p.tpos[k][b] = (uint8_t)cnt;
     }
   }
-  if (rubin_buckets(p, t, K)) return;
-  std::sort(t, t + n);
   // in-order walk of the complete tree with nodes 1 .. 127 = the sorted list
   float sorted[quasar::kRubinThresholds - 1];
-  for (int i = 0; i < quasar::kRubinThresholds - 1; i++) sorted[i] = i < n ? t[i] : INFINITY;
+  for (int i = 0; i < quasar::kRubinThresholds - 1; i++) sorted[i] = i < na ? all[i] : INFINITY;
   int next = 0;
   eytzinger_fill(p.thr, sorted, next, 1);
   p.thr[0] = INFINITY;

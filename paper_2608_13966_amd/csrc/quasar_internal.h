@@ -192,17 +192,20 @@ struct RubinParams {
   float alpha[kMaxClips];  // 7 / (2 f_k)
   float clip[kMaxClips];
   // T(k, b) = the least fp32 u with code >= b + 1 under clip k, for all k < K
-  // and b < 7: sorted, padded with +inf to 127 entries and stored as an
-  // implicit search tree (thr[1] the root, node n's children at 2n and 2n + 1;
-  // thr[0] unused); tpos[k][b] = the number of them at or below T(k, b - 1)
-  // (0 for b = 0, 7K + 1 for b = 8)
+  // and b < 7, plus extra cell boundaries that are no clip's threshold (they
+  // split the cells that hold most of a block; at most 127 in all): sorted,
+  // padded with +inf to 127 entries and stored as an implicit search tree
+  // (thr[1] the root, node n's children at 2n and 2n + 1; thr[0] unused);
+  // tpos[k][b] = the number of them at or below T(k, b - 1) (0 for b = 0, the
+  // count of all plus 1 for b = 8)
   float thr[kRubinThresholds];
   uint8_t tpos[kMaxClips][9];
   // Bucket form (buckets = 1), taken when the clip grid allows it: the
   // tie-cluster thresholds T(k, 3) (all in (-2^-20, 0), where the fp32 code
   // rounding ties at 3.5) are merged into one at their least value, thr holds
-  // the m distinct merged thresholds sorted (NaN padding) and tpos indexes
-  // them (tpos[k][8] = m + 1); base[bkt] = the number of them below bucket bkt
+  // the m distinct merged thresholds and extra boundaries sorted (m <= 125,
+  // then NaN padding, which a bucket's three compares may read) and tpos
+  // indexes them (tpos[k][8] = m + 1); base[bkt] = the number of them below bucket bkt
   // of the binned INT kernel's bucketing, each bucket holding at most cmax.
   // A weight in [unsafe_lo, unsafe_hi] (between tie thresholds) makes the
   // kernel sum its block's code-3 and code-4 entries directly.

@@ -12,7 +12,10 @@
 // Every code is a non-decreasing function of u, so the codes a weight gets
 // under all K clips are fixed by how many of the 7K per-clip thresholds
 // T(k, b) = min{u : q_k(u) >= b + 1} lie at or below u.  That count -- the
-// weight's cell, 0 .. 7K -- is what the kernel bins by, once per block, and
+// weight's cell, 0 .. 7K -- is what the kernel bins by, once per block (the
+// host adds boundaries that are no threshold, splitting the cells that hold
+// most of a block: the lanes of one LDS atomic that meet on a cell
+// serialise, and no code changes inside a cell either way), and
 // for clip k the weights with code b are exactly the cells in a fixed range
 // [tpos(k, b), tpos(k, b + 1)).  The per-clip work then reads two prefix sums
 // per codebook entry instead of re-binning 512 weights.  The thresholds are
@@ -49,7 +52,7 @@ namespace {
 
 constexpr int NE = 8;          // weights per lane
 constexpr int kWaves = kThreads / 64;
-constexpr int kCells = kRubinThresholds;  // cell ids 0 .. 7K <= 112 < 128 (fewer in the bucket form)
+constexpr int kCells = kRubinThresholds;  // cell ids 0 .. (boundaries) <= 127 < 128
 constexpr int kHiBits = 51;    // |scaled value| < 2^51: its nearest integer is the high limb
 constexpr int kLoBits = 50;    // the remainder, scaled by 2^50 and rounded, is the low limb
 constexpr double kMagic = 6755399441055744.0;  // 1.5 * 2^52: x + kMagic rounds x to an integer
