@@ -67,17 +67,20 @@ __device__ __forceinline__ uint32_t e4m3_byte(float x) {
 }
 __device__ __forceinline__ float e4m3_value(uint32_t e) { return __builtin_amdgcn_cvt_f32_fp8((int)e, 0); }
 
-// x (|x| < 2^51) as hi + lo 2^-50 with integer limbs: hi = rint(x), lo =
-// rint((x - hi) 2^50).  For |y| < 2^51, y + 1.5 2^52 lands where the fp64
-// spacing is 1, so its bit pattern minus that of 1.5 2^52 is rint(y) as a
-// two's-complement integer; x - hi and the scaling by 2^50 are exact.
-__device__ __forceinline__ void split_limbs(double x, int64_t& hi, int64_t& lo) {
+// x = a s (s a power of two, |x| < 2^51; the product is exact) as hi + lo
+// 2^-50 with integer limbs: hi = rint(x), lo = rint((x - hi) 2^50).  For
+// |y| < 2^51, y + 1.5 2^52 lands where the fp64 spacing is 1, so its bit
+// pattern minus that of 1.5 2^52 is rint(y) as a two's-complement integer;
+// each fma rounds an exact value once (a s + 1.5 2^52, then x - hi, which is
+// representable, then (x - hi) 2^50 + 1.5 2^52).
+__device__ __forceinline__ void split_limbs(double a, double s, int64_t& hi, int64_t& lo) {
   const int64_t mb = __double_as_longlong(kMagic);
-  const double t = x + kMagic;
+  const double t = __builtin_fma(a, s, kMagic);
   hi = __double_as_longlong(t) - mb;
-  const double r = __builtin_ldexp(x - (t - kMagic), kLoBits);
-  lo = __double_as_longlong(r + kMagic) - mb;
+  const double r = __builtin_fma(a, s, -(t - kMagic));
+  lo = __double_as_longlong(__builtin_fma(r, 0x1p50, kMagic)) - mb;
 }
+static_assert(kLoBits == 50, "split_limbs scales the remainder by 2^50");
 // hi + lo 2^-50 in fp64 (the limb sums stay below 2^60 in magnitude)
 __device__ __forceinline__ double join_limbs(int64_t hi, int64_t lo) {
   return __builtin_ldexp((double)lo, -kLoBits) + (double)hi;
@@ -88,19 +91,22 @@ typedef long long ll2 __attribute__((ext_vector_type(2)));
 // cells 2 l and 2 l + 1 of a cell row as one 16-byte LDS access
 __device__ __forceinline__ ll2* cell_pair(int64_t* row, int l) { return reinterpret_cast<ll2*>(row + 2 * l); }
 
-// One step of a wavefront-wide inclusive scan of four int64 and one int:
-// every lane adds the values DPP control CTRL brings it (lanes of rows outside
-// ROW_MASK, and lanes without a source, add 0).  Integer addition: exact.
+// x of the lane SHIFT places lower in the same row of 16 lanes, 0 for the
+// first SHIFT lanes of a row (row_shr with bound_ctrl)
+template <int SHIFT>
+__device__ __forceinline__ int64_t row_shr64(int64_t x) {
+  const uint64_t u = (uint64_t)x;
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)u, 0x110 + SHIFT, 0xf, 0xf, true);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)(u >> 32), 0x110 + SHIFT, 0xf, 0xf, true);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// One step of a wavefront-wide inclusive scan of an int: every lane adds the
+// value DPP control CTRL brings it (lanes of rows outside ROW_MASK, and lanes
+// without a source, add 0).
 template <int CTRL, int ROW_MASK>
-__device__ __forceinline__ void scan_step(int64_t (&x)[4], int& xf) {
-#pragma unroll
-  for (int j = 0; j < 4; j++) {
-    const uint64_t u = (uint64_t)x[j];
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)u, CTRL, ROW_MASK, 0xf, false);
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(u >> 32), CTRL, ROW_MASK, 0xf, false);
-    x[j] += (int64_t)(((uint64_t)hi << 32) | lo);
-  }
-  xf += __builtin_amdgcn_update_dpp(0, xf, CTRL, ROW_MASK, 0xf, false);
+__device__ __forceinline__ void scan_step(int& x) {
+  x += __builtin_amdgcn_update_dpp(0, x, CTRL, ROW_MASK, 0xf, false);
 }
 
 // BK: the bucket form of the cells (RubinParams::buckets), else the tree form.
@@ -115,7 +121,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(5))) v
   // of the cells per wavefront: at 23 KB per workgroup five wavefronts per
   // SIMD fit (a second copy for the odd lanes, which halves the atomics that
   // meet on one address, measured slower once it set the occupancy)
-  __shared__ int64_t s_limb[kWaves][4][kCells + 2];
+  __shared__ __align__(16) int64_t s_limb[kWaves][4][kCells + 2];
   __shared__ int s_flag[kWaves][kCells + 2];
   __shared__ float s_thr[BK ? 1 : kCells];        // tree form: thresholds in search-tree order
   __shared__ uint4 s_bucket[BK ? kCellBuckets : 1];  // bucket form: first cell, next three thresholds
@@ -317,47 +323,63 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(5))) v
     // a weight between tie thresholds: the block's code-3 and code-4 entries
     // are summed directly below
     const bool block_unsafe = __ballot(unsafe) != 0;  // uniform
+    const double s_h = __builtin_ldexp(1.0, sh_exp), s_hw = __builtin_ldexp(1.0, sw_exp);
+    bool lost = false;
 #pragma unroll
     for (int i = 0; i < NE; i++) {
       int64_t x[4];
-      split_limbs(__builtin_ldexp(H[i], sh_exp), x[0], x[1]);
-      split_limbs(__builtin_ldexp(HW[i], sw_exp), x[2], x[3]);
+      split_limbs(H[i], s_h, x[0], x[1]);
+      split_limbs(HW[i], s_hw, x[2], x[3]);
 #pragma unroll
       for (int j = 0; j < 4; j++)
         atomicAdd(reinterpret_cast<unsigned long long*>(&limb[j][pos[i]]), (unsigned long long)x[j]);
-      if (v[i] > 0.0f && x[0] == 0 && x[1] == 0) flag[pos[i]] = 1;  // rare: h below the fixed point
+      if (v[i] > 0.0f && x[0] == 0 && x[1] == 0) {  // rare: h below the fixed point
+        flag[pos[i]] = 1;
+        lost = true;
+      }
     }
+    const bool block_lost = __ballot(lost) != 0;  // uniform
     wave_lds_fence();
 
-    // ---- exclusive prefix sums over the cells (lane l: cells 2l, 2l + 1) ------
+    // ---- exclusive prefix sums over the cells: lane 16 j + c takes cells
+    // 8 c .. 8 c + 7 of limb j and sums them in order, and the lane totals are
+    // scanned across the lane's row of 16 (one row per limb).  Integer
+    // addition: exact. -------------------------------------------------------
     {
-      int64_t a[4], x[4], t[4];
+      static_assert(kCells == 4 * 16 * 8 / 4, "16 lanes x 8 cells cover one limb");
+      const int j = lane >> 4, c = lane & 15;
+      ll2* seg = reinterpret_cast<ll2*>(&limb[j][8 * c]);
+      ll2 a[4];
 #pragma unroll
-      for (int j = 0; j < 4; j++) {
-        const ll2 c0 = *cell_pair(limb[j], lane);
-        a[j] = c0.x;
-        x[j] = t[j] = a[j] + c0.y;
-      }
+      for (int t = 0; t < 4; t++) a[t] = seg[t];
+      int64_t in[8];  // inclusive sums within the segment
+      in[0] = a[0].x;
+#pragma unroll
+      for (int t = 1; t < 8; t++) in[t] = in[t - 1] + ((t & 1) ? a[t >> 1].y : a[t >> 1].x);
+      int64_t x = in[7];
+      x += row_shr64<1>(x);
+      x += row_shr64<2>(x);
+      x += row_shr64<4>(x);
+      x += row_shr64<8>(x);
+      const int64_t e = x - in[7];  // the cells before the segment
+      seg[0] = ll2{e, e + in[0]};
+#pragma unroll
+      for (int t = 1; t < 4; t++) seg[t] = ll2{e + in[2 * t - 1], e + in[2 * t]};
+      if (c == 15) limb[j][kCells] = x;
+    }
+    if (block_lost) {  // uniform; rare: prefix counts of the flags (lane l: cells 2l, 2l + 1)
       const int2 fl = *reinterpret_cast<const int2*>(flag + 2 * lane);
-      const int fa = fl.x;
-      int xf = fa + fl.y;
-      const int tf = xf;
-      // inclusive scan of the lane totals over the wavefront
-      scan_step<0x111, 0xf>(x, xf);  // row_shr:1
-      scan_step<0x112, 0xf>(x, xf);  // row_shr:2
-      scan_step<0x114, 0xf>(x, xf);  // row_shr:4
-      scan_step<0x118, 0xf>(x, xf);  // row_shr:8: each row of 16 is scanned
-      scan_step<0x142, 0xa>(x, xf);  // row_bcast:15 into rows 1 and 3
-      scan_step<0x143, 0xc>(x, xf);  // row_bcast:31 into rows 2 and 3
-#pragma unroll
-      for (int j = 0; j < 4; j++) {
-        const int64_t e = x[j] - t[j];
-        *cell_pair(limb[j], lane) = ll2{e, e + a[j]};
-        if (lane == 63) limb[j][kCells] = x[j];
-      }
-      const int ef = xf - tf;
-      *reinterpret_cast<int2*>(flag + 2 * lane) = make_int2(ef, ef + fa);
-      if (lane == 63) flag[kCells] = xf;
+      int x = fl.x + fl.y;
+      const int t = x;
+      scan_step<0x111, 0xf>(x);  // row_shr:1
+      scan_step<0x112, 0xf>(x);  // row_shr:2
+      scan_step<0x114, 0xf>(x);  // row_shr:4
+      scan_step<0x118, 0xf>(x);  // row_shr:8: each row of 16 is scanned
+      scan_step<0x142, 0xa>(x);  // row_bcast:15 into rows 1 and 3
+      scan_step<0x143, 0xc>(x);  // row_bcast:31 into rows 2 and 3
+      const int e = x - t;
+      *reinterpret_cast<int2*>(flag + 2 * lane) = make_int2(e, e + fl.x);
+      if (lane == 63) flag[kCells] = x;
     }
     wave_lds_fence();
 
@@ -368,7 +390,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(5))) v
       const bool live = k < K;
       const int kc = live ? k : 0;
       const int t0 = s_tpos[kc][b], t1 = s_tpos[kc][b + 1];
-      const int cnt = flag[t1] - flag[t0];
+      const int cnt = block_lost ? flag[t1] - flag[t0] : 0;
       double hb = __builtin_ldexp(join_limbs(limb[0][t1] - limb[0][t0], limb[1][t1] - limb[1][t0]), -sh_exp);
       double hwb = __builtin_ldexp(join_limbs(limb[2][t1] - limb[2][t0], limb[3][t1] - limb[3][t0]), -sw_exp);
       // entries whose saliency fell below the fixed-point range, and in a
