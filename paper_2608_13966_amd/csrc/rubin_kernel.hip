@@ -26,17 +26,23 @@
 // directly) or by descending an implicit binary search tree over all of them
 // (node n's children at 2n and 2n + 1; any clip grid).
 //
-// The cell sums of h and h w are kept exact, as integers: each value is
-// scaled by a power of two fixed per block (from the block's largest h and
-// |w|) and split into two integer limbs (its nearest integer below 2^51 and
-// the rounded remainder in units of 2^-50), and the limbs are added with
-// 64-bit LDS atomics.  Integer addition is exact and order-independent, so the
-// sums -- and everything computed from them -- are deterministic, and a
-// codebook entry's sums (differences of exact prefix sums) carry a single
-// rounding.  Only a saliency below 2^-101 of the block's largest is lost; a
-// codebook entry whose weights all have such a saliency is recomputed
-// directly in fp64 (it is detected from a per-cell flag, set by a weight with
-// h > 0 whose limbs are both 0).
+// The cell sums of h and h w are kept as integers.  Each value is scaled by a
+// power of two fixed per block (from the block's largest h and |w|), to x
+// with |x| < 2^51, and split into hi = rint(x) - 1 and lo = trunc((x -
+// rint(x) + 1) 2^21), in [2^20, 3 2^20]: x = hi + lo 2^-21 whenever x is a
+// multiple of 2^-21, else lo falls short by less than one unit.  Three 64-bit
+// LDS atomics per weight add the high limbs of h and of h w and both low
+// limbs, packed into the halves of one word (the sums of a half over a block
+// stay below 2^31, so no carry crosses).  Integer addition is exact and
+// order-independent, so the sums -- and everything computed from them -- are
+// deterministic.  A codebook entry's sums are differences of two prefix sums,
+// exact when every scaled value of the block is a multiple of 2^-21 (for h:
+// when no saliency lies below 2^-49 of the block's largest) and within 2^-12
+// units otherwise.  An entry whose h sum is below 2^18 units (about 2^-33 of
+// the block's largest h) is recomputed directly in fp64, so every other
+// entry's h sum is within 2^-30 relative; so is one whose weights all have a
+// saliency that the fixed point lost to 0 (found from a per-cell flag, set by a
+// weight with h > 0 whose value is 0).
 //
 // Work decomposition: one wavefront per block, lane l holding row l/8 of the
 // block and its 8 consecutive columns 8 (l % 8) .. 8 (l % 8) + 7.  The
@@ -54,7 +60,7 @@ constexpr int NE = 8;          // weights per lane
 constexpr int kWaves = kThreads / 64;
 constexpr int kCells = kRubinThresholds;  // cell ids 0 .. (boundaries) <= 127 < 128
 constexpr int kHiBits = 51;    // |scaled value| < 2^51: its nearest integer is the high limb
-constexpr int kLoBits = 50;    // the remainder, scaled by 2^50 and rounded, is the low limb
+constexpr int kLoBits = 21;    // the low limb counts units of 2^-21
 constexpr double kMagic = 6755399441055744.0;  // 1.5 * 2^52: x + kMagic rounds x to an integer
 
 
@@ -68,22 +74,24 @@ __device__ __forceinline__ uint32_t e4m3_byte(float x) {
 __device__ __forceinline__ float e4m3_value(uint32_t e) { return __builtin_amdgcn_cvt_f32_fp8((int)e, 0); }
 
 // x = a s (s a power of two, |x| < 2^51; the product is exact) as hi + lo
-// 2^-50 with integer limbs: hi = rint(x), lo = rint((x - hi) 2^50).  For
-// |y| < 2^51, y + 1.5 2^52 lands where the fp64 spacing is 1, so its bit
-// pattern minus that of 1.5 2^52 is rint(y) as a two's-complement integer;
-// each fma rounds an exact value once (a s + 1.5 2^52, then x - hi, which is
-// representable, then (x - hi) 2^50 + 1.5 2^52).
-__device__ __forceinline__ void split_limbs(double a, double s, int64_t& hi, int64_t& lo) {
+// 2^-21 with hi = rint(x) - 1 and lo = trunc((r + 1) 2^21), r = x - rint(x)
+// in [-1/2, 1/2], so lo lies in [2^20, 3 2^20].  For |y| < 2^51, y + 1.5 2^52
+// lands where the fp64 spacing is 1, so its bit pattern minus that of 1.5
+// 2^52 is rint(y) as a two's-complement integer; r is exact (an fma of the
+// exact product), and (r + 1) 2^21 is rounded once, at a spacing of 2^-31.
+__device__ __forceinline__ void split_limbs(double a, double s, int64_t& hi, uint32_t& lo) {
   const int64_t mb = __double_as_longlong(kMagic);
   const double t = __builtin_fma(a, s, kMagic);
-  hi = __double_as_longlong(t) - mb;
+  hi = __double_as_longlong(t) - (mb + 1);
   const double r = __builtin_fma(a, s, -(t - kMagic));
-  lo = __double_as_longlong(__builtin_fma(r, 0x1p50, kMagic)) - mb;
+  lo = (uint32_t)__builtin_fma(r, 0x1p21, 0x1p21);  // truncates toward zero
 }
-static_assert(kLoBits == 50, "split_limbs scales the remainder by 2^50");
-// hi + lo 2^-50 in fp64 (the limb sums stay below 2^60 in magnitude)
-__device__ __forceinline__ double join_limbs(int64_t hi, int64_t lo) {
-  return __builtin_ldexp((double)lo, -kLoBits) + (double)hi;
+static_assert(kLoBits == 21, "split_limbs scales the remainder by 2^21");
+constexpr uint32_t kLoZero = 1u << kLoBits;  // the low limb of every x below 2^-21: hi + lo 2^-21 = 0
+// the sum of n values from the sums of their high and low limbs (the high
+// sums stay below 2^60 in magnitude)
+__device__ __forceinline__ double join_limbs(int64_t hi, uint32_t lo) {
+  return __builtin_fma((double)lo, 0x1p-21, (double)hi);
 }
 
 typedef long long ll2 __attribute__((ext_vector_type(2)));
@@ -101,28 +109,20 @@ __device__ __forceinline__ int64_t row_shr64(int64_t x) {
   return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
-// One step of a wavefront-wide inclusive scan of an int: every lane adds the
-// value DPP control CTRL brings it (lanes of rows outside ROW_MASK, and lanes
-// without a source, add 0).
-template <int CTRL, int ROW_MASK>
-__device__ __forceinline__ void scan_step(int& x) {
-  x += __builtin_amdgcn_update_dpp(0, x, CTRL, ROW_MASK, 0xf, false);
-}
 
 // BK: the bucket form of the cells (RubinParams::buckets), else the tree form.
 template <bool W_BF16, int EMA, bool BK>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(5))) void rubin_reconstruct_kernel(RubinParams p) {
   static_assert(kThreads == kCellBuckets, "one bucket entry per thread");
-  // per cell: h = hh + hl 2^-50 and h w = wh + wl 2^-50 in scaled units (one
-  // array per limb, so that lanes on different cells spread over the banks),
-  // then their exclusive prefix sums; a flag for an h > 0 lost to the fixed
-  // point, then its prefix count.  Rows of kCells + 2 entries keep every row
-  // 16-byte aligned for the two-cell (128-bit) accesses of the scan.  One copy
-  // of the cells per wavefront: at 23 KB per workgroup five wavefronts per
-  // SIMD fit (a second copy for the odd lanes, which halves the atomics that
-  // meet on one address, measured slower once it set the occupancy)
+  // per cell, one row each (so that lanes on different cells spread over the
+  // banks): the high limbs of h and of h w in scaled units, both low limbs
+  // (h in the lower half), and a flag for an h > 0 lost to the fixed point;
+  // then their exclusive prefix sums.  Rows of kCells + 2 entries keep every
+  // row 16-byte aligned for the 128-bit accesses of the scan.  One copy of
+  // the cells per wavefront (a second copy for the odd lanes, which halves the
+  // atomics that meet on one address, measured slower once it set the
+  // occupancy)
   __shared__ __align__(16) int64_t s_limb[kWaves][4][kCells + 2];
-  __shared__ int s_flag[kWaves][kCells + 2];
   __shared__ float s_thr[BK ? 1 : kCells];        // tree form: thresholds in search-tree order
   __shared__ uint4 s_bucket[BK ? kCellBuckets : 1];  // bucket form: first cell, next three thresholds
   __shared__ uint8_t s_tpos[kMaxClips][9];        // cell range of code b under clip k
@@ -268,10 +268,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(5))) v
 
     // ---- cells: clear, then add every weight's limbs into its cell ------------
     int64_t(*limb)[kCells + 2] = s_limb[wave];
-    int* flag = s_flag[wave];
 #pragma unroll
     for (int j = 0; j < 4; j++) *cell_pair(limb[j], lane) = ll2{0, 0};
-    *reinterpret_cast<int2*>(flag + 2 * lane) = make_int2(0, 0);
     wave_lds_fence();
     // the cell of every weight: the number of thresholds <= u
     int pos[NE];
@@ -327,14 +325,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(5))) v
     bool lost = false;
 #pragma unroll
     for (int i = 0; i < NE; i++) {
-      int64_t x[4];
-      split_limbs(H[i], s_h, x[0], x[1]);
-      split_limbs(HW[i], s_hw, x[2], x[3]);
-#pragma unroll
-      for (int j = 0; j < 4; j++)
-        atomicAdd(reinterpret_cast<unsigned long long*>(&limb[j][pos[i]]), (unsigned long long)x[j]);
-      if (v[i] > 0.0f && x[0] == 0 && x[1] == 0) {  // rare: h below the fixed point
-        flag[pos[i]] = 1;
+      int64_t xh, xw;
+      uint32_t lh, lw;
+      split_limbs(H[i], s_h, xh, lh);
+      split_limbs(HW[i], s_hw, xw, lw);
+      atomicAdd(reinterpret_cast<unsigned long long*>(&limb[0][pos[i]]), (unsigned long long)xh);
+      atomicAdd(reinterpret_cast<unsigned long long*>(&limb[1][pos[i]]), (unsigned long long)xw);
+      atomicAdd(reinterpret_cast<unsigned long long*>(&limb[2][pos[i]]), ((unsigned long long)lw << 32) | lh);
+      if (v[i] > 0.0f && xh == -1 && lh == kLoZero) {  // rare: h below the fixed point
+        limb[3][pos[i]] = 1;
         lost = true;
       }
     }
@@ -367,20 +366,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(5))) v
       for (int t = 1; t < 4; t++) seg[t] = ll2{e + in[2 * t - 1], e + in[2 * t]};
       if (c == 15) limb[j][kCells] = x;
     }
-    if (block_lost) {  // uniform; rare: prefix counts of the flags (lane l: cells 2l, 2l + 1)
-      const int2 fl = *reinterpret_cast<const int2*>(flag + 2 * lane);
-      int x = fl.x + fl.y;
-      const int t = x;
-      scan_step<0x111, 0xf>(x);  // row_shr:1
-      scan_step<0x112, 0xf>(x);  // row_shr:2
-      scan_step<0x114, 0xf>(x);  // row_shr:4
-      scan_step<0x118, 0xf>(x);  // row_shr:8: each row of 16 is scanned
-      scan_step<0x142, 0xa>(x);  // row_bcast:15 into rows 1 and 3
-      scan_step<0x143, 0xc>(x);  // row_bcast:31 into rows 2 and 3
-      const int e = x - t;
-      *reinterpret_cast<int2*>(flag + 2 * lane) = make_int2(e, e + fl.x);
-      if (lane == 63) flag[kCells] = x;
-    }
     wave_lds_fence();
 
     // ---- clips, 8 at a time: lane (kk, b) owns codebook entry b of clip k0+kk --
@@ -390,14 +375,18 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(5))) v
       const bool live = k < K;
       const int kc = live ? k : 0;
       const int t0 = s_tpos[kc][b], t1 = s_tpos[kc][b + 1];
-      const int cnt = block_lost ? flag[t1] - flag[t0] : 0;
-      double hb = __builtin_ldexp(join_limbs(limb[0][t1] - limb[0][t0], limb[1][t1] - limb[1][t0]), -sh_exp);
-      double hwb = __builtin_ldexp(join_limbs(limb[2][t1] - limb[2][t0], limb[3][t1] - limb[3][t0]), -sw_exp);
-      // entries whose saliency fell below the fixed-point range, and in a
-      // block with weights between tie thresholds the entries of codes 3 and 4:
-      // exact fp64 sums
-      uint64_t need = __ballot(live && ((cnt > 0 && !(hb > 0.0)) || (block_unsafe && (b == 3 || b == 4))));
-      while (need) {  // uniform; rare (h spanning over 2^101 in a block, or a weight at the tie)
+      const int64_t cnt = block_lost ? limb[3][t1] - limb[3][t0] : 0;
+      const uint64_t lo = (uint64_t)(limb[2][t1] - limb[2][t0]);  // no borrow crosses: both halves grow
+      const double hbu = join_limbs(limb[0][t1] - limb[0][t0], (uint32_t)lo);
+      double hb = __builtin_ldexp(hbu, -sh_exp);
+      double hwb = __builtin_ldexp(join_limbs(limb[1][t1] - limb[1][t0], (uint32_t)(lo >> 32)), -sw_exp);
+      // entries with a saliency sum below 2^18 units (where the limbs' 2^-12
+      // units could exceed 2^-30 of it) or lost to the fixed point, and in a
+      // block with weights between tie thresholds the entries of codes 3 and
+      // 4: fp64 sums straight from the weights
+      const bool coarse = hbu < 0x1p18 && (hbu > 0.0 || cnt > 0);
+      uint64_t need = __ballot(live && (coarse || (block_unsafe && (b == 3 || b == 4))));
+      while (need) {  // uniform; rare (h spanning over 2^33 in a block, or a weight at the tie)
         const int L = __builtin_ctzll(need);
         need &= need - 1;
         const int kL = k0 + (L >> 3), bL = L & 7;

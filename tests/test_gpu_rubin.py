@@ -202,13 +202,15 @@ def _entries_below_range(W, v, clips):
 
 
 def test_rubin_saliency_beyond_fixed_point_range():
-    """Blocks whose saliency spans more than 2^101: the kernel's exact
-    fixed-point cell sums drop the smallest saliencies, and a codebook entry
-    made only of such weights is recomputed in fp64.  In every block one
-    weight has v = 1e20 and the weights above the block's 90th percentile of
-    w have v = 1e-15 (a ratio of 1e-35), so the top index of most clips holds
-    only those; codebook bytes, codes, r and scores must still match the
-    oracle's direct sums."""
+    """Blocks whose saliency spans more than 2^101: the kernel's fixed-point
+    cell sums drop the smallest saliencies (and round the others to units of
+    2^-72 or so of the block's largest), and a codebook entry whose saliency
+    sum lies below about 2^-33 of the block's largest, or made only of dropped
+    weights, is recomputed in fp64.  In every block one weight has v = 1e20
+    and the weights above the block's 90th percentile of w have v = 1e-15 (a
+    ratio of 1e-35), so the top index of most clips holds only those;
+    codebook bytes, codes, r and scores must still match the oracle's direct
+    sums."""
     torch.manual_seed(5)
     W = (torch.randn(16, 128) * 0.02).float()
     v = torch.rand(16, 128).float() + 0.5
@@ -223,6 +225,24 @@ def test_rubin_saliency_beyond_fixed_point_range():
     assert _entries_below_range(W.numpy(), v.numpy(), clips) > 0  # the case is exercised
     run_rubin("rubin.saliency-range", W.cuda(), v.cuda(), clips=clips)
     run_rubin("rubin.saliency-range.bf16", W.to(torch.bfloat16).cuda(), v.cuda(), clips=(1.0, 0.9, 0.75, 0.6))
+
+
+def test_rubin_saliency_near_recompute_threshold():
+    """Saliencies around the point where the kernel stops trusting its
+    fixed-point sums: one weight per block has v = 1 and the others v = 2^-e
+    with e uniform in [26, 42], so a codebook entry's saliency sum falls on
+    either side of about 2^-33 of the block's largest.  Entries above it are
+    served from the cell sums (whose low limbs then drop bits: a weight with
+    v = 2^-42 keeps about 12 of its 24), those below are recomputed in fp64;
+    both must match the oracle."""
+    rng = np.random.default_rng(17)
+    W = torch.from_numpy((rng.standard_normal((32, 256)) * 0.02).astype(np.float32))
+    e = rng.uniform(26.0, 42.0, size=(32, 256))
+    v = torch.from_numpy(np.exp2(-e).astype(np.float32))
+    v[0::8, 0::64] = 1.0
+    clips = tuple(synth.clip_grid(1.0, 0.3, 15))
+    run_rubin("rubin.saliency-threshold", W.cuda(), v.cuda(), clips=clips)
+    run_rubin("rubin.saliency-threshold.bf16", W.to(torch.bfloat16).cuda(), v.cuda(), clips=clips)
 
 
 def test_rubin_weights_among_tie_thresholds():
