@@ -199,9 +199,11 @@ constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
 constexpr int kDppHalfMirror = 0x141; // lane i <-> 7 - i inside each 8
 constexpr int kDppMirror = 0x140;     // lane i <-> 15 - i inside each 16
 
+// x of the lane that DPP control CTRL names, 0 where it names none (bound_ctrl:
+// no old value to set up first)
 template <int CTRL>
 __device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
-  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, CTRL, 0xF, 0xF, true);
 }
 template <int CTRL>
 __device__ __forceinline__ float dpp_f32(float x) { return as_f32(dpp_u32<CTRL>(as_u32(x))); }
@@ -239,12 +241,19 @@ __device__ __forceinline__ double run_sum(double x) {
   if constexpr (L >= 16) x = x + dpp_f64<kDppMirror>(x);
   return x;
 }
+// minimum of two keys (non-negative, never NaN: see make_key): v_min_f64
+// without the quieting of its inputs that fmin() adds
+__device__ __forceinline__ double min_key(double a, double b) {
+  double r;
+  asm("v_min_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
 template <int L>
 __device__ __forceinline__ double run_min_f64(double x) {
-  if constexpr (L >= 2) x = fmin(x, dpp_f64<kDppXor1>(x));
-  if constexpr (L >= 4) x = fmin(x, dpp_f64<kDppXor2>(x));
-  if constexpr (L >= 8) x = fmin(x, dpp_f64<kDppHalfMirror>(x));
-  if constexpr (L >= 16) x = fmin(x, dpp_f64<kDppMirror>(x));
+  if constexpr (L >= 2) x = min_key(x, dpp_f64<kDppXor1>(x));
+  if constexpr (L >= 4) x = min_key(x, dpp_f64<kDppXor2>(x));
+  if constexpr (L >= 8) x = min_key(x, dpp_f64<kDppHalfMirror>(x));
+  if constexpr (L >= 16) x = min_key(x, dpp_f64<kDppMirror>(x));
   return x;
 }
 
@@ -318,9 +327,9 @@ __device__ __forceinline__ double rows_sum(double x) {
   x = x + dpp_rows_f64<0x143, 0xC>(0.0, x);
   return lane63_f64(x);
 }
-__device__ __forceinline__ double rows_min_f64(double x) {
-  x = fmin(x, dpp_rows_f64<0x142, 0xA>(INFINITY, x));
-  x = fmin(x, dpp_rows_f64<0x143, 0xC>(INFINITY, x));
+__device__ __forceinline__ double rows_min_f64(double x) {  // of keys
+  x = min_key(x, dpp_rows_f64<0x142, 0xA>(INFINITY, x));
+  x = min_key(x, dpp_rows_f64<0x143, 0xC>(INFINITY, x));
   return lane63_f64(x);
 }
 

@@ -57,8 +57,8 @@ struct Members<L, true> {
   static __device__ __forceinline__ float min(float x) { return reduce(x, [](float a, float b) { return fminf(a, b); }); }
   static __device__ __forceinline__ float max(float x) { return reduce(x, [](float a, float b) { return fmaxf(a, b); }); }
   static __device__ __forceinline__ double sum(double x) { return reduce(x, [](double a, double b) { return a + b; }); }
-  static __device__ __forceinline__ double min_f64(double x) {
-    return reduce(x, [](double a, double b) { return fmin(a, b); });
+  static __device__ __forceinline__ double min_f64(double x) {  // of keys
+    return reduce(x, [](double a, double b) { return min_key(a, b); });
   }
 };
 

@@ -60,14 +60,6 @@ __device__ __forceinline__ float fp8_get(uint32_t d, int sel) {
   }
 }
 
-// minimum of two non-negative, non-NaN doubles (v_min_f64 without the
-// quieting of its inputs that fmin() adds)
-__device__ __forceinline__ double min_f64(double a, double b) {
-  double r;
-  asm("v_min_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
-  return r;
-}
-
 template <bool W_BF16, int EMA, int KC, bool MULTI>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu((KC > 8 || MULTI) ? 3 : 4)))
 void nvfp4_reconstruct_kernel(Nvfp4Params p) {
@@ -247,7 +239,7 @@ void nvfp4_reconstruct_kernel(Nvfp4Params p) {
         const double score = __builtin_fma(sb, __builtin_fma(sb, Sqq, -2.0 * Sqw), Sww);
         // keys order like the scores and keep the lowest index among equal
         // ones; padding clips repeat clip K-1 with a larger index
-        best_key = min_f64(best_key, make_key(score, k));
+        best_key = min_key(best_key, make_key(score, k));
       }
     }
     // the winner's E4M3 byte, if it is a clip of this pass

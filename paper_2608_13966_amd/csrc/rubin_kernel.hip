@@ -423,7 +423,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(5))) v
       // score: sum_b (C_b^2 H_b - 2 C_b HW_b) + sum h w^2, over the 8 lanes of the clip
       const double score = sww + run_sum<8>(cv * (cv * hb - 2.0 * hwb));
       double key = live ? make_key(score, k) : __longlong_as_double(0x7ff0000000000000ll);
-      const double kmin = rows_min_f64(run_min_f64<16>(key));
+      // the 8 lanes of a clip hold one key (bit-identical sums): the two
+      // clips of a row meet with one mirror step, then the rows combine
+      const double kmin = rows_min_f64(min_key(key, dpp_f64<kDppMirror>(key)));
       if (kmin < best_key) {  // uniform
         best_key = kmin;
         if (k == key_index(kmin)) {  // the 8 lanes of the winning clip
