@@ -185,7 +185,8 @@ def _f32_fma(a, b, c):
 
 def _entries_below_range(W, v, clips):
     """Number of (block, clip, index) whose weights all have a saliency below
-    2^-101 of their block's largest (and at least one such weight)."""
+    2^-101 of their block's largest (and at least one such weight): far below
+    both the fixed point's range and the recompute threshold."""
     n = 0
     for blk_w, blk_v in zip(_blocks(W, *W.shape), _blocks(v, *v.shape)):
         mn, mx = blk_w.min(), blk_w.max()
