@@ -214,23 +214,38 @@ __device__ __forceinline__ double dpp_f64(double x) {
   return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
+// min / max of two floats as one v_min_f32 / v_max_f32: fminf and fmaxf
+// first quiet their inputs (one more instruction for each value that comes
+// from another lane).  Equal for non-NaN inputs; NaN inputs give unspecified
+// results, as everywhere in the library.
+__device__ __forceinline__ float min_f32(float a, float b) {
+  float r;
+  asm("v_min_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+__device__ __forceinline__ float max_f32(float a, float b) {
+  float r;
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
 // All-reduce over aligned runs of L consecutive lanes (L in 1, 2, 4, 8, 16).
 // The patterns pair lanes symmetrically, and IEEE addition / min / max are
 // commutative, so every lane of a run ends with a bit-identical result.
 template <int L>
 __device__ __forceinline__ float run_min(float x) {
-  if constexpr (L >= 2) x = fminf(x, dpp_f32<kDppXor1>(x));
-  if constexpr (L >= 4) x = fminf(x, dpp_f32<kDppXor2>(x));
-  if constexpr (L >= 8) x = fminf(x, dpp_f32<kDppHalfMirror>(x));
-  if constexpr (L >= 16) x = fminf(x, dpp_f32<kDppMirror>(x));
+  if constexpr (L >= 2) x = min_f32(x, dpp_f32<kDppXor1>(x));
+  if constexpr (L >= 4) x = min_f32(x, dpp_f32<kDppXor2>(x));
+  if constexpr (L >= 8) x = min_f32(x, dpp_f32<kDppHalfMirror>(x));
+  if constexpr (L >= 16) x = min_f32(x, dpp_f32<kDppMirror>(x));
   return x;
 }
 template <int L>
 __device__ __forceinline__ float run_max(float x) {
-  if constexpr (L >= 2) x = fmaxf(x, dpp_f32<kDppXor1>(x));
-  if constexpr (L >= 4) x = fmaxf(x, dpp_f32<kDppXor2>(x));
-  if constexpr (L >= 8) x = fmaxf(x, dpp_f32<kDppHalfMirror>(x));
-  if constexpr (L >= 16) x = fmaxf(x, dpp_f32<kDppMirror>(x));
+  if constexpr (L >= 2) x = max_f32(x, dpp_f32<kDppXor1>(x));
+  if constexpr (L >= 4) x = max_f32(x, dpp_f32<kDppXor2>(x));
+  if constexpr (L >= 8) x = max_f32(x, dpp_f32<kDppHalfMirror>(x));
+  if constexpr (L >= 16) x = max_f32(x, dpp_f32<kDppMirror>(x));
   return x;
 }
 template <int L>
@@ -300,13 +315,13 @@ __device__ __forceinline__ uint32_t dpp_rows(uint32_t id, uint32_t x) {
   return (uint32_t)__builtin_amdgcn_update_dpp((int)id, (int)x, CTRL, ROW_MASK, 0xF, false);
 }
 __device__ __forceinline__ float rows_min(float x) {
-  x = fminf(x, as_f32(dpp_rows<0x142, 0xA>(as_u32(INFINITY), as_u32(x))));
-  x = fminf(x, as_f32(dpp_rows<0x143, 0xC>(as_u32(INFINITY), as_u32(x))));
+  x = min_f32(x, as_f32(dpp_rows<0x142, 0xA>(as_u32(INFINITY), as_u32(x))));
+  x = min_f32(x, as_f32(dpp_rows<0x143, 0xC>(as_u32(INFINITY), as_u32(x))));
   return as_f32((uint32_t)__builtin_amdgcn_readlane((int)as_u32(x), 63));
 }
 __device__ __forceinline__ float rows_max(float x) {
-  x = fmaxf(x, as_f32(dpp_rows<0x142, 0xA>(as_u32(-INFINITY), as_u32(x))));
-  x = fmaxf(x, as_f32(dpp_rows<0x143, 0xC>(as_u32(-INFINITY), as_u32(x))));
+  x = max_f32(x, as_f32(dpp_rows<0x142, 0xA>(as_u32(-INFINITY), as_u32(x))));
+  x = max_f32(x, as_f32(dpp_rows<0x143, 0xC>(as_u32(-INFINITY), as_u32(x))));
   return as_f32((uint32_t)__builtin_amdgcn_readlane((int)as_u32(x), 63));
 }
 template <int CTRL, int ROW_MASK>

@@ -54,8 +54,8 @@ struct Members<L, true> {
     if constexpr (L == 8) x = pair_rows<32>(x, op);
     return x;
   }
-  static __device__ __forceinline__ float min(float x) { return reduce(x, [](float a, float b) { return fminf(a, b); }); }
-  static __device__ __forceinline__ float max(float x) { return reduce(x, [](float a, float b) { return fmaxf(a, b); }); }
+  static __device__ __forceinline__ float min(float x) { return reduce(x, [](float a, float b) { return min_f32(a, b); }); }
+  static __device__ __forceinline__ float max(float x) { return reduce(x, [](float a, float b) { return max_f32(a, b); }); }
   static __device__ __forceinline__ double sum(double x) { return reduce(x, [](double a, double b) { return a + b; }); }
   static __device__ __forceinline__ double min_f64(double x) {  // of keys
     return reduce(x, [](double a, double b) { return min_key(a, b); });

@@ -233,18 +233,22 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(5))) v
   mn = rows_min(run_min<16>(mn));
   mx = rows_max(run_max<16>(mx));
   double H[NE], HW[NE];
-  double sww = 0.0, sh = 0.0;
+  double sww = 0.0;
 #pragma unroll
   for (int i = 0; i < NE; i++) {
     H[i] = (double)v[i];
     HW[i] = H[i] * (double)w[i];  // exact: 24 x 24 significant bits
     sww = __builtin_fma(HW[i], (double)w[i], sww);
-    sh += H[i];
   }
   sww = rows_sum(run_sum<16>(sww));
-  sh = rows_sum(run_sum<16>(sh));
 
   const bool constant = (mx == mn);
+  double sh = 0.0;  // sum h, for a constant block's error only
+  if (constant) {   // uniform
+#pragma unroll
+    for (int i = 0; i < NE; i++) sh += H[i];
+    sh = rows_sum(run_sum<16>(sh));
+  }
   const float c = 0.5f * (mx + mn);
   const float rho = 0.5f * (mx - mn);
   const float rrho = 1.0f / rho;
