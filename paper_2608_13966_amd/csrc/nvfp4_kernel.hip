@@ -226,7 +226,12 @@ void nvfp4_reconstruct_kernel(Nvfp4Params p) {
         const float xrd = __builtin_amdgcn_rcpf(xd);
         const float xq = xn * xrd;
         const float xr = __builtin_fmaf(__builtin_fmaf(-xd, xq, xn), xrd, xq);
-        xc[t] = __builtin_amdgcn_fmed3f((Sqq == 0.0) ? fs[kk + t] * mx : xr, 0.0f, 448.0f);
+        // xr is formed for every clip and the zero case picked by a select:
+        // as a branch (the compiler's choice for the reciprocal) it cost
+        // exec-mask work per clip and kept 27 more registers live
+        float xv = xr;
+        asm volatile("" : "+v"(xv));
+        xc[t] = __builtin_amdgcn_fmed3f((Sqq == 0.0) ? fs[kk + t] * mx : xv, 0.0f, 448.0f);
       }
       // nearest E4M3FN (RNE) of both
       eb[kk / 4] = fp8_put(kk % 4 == 0 ? __float_as_uint(xc[0]) : eb[kk / 4], xc[0], xc[1], (kk / 2) & 1);
