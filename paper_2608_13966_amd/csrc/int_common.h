@@ -282,20 +282,24 @@ __device__ __forceinline__ void int_fit_bounds(IntMoments& mo) {
 template <bool SYM, int QMAX>
 __device__ __forceinline__ bool int_fit_ill(const IntMoments& mo, double A0, double A1, double A2) {
   constexpr double Q = (double)QMAX;
+  // every test is evaluated and combined bitwise: short-circuit forms
+  // compile to a branch per test and clip
   if constexpr (SYM) {
     const double e1 = mo.qh * Q * Q + mo.rel * A1, e2 = mo.qhw * Q + mo.rel * mo.wabs * Q * mo.Sv;
-    return A1 > 0.0 && (e1 > kFitTol * A1 || e2 > kFitTol * fabs(A2));
+    return (A1 > 0.0) & ((e1 > kFitTol * A1) | (e2 > kFitTol * fabs(A2)));
   } else {
     const double Sv = mo.Sv;
-    if (Sv == 0.0) return false;  // every candidate keeps its RTN dequantiser and scores 0
     const double p1 = Sv * A1, p2 = A0 * A0;
     const double D = p1 - p2;
     const double eD = __builtin_fma(mo.rel, p1 + p2, mo.eD0);
-    if (D + eD <= mo.thr) return false;  // certainly rank-deficient
-    if (D - eD <= mo.thr) return true;   // either side of the threshold
     const double num = Sv * A2 - A0 * mo.Svw;
     const double eN = __builtin_fma(mo.eN1, A0, mo.eN0);
-    return eD > kFitTol * D || eN > kFitTol * fabs(num);
+    // Sv = 0: every candidate keeps its RTN dequantiser and scores 0.  D + eD
+    // <= thr: certainly rank-deficient.  D - eD <= thr: either side of the
+    // threshold.  Otherwise the bounds against their values.
+    const bool deficient = D + eD <= mo.thr, straddles = D - eD <= mo.thr;
+    const bool loose = (eD > kFitTol * D) | (eN > kFitTol * fabs(num));
+    return (Sv != 0.0) & !deficient & (straddles | loose);
   }
 }
 
