@@ -246,6 +246,26 @@ def test_rubin_saliency_near_recompute_threshold():
     run_rubin("rubin.saliency-threshold.bf16", W.to(torch.bfloat16).cuda(), v.cuda(), clips=clips)
 
 
+def test_rubin_weights_in_split_cells():
+    """Blocks whose weights sit almost all within 0.085 of the block's centre
+    (in units of its half-range), where every clip of the paper's grid has
+    only its tie threshold at 0 and the host adds its extra cell boundaries:
+    each of those boundaries then has many weights on both sides.  The codes
+    do not change at an extra boundary, so the kernel must still match the
+    oracle on every block, in both cell forms."""
+    rng = np.random.default_rng(23)
+    W = (rng.uniform(-0.085, 0.085, size=(16, 256)) * 0.1).astype(np.float32)
+    for rb in range(2):
+        for cb in range(4):
+            W[8 * rb, 64 * cb] = -0.1  # the block's range: u = w / 0.1
+            W[8 * rb + 1, 64 * cb] = 0.1
+    W = torch.from_numpy(W)
+    v = torch.from_numpy(rng.uniform(0.1, 1.0, size=(16, 256)).astype(np.float32))
+    clips = tuple(synth.clip_grid(1.0, 0.3, 15))
+    run_rubin("rubin.split-cells", W.cuda(), v.cuda(), clips=clips)
+    run_rubin("rubin.split-cells.bf16", W.to(torch.bfloat16).cuda(), v.cuda(), clips=clips)
+
+
 def test_rubin_weights_among_tie_thresholds():
     """Weights whose normalised position lies between the clips' tie
     thresholds T(k, 3) (just below u = 0, where the fp32 code rounding ties at
