@@ -262,34 +262,41 @@ int cell_bucket(float u);
 int rubin_split_cells(float* s, int m, int m_max, int* cnt, int cmax, float ulo, float uhi) {
   constexpr double kSigma = 0.3, kTarget = 0.012;
   auto cdf = [&](double x) { return 0.5 * std::erfc(-x / (kSigma * std::sqrt(2.0))); };
-  bool frozen[quasar::kRubinThresholds + 1] = {};  // cells found not to split
+  // cell i = [s[i - 1], s[i]), the ends taken at -1 and 1; its model mass, or
+  // -1 for an empty cell and for one found not to split
+  auto lo = [&](int i) { return i == 0 ? -1.0f : s[i - 1]; };
+  auto hi = [&](int i, int n) { return i == n ? 1.0f : s[i]; };
+  auto mass_of = [&](int i, int n) {
+    const double a = lo(i), b = hi(i, n);
+    return b > a ? cdf(b) - cdf(a) : -1.0;
+  };
+  double mass[quasar::kRubinThresholds + 1];
+  for (int i = 0; i <= m; i++) mass[i] = mass_of(i, m);
   while (m < m_max) {
     int best = -1;
     double best_mass = kTarget;
-    for (int i = 0; i <= m; i++) {  // cell i = [s[i - 1], s[i]), the ends taken at -1 and 1
-      const double a = i == 0 ? -1.0 : s[i - 1], b = i == m ? 1.0 : s[i];
-      if (frozen[i] || !(b > a)) continue;
-      const double mass = cdf(b) - cdf(a);
-      if (mass > best_mass) {
-        best_mass = mass;
+    for (int i = 0; i <= m; i++) {
+      if (mass[i] > best_mass) {
+        best_mass = mass[i];
         best = i;
       }
     }
     if (best < 0) break;
-    const float a = best == 0 ? -1.0f : s[best - 1], b = best == m ? 1.0f : s[best];
+    const float a = lo(best), b = hi(best, m);
     const float mid = 0.5f * (a + b);
     bool ok = mid > a && mid < b && !(mid >= ulo && mid <= uhi);
     if (ok && cnt != nullptr) ok = cnt[cell_bucket(mid)] < cmax;
     if (!ok) {
-      frozen[best] = true;
+      mass[best] = -1.0;
       continue;
     }
     if (cnt != nullptr) cnt[cell_bucket(mid)]++;
     for (int j = m; j > best; j--) s[j] = s[j - 1];
     s[best] = mid;
-    for (int j = m + 1; j > best + 1; j--) frozen[j] = frozen[j - 1];
-    frozen[best] = frozen[best + 1] = false;
+    for (int j = m + 1; j > best + 1; j--) mass[j] = mass[j - 1];
     m++;
+    mass[best] = mass_of(best, m);
+    mass[best + 1] = mass_of(best + 1, m);
   }
   return m;
 }
